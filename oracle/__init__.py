@@ -1,0 +1,26 @@
+"""CPU oracle for expert-map matching and prefetch-set selection.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path may import, call or
+execute this package: only the test suite, the smoke check and the CPU
+baseline leg of the benchmark use it.  It shares no code with the HIP path
+(no kernels, headers, helpers or constant tables) and imports nothing from it.
+
+It is a plain, slow, obviously correct restatement of what the paper defines:
+
+* ``finemoe``  NumPy float64 implementation of semantic and trajectory cosine
+  search (Eq. 4, Eq. 5), ranking by highest score, the optional
+  similarity-weighted blend, the similarity-aware threshold of Section 4.3 and
+  the minimum-cardinality prefetch set of Eq. 6-8.
+* ``brute``    pure-Python brute force with correctly rounded sums
+  (``math.fsum``) and full subset enumeration, used to pin ``finemoe`` on
+  tiny inputs.
+
+Every function is pinned by the ``-m "not gpu"`` tests against closed forms,
+invariants and brute force; none is "parity unpinned".
+"""
+from . import finemoe, brute  # noqa: F401
+from .finemoe import (  # noqa: F401
+    widen, cosine, trajectory_scores, semantic_scores, rank, match_trajectory,
+    match_semantic, threshold, select_row, blend_rows, select_prefetch,
+    TAU_FIXED, TAU_DYNAMIC, BLEND_NONE, BLEND_SCORE,
+)

@@ -1,0 +1,255 @@
+"""NumPy float64 oracle of FineMoE's expert-map search and prefetch selection.
+
+Test infrastructure only (see the package docstring).  Inputs are the arrays
+the synthetic generator draws: float32 arrays, or bf16 values carried as
+uint16 bit patterns.  Both widen to float64 exactly, and every sum below is
+taken in float64.
+
+Conventions where the paper leaves a choice open (each is listed, with its
+reason, in the design notes of the repository):
+
+* equal scores: the lower store index ranks first; NaN scores rank last;
+* a zero-norm vector has cosine 0 with everything;
+* equal probabilities: the lower expert index is picked first;
+* the threshold test is ``>=`` (Eq. 7); if no prefix reaches it, all experts
+  are taken before the cap;
+* a store with fewer than k entries fills the rest with index -1 and score
+  -inf, and a query whose best index is -1 selects nothing.
+"""
+from __future__ import annotations
+
+import math
+from typing import Tuple
+
+import numpy as np
+
+TAU_FIXED = 0
+TAU_DYNAMIC = 1
+BLEND_NONE = 0
+BLEND_SCORE = 1
+
+_CHUNK = 16384
+
+
+# ---------------------------------------------------------------- inputs
+
+def widen(arr: np.ndarray, dtype: str) -> np.ndarray:
+    """Exact float64 values of a float32 array or of bf16 bit patterns."""
+    if dtype == "bf16":
+        a = np.ascontiguousarray(arr, dtype=np.uint16)
+        return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    if dtype == "f32":
+        return np.asarray(arr, dtype=np.float32).astype(np.float64)
+    raise ValueError(dtype)
+
+
+# ---------------------------------------------------------------- cosine (Eq. 4, Eq. 5)
+
+def cosine(u: np.ndarray, v: np.ndarray) -> float:
+    """Cosine similarity u.v / (|u| |v|) in float64; 0 if either norm is 0."""
+    u = np.asarray(u, dtype=np.float64).ravel()
+    v = np.asarray(v, dtype=np.float64).ravel()
+    nu = math.sqrt(float(np.dot(u, u)))
+    nv = math.sqrt(float(np.dot(v, v)))
+    dot = float(np.dot(u, v))
+    if math.isnan(dot) or math.isnan(nu) or math.isnan(nv):
+        return math.nan
+    if nu == 0.0 or nv == 0.0:
+        return 0.0
+    return dot / (nu * nv)
+
+
+def _cosine_many(V: np.ndarray, u: np.ndarray) -> np.ndarray:
+    """Cosine of every row of V with u (float64), same conventions as cosine()."""
+    dots = V @ u
+    nv = np.sqrt(np.einsum("ij,ij->i", V, V))
+    nu = math.sqrt(float(np.dot(u, u)))
+    with np.errstate(invalid="ignore", divide="ignore"):
+        s = dots / (nv * nu)
+    zero = (nv == 0.0) | (nu == 0.0)
+    s[zero & ~np.isnan(dots) & ~np.isnan(nv)] = 0.0
+    if math.isnan(nu):
+        s[:] = np.nan
+    return s
+
+
+def trajectory_scores(maps64: np.ndarray, q64: np.ndarray, p: int) -> np.ndarray:
+    """Eq. 5: cosine between the observed trajectory of the first ``p`` layers of
+    query ``q64`` [L][E] and the same ``p`` layers of every stored map
+    ``maps64`` [n][L][E], both flattened over (layer, expert)."""
+    n, L, E = maps64.shape
+    V = maps64[:, :p, :].reshape(n, p * E)
+    u = q64[:p, :].reshape(p * E)
+    return _cosine_many(V, u)
+
+
+def semantic_scores(embs64: np.ndarray, qs64: np.ndarray) -> np.ndarray:
+    """Eq. 4: cosine between a query embedding [d] and every stored embedding [n][d]."""
+    return _cosine_many(embs64, qs64)
+
+
+# ---------------------------------------------------------------- ranking
+
+def rank(scores: np.ndarray, k: int, idx: np.ndarray = None) -> Tuple[np.ndarray, np.ndarray]:
+    """The k best entries by (score descending, index ascending), NaN last.
+
+    ``idx`` gives the store index of each score (default 0..n-1).  Missing
+    entries (fewer than k scores) are returned as index -1, score -inf.
+    """
+    s = np.asarray(scores, dtype=np.float64)
+    if idx is None:
+        idx = np.arange(s.shape[0], dtype=np.int64)
+    idx = np.asarray(idx, dtype=np.int64)
+    nan = np.isnan(s)
+    order = np.lexsort((idx, -np.where(nan, 0.0, s), nan))
+    top = order[:k]
+    out_i = np.full(k, -1, dtype=np.int64)
+    out_s = np.full(k, -np.inf, dtype=np.float64)
+    out_i[:top.size] = idx[top]
+    out_s[:top.size] = s[top]
+    return out_i, out_s
+
+
+def _merge(best_i, best_s, new_i, new_s, k):
+    keep = best_i >= 0
+    return rank(np.concatenate([best_s[keep], new_s]), k, np.concatenate([best_i[keep], new_i]))
+
+
+def match_trajectory(maps: np.ndarray, dtype: str, Q: np.ndarray, depth: np.ndarray, k: int,
+                     n: int = None) -> Tuple[np.ndarray, np.ndarray]:
+    """Trajectory search (Section 4.2.2): for each query b, the k stored maps with
+    the highest Eq. 5 score over the first depth[b] layers (clamped to [1, L]).
+
+    maps [n][L][E], Q [B][L][E] (dtype "f32" or "bf16"), depth [B].
+    Returns idx [B][k] (int64, -1 if missing) and score [B][k] (float64).
+    """
+    n = maps.shape[0] if n is None else n
+    B, L, E = Q.shape
+    depth = np.clip(np.asarray(depth, dtype=np.int64), 1, L)
+    Q64 = widen(Q, dtype)
+    out_i = np.full((B, k), -1, dtype=np.int64)
+    out_s = np.full((B, k), -np.inf, dtype=np.float64)
+    for a in range(0, n, _CHUNK):
+        b = min(a + _CHUNK, n)
+        M = widen(maps[a:b], dtype)
+        ids = np.arange(a, b, dtype=np.int64)
+        for q in range(B):
+            s = trajectory_scores(M, Q64[q], int(depth[q]))
+            out_i[q], out_s[q] = _merge(out_i[q], out_s[q], ids, s, k)
+    return out_i, out_s
+
+
+def match_semantic(embs: np.ndarray, Qs: np.ndarray, k: int, n: int = None) -> Tuple[np.ndarray, np.ndarray]:
+    """Semantic search (Section 4.2.1): for each query embedding, the k stored
+    embeddings with the highest Eq. 4 score.  embs [n][d], Qs [B][d], bf16 bits."""
+    n = embs.shape[0] if n is None else n
+    B = Qs.shape[0]
+    Q64 = widen(Qs, "bf16")
+    out_i = np.full((B, k), -1, dtype=np.int64)
+    out_s = np.full((B, k), -np.inf, dtype=np.float64)
+    for a in range(0, n, _CHUNK):
+        b = min(a + _CHUNK, n)
+        X = widen(embs[a:b], "bf16")
+        ids = np.arange(a, b, dtype=np.int64)
+        for q in range(B):
+            s = semantic_scores(X, Q64[q])
+            out_i[q], out_s[q] = _merge(out_i[q], out_s[q], ids, s, k)
+    return out_i, out_s
+
+
+# ---------------------------------------------------------------- threshold and selection (Section 4.3)
+
+def threshold(mode: int, tau: float, score: float) -> float:
+    """The probability mass a prefetch set must reach.
+
+    FIXED: the given tau (a float32 parameter, widened exactly).
+    DYNAMIC: delta = Clip(1 - score, 0, 1) of Section 4.3; a NaN score gives 1.
+    """
+    if mode == TAU_FIXED:
+        return float(np.float32(tau))
+    if mode == TAU_DYNAMIC:
+        s = float(score)
+        if math.isnan(s):
+            return 1.0
+        return max(0.0, min(1.0 - s, 1.0))
+    raise ValueError(mode)
+
+
+def select_row(p: np.ndarray, tau: float, k_min: int, k_max: int) -> Tuple[int, int, np.ndarray]:
+    """Eq. 6-8 on one layer's probabilities ``p`` [E] (float64 values).
+
+    Experts are taken in order of probability (highest first, lower index
+    first on equal values, NaN last); k* is the smallest k whose running sum of
+    the first k taken reaches tau (k* = E if none does); the set is the first
+    min(max(k*, k_min), k_max) of that order.
+    Returns (mask with bit j = expert j, count, order).
+    """
+    p = np.asarray(p, dtype=np.float64)
+    E = p.shape[0]
+    nan = np.isnan(p)
+    order = np.lexsort((np.arange(E), -np.where(nan, 0.0, p), nan))
+    kstar = E
+    c = 0.0
+    for k in range(E + 1):
+        if c >= tau:
+            kstar = k
+            break
+        if k < E:
+            c = c + float(p[order[k]])
+    kk = min(max(kstar, k_min), k_max)
+    mask = 0
+    for i in range(kk):
+        mask |= 1 << int(order[i])
+    return mask, kk, order
+
+
+def blend_rows(rows: np.ndarray, scores: np.ndarray) -> np.ndarray:
+    """Similarity-weighted mean of k rows: sum_i w_i row_i / sum_i w_i with
+    w_i = max(score_i, 0), summed in order i = 0..k-1; if every weight is 0
+    the plain mean is used."""
+    rows = np.asarray(rows, dtype=np.float64)
+    w = [max(float(s), 0.0) for s in scores]
+    if sum(w) == 0.0:
+        w = [1.0] * len(w)
+    num = np.zeros(rows.shape[1], dtype=np.float64)
+    den = 0.0
+    for i in range(rows.shape[0]):
+        num = num + w[i] * rows[i]
+        den = den + w[i]
+    return num / den
+
+
+def select_prefetch(maps: np.ndarray, dtype: str, idx: np.ndarray, score: np.ndarray,
+                    lb: np.ndarray, le: np.ndarray, mode: int, tau: float, k_min: int, k_max: int,
+                    blend: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Prefetch sets for each query b and layer l in [lb[b], le[b]).
+
+    The guiding row is layer l of the best match idx[b][0] (BLEND_NONE), or
+    the similarity-weighted mean of layer l over the valid matches in idx[b]
+    (BLEND_SCORE).  The threshold comes from ``threshold`` with the best
+    match's score.  Layers outside the range, and queries without a match,
+    get an empty set.  Returns mask [B][L] uint64 and count [B][L] uint8.
+    """
+    n, L, E = maps.shape
+    idx = np.asarray(idx, dtype=np.int64)
+    score = np.asarray(score, dtype=np.float64)
+    B = idx.shape[0]
+    mask = np.zeros((B, L), dtype=np.uint64)
+    count = np.zeros((B, L), dtype=np.uint8)
+    for b in range(B):
+        if idx[b, 0] < 0:
+            continue
+        t = threshold(mode, tau, score[b, 0])
+        valid = [i for i in range(idx.shape[1]) if idx[b, i] >= 0]
+        lo = max(0, int(lb[b]))
+        hi = min(L, int(le[b]))
+        for l in range(lo, hi):
+            if blend == BLEND_SCORE:
+                rows = np.stack([widen(maps[idx[b, i], l], dtype) for i in valid])
+                p = blend_rows(rows, [score[b, i] for i in valid])
+            else:
+                p = widen(maps[idx[b, 0], l], dtype)
+            m, c, _ = select_row(p, t, k_min, k_max)
+            mask[b, l] = np.uint64(m)
+            count[b, l] = c
+    return mask, count

@@ -1,0 +1,284 @@
+"""Checks that pin the CPU oracle to facts fixed outside of it.
+
+Each check reaches the oracle through ``oracle.finemoe`` attribute lookups at
+call time, so the mutant tests can swap a function for a deliberately wrong
+one (on the CPU) and confirm that at least one check fails.
+"""
+import json
+import math
+import os
+
+import numpy as np
+
+import oracle.brute as brute
+import oracle.finemoe as F
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def _rand_maps(rng, n, L, E, zero_frac=0.0):
+    z = rng.standard_normal((n, L, E))
+    p = np.exp(z)
+    if zero_frac:
+        p[rng.random(p.shape) < zero_frac] = 0.0
+        p[..., 0] += 1e-3
+    p /= p.sum(-1, keepdims=True)
+    return p.astype(np.float32)
+
+
+# ------------------------------------------------------------------ cosine / trajectory / semantic
+
+def check_cosine_vs_fsum(seed=0):
+    rng = np.random.default_rng(seed)
+    for _ in range(50):
+        d = int(rng.integers(1, 40))
+        u = rng.standard_normal(d)
+        v = rng.standard_normal(d)
+        if rng.random() < 0.3:
+            v = np.abs(v)
+        ref = brute.cosine_fsum(list(u), list(v))
+        got = F.cosine(u, v)
+        assert abs(got - ref) <= 1e-14, (got, ref)
+        got_many = F._cosine_many(v[None, :], u)[0]
+        assert abs(got_many - ref) <= 1e-14, (got_many, ref)
+    assert F.cosine(np.zeros(5), np.ones(5)) == 0.0
+    assert F.cosine(np.ones(5), np.zeros(5)) == 0.0
+
+
+def check_cosine_vs_torch(seed=1):
+    import torch
+    rng = np.random.default_rng(seed)
+    V = rng.standard_normal((64, 33))
+    u = rng.standard_normal(33)
+    ref = torch.nn.functional.cosine_similarity(
+        torch.from_numpy(V), torch.from_numpy(u)[None, :].expand(64, 33), dim=1, eps=0.0).numpy()
+    got = F._cosine_many(V, u)
+    assert np.max(np.abs(got - ref)) <= 1e-14
+
+
+def check_self_match(seed=2):
+    rng = np.random.default_rng(seed)
+    maps = _rand_maps(rng, 40, 6, 5)
+    m64 = F.widen(maps, "f32")
+    for y in (0, 17, 39):
+        for p in (1, 3, 6):
+            s = F.trajectory_scores(m64, m64[y], p)
+            assert abs(s[y] - 1.0) <= 1e-15, s[y]
+            assert np.all(s <= 1.0 + 1e-15)
+            i, sc = F.match_trajectory(maps, "f32", maps[y:y + 1], np.array([p]), 1)
+            assert i[0, 0] == y and abs(sc[0, 0] - 1.0) <= 1e-15
+
+
+def check_disjoint_support():
+    L, E = 3, 6
+    store = np.zeros((2, L, E), dtype=np.float32)
+    store[0, :, 3:] = 1.0 / 3
+    store[1, :, :3] = 1.0 / 3
+    q = np.zeros((L, E), dtype=np.float32)
+    q[:, :3] = [0.5, 0.25, 0.25]
+    s = F.trajectory_scores(F.widen(store, "f32"), F.widen(q, "f32"), L)
+    assert s[0] == 0.0
+    assert s[1] > 0.9
+
+
+def check_depth_special_cases(seed=3):
+    rng = np.random.default_rng(seed)
+    n, L, E = 30, 5, 4
+    maps = F.widen(_rand_maps(rng, n, L, E), "f32")
+    q = F.widen(_rand_maps(rng, 1, L, E)[0], "f32")
+    full = F.trajectory_scores(maps, q, L)
+    one = F.trajectory_scores(maps, q, 1)
+    for y in range(n):
+        ref_full = brute.cosine_fsum(list(q.ravel()), list(maps[y].ravel()))
+        ref_one = brute.cosine_fsum(list(q[0]), list(maps[y, 0]))
+        assert abs(full[y] - ref_full) <= 1e-14
+        assert abs(one[y] - ref_one) <= 1e-14
+    for p in range(1, L + 1):
+        s = F.trajectory_scores(maps, q, p)
+        for y in range(0, n, 7):
+            ref = brute.cosine_fsum(list(q[:p].ravel()), list(maps[y, :p].ravel()))
+            assert abs(s[y] - ref) <= 1e-14
+
+
+def check_unobserved_layers_ignored(seed=4):
+    rng = np.random.default_rng(seed)
+    n, L, E = 25, 6, 4
+    maps = _rand_maps(rng, n, L, E)
+    Q = _rand_maps(rng, 3, L, E)
+    depth = np.array([1, 3, 5])
+    i0, s0 = F.match_trajectory(maps, "f32", Q, depth, 3)
+    Q2 = Q.copy()
+    for b, p in enumerate(depth):
+        Q2[b, p:] = np.nan
+    i1, s1 = F.match_trajectory(maps, "f32", Q2, depth, 3)
+    assert np.array_equal(i0, i1) and np.array_equal(s0, s1)
+
+
+def check_semantic_vs_fsum(seed=5):
+    rng = np.random.default_rng(seed)
+    import synth
+    X = synth.bf16_bits(rng.standard_normal((20, 16)).astype(np.float32))
+    Qs = synth.bf16_bits(rng.standard_normal((3, 16)).astype(np.float32))
+    idx, sc = F.match_semantic(X, Qs, 2)
+    X64 = F.widen(X, "bf16")
+    Q64 = F.widen(Qs, "bf16")
+    for b in range(3):
+        ref = [brute.cosine_fsum(list(Q64[b]), list(X64[y])) for y in range(20)]
+        best = brute.best_matches(ref, 2)
+        assert list(idx[b]) == best
+        for j in range(2):
+            assert abs(sc[b, j] - ref[best[j]]) <= 1e-14
+
+
+def check_match_vs_bruteforce(seed=6):
+    rng = np.random.default_rng(seed)
+    n, L, E = 60, 4, 4
+    maps = _rand_maps(rng, n, L, E)
+    maps[40] = maps[12]           # exact duplicate: the lower index must win
+    maps[41] = maps[12]
+    Q = _rand_maps(rng, 4, L, E)
+    Q[0] = maps[12]
+    depth = np.array([4, 1, 2, 3])
+    idx, sc = F.match_trajectory(maps, "f32", Q, depth, 4)
+    m64 = F.widen(maps, "f32")
+    q64 = F.widen(Q, "f32")
+    for b in range(4):
+        p = depth[b]
+        ref = [brute.cosine_fsum(list(q64[b, :p].ravel()), list(m64[y, :p].ravel())) for y in range(n)]
+        best = brute.best_matches(ref, 4)
+        assert list(idx[b]) == best, (b, list(idx[b]), best)
+        for j in range(4):
+            assert abs(sc[b, j] - ref[best[j]]) <= 1e-14
+    assert list(idx[0, :3]) == [12, 40, 41]
+
+
+def check_rank_rules():
+    s = np.array([0.5, 0.9, np.nan, 0.9, 0.1, 0.9])
+    i, v = F.rank(s, 6)
+    assert list(i) == [1, 3, 5, 0, 4, 2]
+    i, v = F.rank(s, 8)
+    assert list(i[6:]) == [-1, -1] and np.all(np.isneginf(v[6:]))
+    i, v = F.rank(np.zeros(0), 2)
+    assert list(i) == [-1, -1]
+    rng = np.random.default_rng(7)
+    for _ in range(20):
+        n = int(rng.integers(1, 256))
+        s = np.round(rng.random(n), 2)          # many exact ties
+        k = int(rng.integers(1, 9))
+        i, v = F.rank(s, k)
+        assert list(i) == brute.best_matches(list(s), k)
+
+
+# ------------------------------------------------------------------ selection
+
+def check_uniform_golden():
+    g = golden("uniform4.json")
+    p = np.array(g["p"])
+    for case in g["cases"]:
+        m, c, _ = F.select_row(p, case["tau"], 0, 4)
+        assert c == case["kstar"], (case, c)
+        assert m == (1 << c) - 1, (case, m)
+
+
+def check_delta_golden():
+    g = golden("delta.json")
+    for case in g["cases"]:
+        t = F.threshold(F.TAU_DYNAMIC, 0.0, case["score"])
+        assert abs(t - case["delta"]) <= 1e-15, (case, t)
+    assert F.threshold(F.TAU_FIXED, 0.8, 0.3) == float(np.float32(0.8))
+
+
+def check_select_vs_enumeration(seed=8):
+    rng = np.random.default_rng(seed)
+    for _ in range(300):
+        E = int(rng.integers(1, 11))
+        p = rng.dirichlet(np.full(E, float(rng.choice([0.3, 1.0, 5.0]))))
+        if rng.random() < 0.3:
+            p = np.round(p * 8) / 8           # ties and exact dyadic sums
+        tau = float(rng.choice([0.0, 0.1, 0.5, 0.8, 0.9, 0.99, 1.0, rng.random()]))
+        k_min = int(rng.integers(0, E + 1))
+        k_max = int(rng.integers(k_min, E + 1))
+        m, c, order = F.select_row(p, tau, k_min, k_max)
+        kk, S = brute.prefetch_set(list(p), tau, k_min, k_max)
+        assert c == kk, (p, tau, k_min, k_max, c, kk)
+        assert m == sum(1 << j for j in S), (p, tau, m, S)
+        m0, c0, _ = F.select_row(p, tau, 0, E)
+        assert c0 == brute.min_cardinality(list(p), tau)
+        chosen = [j for j in range(E) if (m0 >> j) & 1]
+        assert math.fsum(p[j] for j in chosen) == brute.max_sum_of_size(list(p), c0)
+
+
+def check_select_nesting_and_minimality(seed=9):
+    rng = np.random.default_rng(seed)
+    for _ in range(200):
+        E = int(rng.integers(2, 64))
+        p = rng.dirichlet(np.full(E, 0.5))
+        taus = np.sort(rng.random(4))
+        prev = 0
+        for t in taus:
+            m, c, order = F.select_row(p, float(t), 0, E)
+            assert (prev & ~m) == 0, "sets must grow with tau"
+            prev = m
+            chosen = [int(order[i]) for i in range(c)]
+            total = math.fsum(p[j] for j in chosen)
+            if c < E:
+                assert total >= t - 1e-12
+            if c > 0:
+                assert math.fsum(p[j] for j in chosen[:-1]) < t + 1e-12
+        m, c, _ = F.select_row(p, 1.5, 0, E)
+        assert c == E and m == (1 << E) - 1
+        m, c, _ = F.select_row(p, 0.999, 2, 3)
+        assert 2 <= c <= 3
+
+
+def check_blend():
+    a = np.array([0.5, 0.25, 0.25])
+    b = np.array([0.0, 0.5, 0.5])
+    got = F.blend_rows(np.stack([a, b]), [0.5, 0.25])
+    ref = (2 * a + b) / 3
+    assert np.max(np.abs(got - ref)) <= 1e-16
+    assert np.array_equal(F.blend_rows(a[None, :], [0.7]), a)
+    assert np.max(np.abs(F.blend_rows(np.stack([a, a, a]), [0.9, 0.3, 0.1]) - a)) <= 1e-16
+    got = F.blend_rows(np.stack([a, b]), [-0.5, 0.0])     # all weights clipped to 0: plain mean
+    assert np.max(np.abs(got - (a + b) / 2)) <= 1e-16
+    got = F.blend_rows(np.stack([a, b]), [0.9, -0.2])     # negative weight is dropped
+    assert np.array_equal(got, a)
+    rng = np.random.default_rng(10)
+    rows = rng.dirichlet(np.ones(16), size=4)
+    got = F.blend_rows(rows, rng.random(4))
+    assert abs(got.sum() - 1.0) <= 1e-14 and np.all(got >= 0)
+
+
+def check_select_prefetch_layout(seed=11):
+    rng = np.random.default_rng(seed)
+    n, L, E = 10, 5, 6
+    maps = _rand_maps(rng, n, L, E)
+    idx = np.array([[3], [-1], [7]])
+    score = np.array([[0.9], [-np.inf], [0.2]])
+    lb = np.array([1, 0, 4])
+    le = np.array([4, 5, 9])
+    mask, cnt = F.select_prefetch(maps, "f32", idx, score, lb, le, F.TAU_FIXED, 0.5, 1, 6, F.BLEND_NONE)
+    assert np.all(mask[0, [0, 4]] == 0) and np.all(cnt[0, 1:4] > 0)
+    assert np.all(mask[1] == 0) and np.all(cnt[1] == 0)
+    assert np.all(mask[2, :4] == 0) and cnt[2, 4] > 0
+    for l in range(1, 4):
+        m, c, _ = F.select_row(F.widen(maps[3, l], "f32"), float(np.float32(0.5)), 1, 6)
+        assert mask[0, l] == m and cnt[0, l] == c
+    # dynamic threshold: score 0.9 -> delta 0.1 -> small sets, score 0.2 -> delta 0.8
+    mask, cnt = F.select_prefetch(maps, "f32", idx, score, lb, le, F.TAU_DYNAMIC, 0.0, 0, 6, F.BLEND_NONE)
+    m, c, _ = F.select_row(F.widen(maps[7, 4], "f32"), 1.0 - 0.2, 0, 6)
+    assert mask[2, 4] == m and cnt[2, 4] == c
+
+
+ALL_CHECKS = [
+    check_cosine_vs_fsum, check_cosine_vs_torch, check_self_match, check_disjoint_support,
+    check_depth_special_cases, check_unobserved_layers_ignored, check_semantic_vs_fsum,
+    check_match_vs_bruteforce, check_rank_rules, check_uniform_golden, check_delta_golden,
+    check_select_vs_enumeration, check_select_nesting_and_minimality, check_blend,
+    check_select_prefetch_layout,
+]

@@ -1,0 +1,180 @@
+"""Planted mistakes in the oracle (on the CPU only): each plausible slip — a
+dropped term, a wrong sign or index, a transposed operand, a reversed tie
+rule — must make at least one pin of oracle_checks fail."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle.finemoe as F
+import oracle_checks as C
+
+_orig_select_row = F.select_row
+_orig_traj = F.trajectory_scores
+_orig_cos_many = F._cosine_many
+_orig_rank = F.rank
+_orig_threshold = F.threshold
+
+
+def strict_threshold_select(p, tau, k_min, k_max):
+    p = np.asarray(p, dtype=np.float64)
+    E = p.shape[0]
+    order = np.lexsort((np.arange(E), -p))
+    kstar, c = E, 0.0
+    for k in range(E + 1):
+        if c > tau:                       # ">" instead of ">="
+            kstar = k
+            break
+        if k < E:
+            c += p[order[k]]
+    kk = min(max(kstar, k_min), k_max)
+    return sum(1 << int(order[i]) for i in range(kk)), kk, order
+
+
+def high_index_first_select(p, tau, k_min, k_max):
+    p = np.asarray(p, dtype=np.float64)
+    E = p.shape[0]
+    order = np.lexsort((-np.arange(E), -p))   # ties: higher expert index first
+    kstar, c = E, 0.0
+    for k in range(E + 1):
+        if c >= tau:
+            kstar = k
+            break
+        if k < E:
+            c += p[order[k]]
+    kk = min(max(kstar, k_min), k_max)
+    return sum(1 << int(order[i]) for i in range(kk)), kk, order
+
+
+def sum_before_test_select(p, tau, k_min, k_max):
+    p = np.asarray(p, dtype=np.float64)
+    E = p.shape[0]
+    order = np.lexsort((np.arange(E), -p))
+    kstar, c = E, 0.0
+    for k in range(E):
+        c += p[order[k]]                  # adds expert k before testing c_k
+        if c >= tau:
+            kstar = k
+            break
+    kk = min(max(kstar, k_min), k_max)
+    return sum(1 << int(order[i]) for i in range(kk)), kk, order
+
+
+def no_cap_select(p, tau, k_min, k_max):
+    m, c, order = _orig_select_row(p, tau, k_min, len(p))
+    c = max(c, k_min)
+    return sum(1 << int(order[i]) for i in range(c)), c, order
+
+
+def ascending_select(p, tau, k_min, k_max):
+    return _orig_select_row(-np.asarray(p, dtype=np.float64), -tau, k_min, k_max)
+
+
+def prefix_off_by_one(maps64, q64, p):
+    return _orig_traj(maps64, q64, min(p + 1, maps64.shape[1]))
+
+
+def prefix_over_experts(maps64, q64, p):
+    n, L, E = maps64.shape
+    V = maps64[:, :, :min(p, E)].reshape(n, -1)
+    u = q64[:, :min(p, E)].reshape(-1)
+    return F._cosine_many(V, u)
+
+
+def missing_sqrt(V, u):
+    dots = V @ u
+    nv = np.einsum("ij,ij->i", V, V)      # squared norm used as the norm
+    nu = math.sqrt(float(np.dot(u, u)))
+    with np.errstate(invalid="ignore", divide="ignore"):
+        s = dots / (nv * nu)
+    s[(nv == 0) | (nu == 0)] = 0.0
+    return s
+
+
+def no_query_norm(V, u):
+    dots = V @ u
+    nv = np.sqrt(np.einsum("ij,ij->i", V, V))
+    with np.errstate(invalid="ignore", divide="ignore"):
+        s = dots / nv
+    s[nv == 0] = 0.0
+    return s
+
+
+def rank_high_index_first(scores, k, idx=None):
+    s = np.asarray(scores, dtype=np.float64)
+    if idx is None:
+        idx = np.arange(s.shape[0])
+    return _orig_rank(s, k, idx) if s.size == 0 else _rank_rev(s, k, np.asarray(idx))
+
+
+def _rank_rev(s, k, idx):
+    nan = np.isnan(s)
+    order = np.lexsort((-idx, -np.where(nan, 0.0, s), nan))[:k]
+    oi = np.full(k, -1, dtype=np.int64)
+    os_ = np.full(k, -np.inf)
+    oi[:order.size] = idx[order]
+    os_[:order.size] = s[order]
+    return oi, os_
+
+
+def rank_ascending(scores, k, idx=None):
+    s = np.asarray(scores, dtype=np.float64)
+    i, _ = _orig_rank(-s, k, idx)
+    full_idx = np.arange(s.shape[0]) if idx is None else np.asarray(idx)
+    pos = {int(v): j for j, v in enumerate(full_idx)}
+    return i, np.array([s[pos[int(v)]] if v >= 0 else -np.inf for v in i])
+
+
+def unnormalised_blend(rows, scores):
+    rows = np.asarray(rows, dtype=np.float64)
+    w = [max(float(s), 0.0) for s in scores]
+    return sum(w[i] * rows[i] for i in range(rows.shape[0]))
+
+
+def softmax_weight_blend(rows, scores):
+    rows = np.asarray(rows, dtype=np.float64)
+    w = np.exp(np.asarray(scores, dtype=np.float64))
+    return (w[:, None] * rows).sum(0) / w.sum()
+
+
+def unclipped_delta(mode, tau, score):
+    if mode == F.TAU_DYNAMIC:
+        return 1.0 - float(score)
+    return _orig_threshold(mode, tau, score)
+
+
+def score_as_delta(mode, tau, score):
+    if mode == F.TAU_DYNAMIC:
+        return max(0.0, min(float(score), 1.0))
+    return _orig_threshold(mode, tau, score)
+
+
+MUTANTS = [
+    ("select_row", strict_threshold_select),
+    ("select_row", high_index_first_select),
+    ("select_row", sum_before_test_select),
+    ("select_row", no_cap_select),
+    ("select_row", ascending_select),
+    ("trajectory_scores", prefix_off_by_one),
+    ("trajectory_scores", prefix_over_experts),
+    ("_cosine_many", missing_sqrt),
+    ("_cosine_many", no_query_norm),
+    ("rank", rank_high_index_first),
+    ("rank", rank_ascending),
+    ("blend_rows", unnormalised_blend),
+    ("blend_rows", softmax_weight_blend),
+    ("threshold", unclipped_delta),
+    ("threshold", score_as_delta),
+]
+
+
+@pytest.mark.parametrize("name,mutant", MUTANTS, ids=lambda x: getattr(x, "__name__", str(x)))
+def test_planted_mistake_is_caught(monkeypatch, name, mutant):
+    monkeypatch.setattr(F, name, mutant)
+    failed = []
+    for check in C.ALL_CHECKS:
+        try:
+            check()
+        except Exception:  # noqa: BLE001 - any failure of a pin counts as caught
+            failed.append(check.__name__)
+    assert failed, f"no pin catches the planted mistake {mutant.__name__}"
