@@ -1,0 +1,199 @@
+/*
+ * finemoe_map.h - C ABI of the expert-map matching and prefetch-selection
+ * library for AMD Instinct MI355X (gfx950).
+ *
+ * The library implements the per-iteration search of FineMoE (arXiv
+ * 2502.05370): a batch of queries is scored by cosine similarity against a
+ * GPU-resident store of historical iterations, the best stored iteration(s)
+ * are kept per query, and the matched expert map is turned into per-layer
+ * expert prefetch sets by probability thresholding.
+ *
+ *   expert map (Section 4.1)      L rows of E gate probabilities, one row per
+ *                                 MoE layer (the paper's J experts are E here)
+ *   semantic search (Eq. 4)       cosine of embedding-layer outputs
+ *   trajectory search (Eq. 5)     cosine of the first p observed layers of
+ *                                 gate probabilities, flattened
+ *   threshold (Section 4.3)       fixed tau, or delta = Clip(1 - score, 0, 1)
+ *   prefetch set (Eq. 6-8)        fewest experts, highest probability first,
+ *                                 whose summed probability reaches the
+ *                                 threshold, clamped to [k_min, k_max]
+ *
+ * Conventions shared by every call:
+ *   - All pointers marked "device" are HIP device pointers owned by the
+ *     caller; the library never allocates device memory and never frees a
+ *     caller buffer.  A store handle only borrows its buffer.
+ *   - Work is enqueued asynchronously on the given stream (a hipStream_t
+ *     passed as void*; NULL means the null stream).  Outputs are valid once
+ *     the caller has synchronised that stream.  No call synchronises the
+ *     stream except fm_store_check.
+ *   - Arguments are validated on the host before anything is enqueued; an
+ *     invalid call returns a non-zero fm_status, enqueues nothing and leaves
+ *     every output untouched.  fm_last_error() then describes the problem
+ *     (thread-local, valid until the next call on the same thread).
+ *   - Ranking order is (score descending, store index ascending); a NaN
+ *     score ranks below every number.  Missing matches (an empty store, or
+ *     k larger than the store) are returned as index -1 and score -inf, and
+ *     select nothing.
+ *   - bf16 values are IEEE-754 binary32 values truncated to their upper 16
+ *     bits (as produced by round-to-nearest-even), stored as uint16.
+ */
+#ifndef FINEMOE_MAP_H
+#define FINEMOE_MAP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    FM_OK = 0,
+    FM_ERR_INVALID = 1,      /* bad argument: NULL pointer, out-of-range size or parameter */
+    FM_ERR_UNSUPPORTED = 2,  /* valid but not implemented (e.g. E > 64, d_emb not a multiple of 128) */
+    FM_ERR_FULL = 3,         /* insert would exceed the store capacity */
+    FM_ERR_HIP = 4,          /* a HIP runtime call failed (message from the runtime) */
+    FM_ERR_DEVICE = 5        /* fm_store_check found a sticky device-side range error */
+} fm_status;
+
+typedef enum { FM_F32 = 0, FM_BF16 = 1 } fm_dtype;
+
+/* Threshold of Section 4.3: FIXED uses params.tau for every layer; DYNAMIC
+ * uses delta = Clip(1 - score, 0, 1) with the best match's score (a NaN score
+ * gives delta = 1). */
+typedef enum { FM_TAU_FIXED = 0, FM_TAU_DYNAMIC = 1 } fm_tau_mode;
+
+/* Which probabilities guide a layer: NONE = the layer's row of the best match
+ * (Sections 4.2.1 and 4.2.2 use the single highest-scoring map); SCORE = the
+ * similarity-weighted mean of that row over the k kept matches, with weights
+ * max(score, 0) (plain mean if every weight is 0). */
+typedef enum { FM_BLEND_NONE = 0, FM_BLEND_SCORE = 1 } fm_blend;
+
+/* Sticky device-side flags reported by fm_store_check. */
+#define FM_FLAG_DEPTH_CLAMPED 0x1u   /* a trajectory depth was outside [1, max_depth] and was clamped */
+#define FM_FLAG_INDEX_RANGE   0x2u   /* fm_select_prefetch met an index >= the store size (row skipped) */
+
+typedef struct fm_store fm_store;   /* opaque host-side handle */
+
+typedef struct {
+    int32_t cap;         /* capacity C in stored iterations, >= 1 */
+    int32_t L;           /* MoE layers, 1..64 */
+    int32_t E;           /* experts per layer, 1..64 (a prefetch set is a 64-bit mask) */
+    int32_t d_emb;       /* semantic embedding size (hidden size h); 0 = no embeddings,
+                            otherwise a positive multiple of 128 */
+    fm_dtype map_dtype;  /* element type of stored maps and trajectory queries */
+    void* buffer;        /* device, at least fm_store_bytes(...) bytes, 256-byte aligned */
+    size_t buffer_bytes;
+} fm_store_desc;
+
+typedef struct {
+    fm_tau_mode mode;
+    float tau;           /* FIXED threshold; compared as the exact float value */
+    int32_t k_min;       /* Eq. 8 floor (the model's K), 0 <= k_min <= k_max */
+    int32_t k_max;       /* cap on the set size, k_max <= E */
+    fm_blend blend;
+} fm_select_params;
+
+/* Bytes of the layer-major map planes alone: L planes of cap rows of E
+ * elements, each plane padded to 256 bytes.  For cap = 32768 maps of 24 x 60
+ * float32 (Section 6.8's largest store, Qwen1.5-MoE shape) this is
+ * 188,743,680 bytes. */
+size_t fm_map_bytes(int32_t cap, int32_t L, int32_t E, fm_dtype map_dtype);
+
+/* Bytes of the whole device buffer a store needs: map planes, embeddings
+ * (cap x d_emb bf16), their float32 norms and 256 bytes of device flags,
+ * each part 256-byte aligned.  Returns 0 for invalid sizes. */
+size_t fm_store_bytes(int32_t cap, int32_t L, int32_t E, int32_t d_emb, fm_dtype map_dtype);
+
+/* Bytes of match workspace for batches of up to B_max queries keeping up to
+ * k_max matches each.  The workspace must be zero-filled before its first use;
+ * every completed match call leaves it zero-filled again.  Calls that share a
+ * workspace must be ordered (same stream, or synchronised). */
+size_t fm_workspace_bytes(int32_t B_max, int32_t k_max);
+
+/* Create a host handle over a caller-owned device buffer (Expert Map Store,
+ * Section 4.4).  The store starts empty.  The buffer contents are not read;
+ * the current HIP device at this call is the store's device.  Errors:
+ * FM_ERR_INVALID for NULL pointers, out-of-range sizes or a short or
+ * misaligned buffer; FM_ERR_UNSUPPORTED for E or L above 64 or a d_emb that is
+ * not a multiple of 128. */
+fm_status fm_store_build(fm_store** out, const fm_store_desc* desc);
+
+/* Append n iterations (Step 5 of Section 3.2: new expert maps enter the
+ * store).  maps: device [n][L][E] of map_dtype, map-major; embs: device
+ * [n][d_emb] bf16, required when d_emb > 0 and ignored otherwise.  The maps
+ * are transposed into the layer-major planes and the embedding norms are
+ * computed.  slots_out: device [n] int32 receiving the store index of each
+ * inserted iteration, or NULL.  FM_ERR_FULL if size + n > cap (nothing is
+ * inserted).  n == 0 is a no-op. */
+fm_status fm_store_insert(fm_store* store, const void* maps, const void* embs, int32_t n,
+                          int32_t* slots_out, void* stream);
+
+/* Current number of stored iterations (host-side count, no synchronisation). */
+fm_status fm_store_size(const fm_store* store, int32_t* n_out);
+
+/* Synchronise the stream, read and clear the sticky device flags
+ * (FM_FLAG_*).  Returns FM_ERR_DEVICE when any flag was set; *flags_out (may
+ * be NULL) receives them. */
+fm_status fm_store_check(fm_store* store, void* stream, uint32_t* flags_out);
+
+/* Release the host handle (the caller's buffer is untouched). */
+fm_status fm_store_destroy(fm_store* store);
+
+/* Semantic search, Eq. 4: for each query embedding q[b] (device [B][d_emb]
+ * bf16) the k stored iterations with the highest cosine
+ * q[b].x[y] / (|q[b]| |x[y]|) over y < size, accumulated in float32.  A zero
+ * norm gives score 0.  Outputs: idx_out device [B][k] int32, score_out device
+ * [B][k] float32, in ranking order.  1 <= k <= 8, 1 <= B <= 65536.
+ * FM_ERR_INVALID if the store has no embeddings or the workspace is too
+ * small. */
+fm_status fm_match_semantic(const fm_store* store, const void* q, int32_t B, int32_t k,
+                            int32_t* idx_out, float* score_out,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
+/* Trajectory search, Eq. 5: query b observed its first p_b = depth[b] layers
+ * (device [B] int32); q is device [B][L][E] of map_dtype, map-major, and rows
+ * l >= p_b are never read.  Score = cosine between q[b][0:p_b] and
+ * x[y][0:p_b], both flattened over (layer, expert), accumulated in float32.
+ * max_depth (1..L) is a host-side bound on the depths that sizes the scan;
+ * a depth outside [1, max_depth] is clamped and sets FM_FLAG_DEPTH_CLAMPED.
+ * Outputs and limits as for fm_match_semantic. */
+fm_status fm_match_trajectory(const fm_store* store, const void* q, const int32_t* depth,
+                              int32_t max_depth, int32_t B, int32_t k,
+                              int32_t* idx_out, float* score_out,
+                              void* workspace, size_t workspace_bytes, void* stream);
+
+/* Prefetch sets, Section 4.3 (Eq. 6-8): for query b and every layer l in
+ * [layer_begin[b], layer_end[b]) (device [B] int32 each, clamped to [0, L]),
+ * take the guiding probabilities (fm_blend), the threshold (fm_tau_mode) from
+ * score[b][0], order the experts by probability (descending, lower expert
+ * index first on equal values), find the smallest k* whose running float64
+ * sum of the first k* reaches the threshold (k* = E if none does) and keep
+ * the first min(max(k*, k_min), k_max).  idx/score: device [B][k] as written
+ * by a match call.  mask_out: device [B][L] uint64, bit j = expert j;
+ * count_out: device [B][L] uint8.  Layers outside the range, and queries whose
+ * idx[b][0] is -1, get mask 0 and count 0. */
+fm_status fm_select_prefetch(const fm_store* store, const int32_t* idx, const float* score,
+                             int32_t B, int32_t k, const int32_t* layer_begin,
+                             const int32_t* layer_end, const fm_select_params* params,
+                             uint64_t* mask_out, uint8_t* count_out, void* stream);
+
+/* Test support: the dense float32 score matrix of a trajectory (q, depth
+ * non-NULL) or semantic (q_sem non-NULL) search, written to scores_out device
+ * [B][size] by the same kernels and arithmetic as the match calls.
+ * Exactly one of q / q_sem must be non-NULL. */
+fm_status fm_debug_scores(const fm_store* store, const void* q, const int32_t* depth,
+                          int32_t max_depth, const void* q_sem, int32_t B, float* scores_out,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* Description of the last non-OK status on this thread ("" if none). */
+const char* fm_last_error(void);
+
+/* ABI version: (major << 16) | minor. */
+int32_t fm_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FINEMOE_MAP_H */

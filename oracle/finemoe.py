@@ -205,10 +205,10 @@ def select_row(p: np.ndarray, tau: float, k_min: int, k_max: int) -> Tuple[int, 
 
 def blend_rows(rows: np.ndarray, scores: np.ndarray) -> np.ndarray:
     """Similarity-weighted mean of k rows: sum_i w_i row_i / sum_i w_i with
-    w_i = max(score_i, 0), summed in order i = 0..k-1; if every weight is 0
-    the plain mean is used."""
+    w_i = max(score_i, 0) (a NaN score weighs 0), summed in order
+    i = 0..k-1; if every weight is 0 the plain mean is used."""
     rows = np.asarray(rows, dtype=np.float64)
-    w = [max(float(s), 0.0) for s in scores]
+    w = [float(s) if float(s) > 0.0 else 0.0 for s in scores]
     if sum(w) == 0.0:
         w = [1.0] * len(w)
     num = np.zeros(rows.shape[1], dtype=np.float64)

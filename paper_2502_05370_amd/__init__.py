@@ -1,0 +1,211 @@
+"""FineMoE expert-map matching and prefetch selection on MI355X (gfx950).
+
+A thin Python binding over the C ABI of ``libfinemoe_map.so``
+(include/finemoe_map.h).  PyTorch provides device memory and streams only:
+every step of the path (store residency, semantic and trajectory search,
+ranking, blending, thresholding and selection) runs in the library's HIP
+kernels.  There is no CPU fallback; the import fails if the library has not
+been built.
+
+    store = Store(cap, L, E, d_emb=0, map_dtype="f32")
+    store.insert(maps, embs=None)                       # maps [n][L][E] on the GPU
+    idx, score = match_trajectory(store, q, depth, k=1) # Eq. 5
+    idx, score = match_semantic(store, q_sem, k=1)      # Eq. 4
+    mask, count = select_prefetch(store, idx, score, layer_begin, layer_end,
+                                  tau=0.8, k_min=1, k_max=8)   # Eq. 6-8
+"""
+from __future__ import annotations
+
+import ctypes as C
+from typing import Optional, Tuple
+
+import torch
+
+from . import _lib
+from ._lib import (FM_BF16, FM_BLEND_NONE, FM_BLEND_SCORE, FM_F32, FM_FLAG_DEPTH_CLAMPED,  # noqa: F401
+                   FM_FLAG_INDEX_RANGE, FM_TAU_DYNAMIC, FM_TAU_FIXED, FmError, SelectParams)
+
+_lib.load()
+
+__all__ = ["Store", "Workspace", "match_semantic", "match_trajectory", "select_prefetch", "debug_scores",
+           "map_bytes", "store_bytes", "workspace_bytes", "FmError"]
+
+_DTYPES = {"f32": FM_F32, "bf16": FM_BF16}
+_TORCH = {FM_F32: torch.float32, FM_BF16: torch.bfloat16}
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> C.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return C.c_void_p(stream.cuda_stream)
+
+
+def _aligned_bytes(nbytes: int, device) -> torch.Tensor:
+    """A 256-byte aligned uint8 device tensor of ``nbytes`` bytes."""
+    raw = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+    off = (-raw.data_ptr()) % 256
+    return raw[off:off + nbytes]
+
+
+def map_bytes(cap: int, L: int, E: int, map_dtype: str = "f32") -> int:
+    return int(_lib.load().fm_map_bytes(cap, L, E, _DTYPES[map_dtype]))
+
+
+def store_bytes(cap: int, L: int, E: int, d_emb: int = 0, map_dtype: str = "f32") -> int:
+    return int(_lib.load().fm_store_bytes(cap, L, E, d_emb, _DTYPES[map_dtype]))
+
+
+def workspace_bytes(B_max: int, k_max: int) -> int:
+    return int(_lib.load().fm_workspace_bytes(B_max, k_max))
+
+
+class Workspace:
+    """Device scratch for match calls (contents need no initialisation)."""
+
+    def __init__(self, B_max: int = 1024, k_max: int = 8, device="cuda"):
+        self.nbytes = workspace_bytes(B_max, k_max)
+        if self.nbytes == 0:
+            raise ValueError(f"invalid workspace request B_max={B_max} k_max={k_max}")
+        self.buf = _aligned_bytes(self.nbytes, device)
+
+    @property
+    def ptr(self):
+        return C.c_void_p(self.buf.data_ptr())
+
+
+class Store:
+    """Expert Map Store held in one device buffer owned by this object."""
+
+    def __init__(self, cap: int, L: int, E: int, d_emb: int = 0, map_dtype: str = "f32", device="cuda"):
+        self.cap, self.L, self.E, self.d_emb = int(cap), int(L), int(E), int(d_emb)
+        self.map_dtype = map_dtype
+        self.dtype_code = _DTYPES[map_dtype]
+        self.device = torch.device(device)
+        nbytes = store_bytes(cap, L, E, d_emb, map_dtype)
+        if nbytes == 0:
+            raise ValueError(f"invalid store shape cap={cap} L={L} E={E} d_emb={d_emb}")
+        with torch.cuda.device(self.device):
+            self.buf = _aligned_bytes(nbytes, self.device)
+            desc = _lib.StoreDesc(self.cap, self.L, self.E, self.d_emb, self.dtype_code,
+                                  C.c_void_p(self.buf.data_ptr()), nbytes)
+            h = C.c_void_p()
+            _lib.check(_lib.load().fm_store_build(C.byref(h), C.byref(desc)), "fm_store_build")
+        self.handle = h
+        self.workspace = None
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h is not None and h.value:
+            _lib.load().fm_store_destroy(h)
+            self.handle = None
+
+    @property
+    def size(self) -> int:
+        n = C.c_int32()
+        _lib.check(_lib.load().fm_store_size(self.handle, C.byref(n)), "fm_store_size")
+        return n.value
+
+    def insert(self, maps: torch.Tensor, embs: Optional[torch.Tensor] = None, stream=None,
+               return_slots: bool = False):
+        """Append maps [n][L][E] (and embeddings [n][d_emb] bf16) already on the device."""
+        maps = maps.contiguous()
+        if maps.dtype != _TORCH[self.dtype_code] or maps.dim() != 3 or tuple(maps.shape[1:]) != (self.L, self.E):
+            raise ValueError(f"maps must be [n][{self.L}][{self.E}] {_TORCH[self.dtype_code]}, got "
+                             f"{tuple(maps.shape)} {maps.dtype}")
+        n = maps.shape[0]
+        if embs is not None:
+            embs = embs.contiguous()
+            if embs.dtype != torch.bfloat16 or tuple(embs.shape) != (n, self.d_emb):
+                raise ValueError(f"embs must be [{n}][{self.d_emb}] bfloat16")
+        slots = torch.empty(n, dtype=torch.int32, device=self.device) if return_slots else None
+        _lib.check(_lib.load().fm_store_insert(self.handle, _ptr(maps), _ptr(embs), n, _ptr(slots),
+                                               _stream(stream)), "fm_store_insert")
+        return slots
+
+    def check(self, stream=None) -> int:
+        """Synchronise and return the sticky device flags (raises FmError if any)."""
+        f = C.c_uint32()
+        st = _lib.load().fm_store_check(self.handle, _stream(stream), C.byref(f))
+        if st == _lib.FM_ERR_DEVICE:
+            return f.value
+        _lib.check(st, "fm_store_check")
+        return f.value
+
+    def ensure_workspace(self) -> Workspace:
+        if self.workspace is None:
+            self.workspace = Workspace(device=self.device)
+        return self.workspace
+
+
+def _ws(store: Store, workspace: Optional[Workspace]) -> Workspace:
+    return workspace if workspace is not None else store.ensure_workspace()
+
+
+def match_trajectory(store: Store, q: torch.Tensor, depth: torch.Tensor, k: int = 1,
+                     max_depth: Optional[int] = None, out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None,
+                     workspace: Optional[Workspace] = None, stream=None):
+    """Eq. 5 search: q [B][L][E] (store dtype), depth [B] int32 -> idx [B][k] int32, score [B][k] float32."""
+    B = q.shape[0]
+    if max_depth is None:
+        max_depth = store.L
+    if out is None:
+        out = (torch.empty((B, k), dtype=torch.int32, device=store.device),
+               torch.empty((B, k), dtype=torch.float32, device=store.device))
+    idx, score = out
+    ws = _ws(store, workspace)
+    _lib.check(_lib.load().fm_match_trajectory(store.handle, _ptr(q), _ptr(depth), max_depth, B, k,
+                                               _ptr(idx), _ptr(score), ws.ptr, ws.nbytes, _stream(stream)),
+               "fm_match_trajectory")
+    return idx, score
+
+
+def match_semantic(store: Store, q: torch.Tensor, k: int = 1,
+                   out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None,
+                   workspace: Optional[Workspace] = None, stream=None):
+    """Eq. 4 search: q [B][d_emb] bfloat16 -> idx [B][k] int32, score [B][k] float32."""
+    B = q.shape[0]
+    if out is None:
+        out = (torch.empty((B, k), dtype=torch.int32, device=store.device),
+               torch.empty((B, k), dtype=torch.float32, device=store.device))
+    idx, score = out
+    ws = _ws(store, workspace)
+    _lib.check(_lib.load().fm_match_semantic(store.handle, _ptr(q), B, k, _ptr(idx), _ptr(score), ws.ptr,
+                                             ws.nbytes, _stream(stream)), "fm_match_semantic")
+    return idx, score
+
+
+def select_prefetch(store: Store, idx: torch.Tensor, score: torch.Tensor, layer_begin: torch.Tensor,
+                    layer_end: torch.Tensor, tau: float = 0.9, k_min: int = 1, k_max: Optional[int] = None,
+                    mode: int = FM_TAU_FIXED, blend: int = FM_BLEND_NONE,
+                    out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None, stream=None):
+    """Eq. 6-8 prefetch sets -> mask [B][L] (int64 holding uint64 bits), count [B][L] uint8."""
+    B, k = idx.shape
+    if k_max is None:
+        k_max = store.E
+    if out is None:
+        out = (torch.empty((B, store.L), dtype=torch.int64, device=store.device),
+               torch.empty((B, store.L), dtype=torch.uint8, device=store.device))
+    mask, count = out
+    p = SelectParams(mode, tau, k_min, k_max, blend)
+    _lib.check(_lib.load().fm_select_prefetch(store.handle, _ptr(idx), _ptr(score), B, k, _ptr(layer_begin),
+                                              _ptr(layer_end), C.byref(p), _ptr(mask), _ptr(count),
+                                              _stream(stream)), "fm_select_prefetch")
+    return mask, count
+
+
+def debug_scores(store: Store, q: Optional[torch.Tensor] = None, depth: Optional[torch.Tensor] = None,
+                 q_sem: Optional[torch.Tensor] = None, max_depth: Optional[int] = None,
+                 workspace: Optional[Workspace] = None, stream=None) -> torch.Tensor:
+    """Dense float32 scores [B][size] from the same kernels as the match calls (test support)."""
+    B = (q if q is not None else q_sem).shape[0]
+    n = store.size
+    out = torch.full((B, max(n, 1)), float("nan"), dtype=torch.float32, device=store.device)
+    ws = _ws(store, workspace)
+    _lib.check(_lib.load().fm_debug_scores(store.handle, _ptr(q), _ptr(depth),
+                                           max_depth if max_depth is not None else store.L, _ptr(q_sem), B,
+                                           _ptr(out), ws.ptr, ws.nbytes, _stream(stream)), "fm_debug_scores")
+    return out[:, :n]

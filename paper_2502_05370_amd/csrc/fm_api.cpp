@@ -1,0 +1,336 @@
+// Host layer of libfinemoe_map: argument validation, store handles, buffer
+// layout and dispatch to the kernels.  Every entry point validates all of its
+// arguments before enqueueing anything and reports failures as an fm_status
+// plus a thread-local message; no C++ exception crosses the ABI.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <new>
+#include <string>
+
+#include "fm_internal.h"
+
+namespace {
+
+thread_local std::string g_error;
+
+fm_status fail(fm_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_error = buf;
+  return st;
+}
+
+fm_status ok() {
+  g_error.clear();
+  return FM_OK;
+}
+
+fm_status hip_fail(hipError_t e, const char* what) {
+  return fail(FM_ERR_HIP, "%s: %s (%d)", what, hipGetErrorString(e), static_cast<int>(e));
+}
+
+size_t elem_size(fm_dtype t) { return t == FM_BF16 ? 2 : 4; }
+
+bool valid_dtype(int t) { return t == FM_F32 || t == FM_BF16; }
+
+struct Layout {
+  size_t plane_bytes, maps, embs, norms, flags, total;
+  int64_t plane_elems;
+};
+
+// Buffer layout: [L map planes][embeddings][norms][flags], 256-byte aligned parts.
+bool make_layout(int32_t cap, int32_t L, int32_t E, int32_t d_emb, fm_dtype t, Layout* out) {
+  if (cap < 1 || L < 1 || E < 1 || d_emb < 0 || !valid_dtype(t)) return false;
+  Layout ly;
+  const size_t es = elem_size(t);
+  ly.plane_bytes = fm::align_up(static_cast<size_t>(cap) * E * es, fm::kAlign);
+  ly.plane_elems = static_cast<int64_t>(ly.plane_bytes / es);
+  ly.maps = ly.plane_bytes * L;
+  ly.embs = fm::align_up(static_cast<size_t>(cap) * d_emb * 2, fm::kAlign);
+  ly.norms = d_emb > 0 ? fm::align_up(static_cast<size_t>(cap) * 4, fm::kAlign) : 0;
+  ly.flags = fm::kAlign;
+  ly.total = ly.maps + ly.embs + ly.norms + ly.flags;
+  *out = ly;
+  return true;
+}
+
+}  // namespace
+
+struct fm_store {
+  fm::StoreView v;
+  int device;
+};
+
+namespace fm {
+
+size_t workspace_bytes_needed() {
+  size_t b = 0;
+  b += align_up(sizeof(uint64_t) * kChunkB * kMaxK, kAlign);
+  b += kAlign;  // counter
+  b += align_up(sizeof(int32_t) * kChunkB, kAlign) * 2;
+  b += align_up(sizeof(float) * kChunkB, kAlign);
+  return b;
+}
+
+Workspace carve_workspace(void* base) {
+  char* p = static_cast<char*>(base);
+  Workspace w;
+  w.keys = reinterpret_cast<uint64_t*>(p);
+  p += align_up(sizeof(uint64_t) * kChunkB * kMaxK, kAlign);
+  w.counter = reinterpret_cast<uint32_t*>(p);
+  p += kAlign;
+  w.perm = reinterpret_cast<int32_t*>(p);
+  p += align_up(sizeof(int32_t) * kChunkB, kAlign);
+  w.sdepth = reinterpret_cast<int32_t*>(p);
+  p += align_up(sizeof(int32_t) * kChunkB, kAlign);
+  w.rq = reinterpret_cast<float*>(p);
+  return w;
+}
+
+}  // namespace fm
+
+namespace {
+
+fm_status check_store(const fm_store* s) {
+  if (s == nullptr) return fail(FM_ERR_INVALID, "store handle is NULL");
+  return FM_OK;
+}
+
+fm_status check_workspace(void* ws, size_t bytes) {
+  if (ws == nullptr) return fail(FM_ERR_INVALID, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % fm::kAlign != 0)
+    return fail(FM_ERR_INVALID, "workspace must be %zu-byte aligned", fm::kAlign);
+  if (bytes < fm::workspace_bytes_needed())
+    return fail(FM_ERR_INVALID, "workspace of %zu bytes is smaller than the %zu bytes required", bytes,
+                fm::workspace_bytes_needed());
+  return FM_OK;
+}
+
+// The kernels run on the store's device; make it current for the enqueue.
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = true;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) {
+      ok = false;
+      return;
+    }
+    if (prev != dev && hipSetDevice(dev) != hipSuccess) ok = false;
+  }
+  ~DeviceGuard() {
+    int cur = -1;
+    if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+}  // namespace
+
+extern "C" {
+
+int32_t fm_version(void) { return (1 << 16) | 0; }
+
+const char* fm_last_error(void) { return g_error.c_str(); }
+
+size_t fm_map_bytes(int32_t cap, int32_t L, int32_t E, fm_dtype map_dtype) {
+  Layout ly;
+  if (!make_layout(cap, L, E, 0, map_dtype, &ly)) return 0;
+  return ly.maps;
+}
+
+size_t fm_store_bytes(int32_t cap, int32_t L, int32_t E, int32_t d_emb, fm_dtype map_dtype) {
+  Layout ly;
+  if (!make_layout(cap, L, E, d_emb, map_dtype, &ly)) return 0;
+  return ly.total;
+}
+
+size_t fm_workspace_bytes(int32_t B_max, int32_t k_max) {
+  if (B_max < 1 || k_max < 1 || k_max > fm::kMaxK) return 0;
+  return fm::workspace_bytes_needed();
+}
+
+fm_status fm_store_build(fm_store** out, const fm_store_desc* d) {
+  if (out == nullptr || d == nullptr) return fail(FM_ERR_INVALID, "out and desc must be non-NULL");
+  if (!valid_dtype(d->map_dtype)) return fail(FM_ERR_INVALID, "map_dtype %d is not FM_F32 or FM_BF16", d->map_dtype);
+  if (d->cap < 1 || d->L < 1 || d->E < 1 || d->d_emb < 0)
+    return fail(FM_ERR_INVALID, "cap=%d L=%d E=%d d_emb=%d out of range", d->cap, d->L, d->E, d->d_emb);
+  if (d->E > fm::kMaxE) return fail(FM_ERR_UNSUPPORTED, "E=%d exceeds %d experts per layer", d->E, fm::kMaxE);
+  if (d->L > fm::kMaxL) return fail(FM_ERR_UNSUPPORTED, "L=%d exceeds %d layers", d->L, fm::kMaxL);
+  if (d->d_emb % 128 != 0)
+    return fail(FM_ERR_UNSUPPORTED, "d_emb=%d is not a multiple of 128", d->d_emb);
+  if (static_cast<int64_t>(d->cap) * d->E > (static_cast<int64_t>(1) << 31) - 1)
+    return fail(FM_ERR_UNSUPPORTED, "cap*E exceeds 2^31-1");
+  Layout ly;
+  make_layout(d->cap, d->L, d->E, d->d_emb, d->map_dtype, &ly);
+  if (d->buffer == nullptr) return fail(FM_ERR_INVALID, "buffer is NULL");
+  if (reinterpret_cast<uintptr_t>(d->buffer) % fm::kAlign != 0)
+    return fail(FM_ERR_INVALID, "buffer must be %zu-byte aligned", fm::kAlign);
+  if (d->buffer_bytes < ly.total)
+    return fail(FM_ERR_INVALID, "buffer of %zu bytes is smaller than fm_store_bytes = %zu", d->buffer_bytes, ly.total);
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  fm_store* s = new (std::nothrow) fm_store;
+  if (s == nullptr) return fail(FM_ERR_INVALID, "out of host memory");
+  char* base = static_cast<char*>(d->buffer);
+  s->v.planes = base;
+  s->v.plane_elems = ly.plane_elems;
+  s->v.embs = d->d_emb > 0 ? reinterpret_cast<uint16_t*>(base + ly.maps) : nullptr;
+  s->v.emb_norm = d->d_emb > 0 ? reinterpret_cast<float*>(base + ly.maps + ly.embs) : nullptr;
+  s->v.flags = reinterpret_cast<uint32_t*>(base + ly.maps + ly.embs + ly.norms);
+  s->v.cap = d->cap;
+  s->v.L = d->L;
+  s->v.E = d->E;
+  s->v.d_emb = d->d_emb;
+  s->v.n = 0;
+  s->v.map_dtype = d->map_dtype;
+  s->device = dev;
+  // Clear the device flags once (synchronous, outside any stream work).
+  e = hipMemset(s->v.flags, 0, fm::kAlign);
+  if (e != hipSuccess) {
+    delete s;
+    return hip_fail(e, "hipMemset(flags)");
+  }
+  *out = s;
+  return ok();
+}
+
+fm_status fm_store_insert(fm_store* s, const void* maps, const void* embs, int32_t n, int32_t* slots_out,
+                          void* stream) {
+  if (fm_status st = check_store(s)) return st;
+  if (n < 0) return fail(FM_ERR_INVALID, "n=%d is negative", n);
+  if (n == 0) return ok();
+  if (maps == nullptr) return fail(FM_ERR_INVALID, "maps is NULL");
+  if (s->v.d_emb > 0 && embs == nullptr) return fail(FM_ERR_INVALID, "store has d_emb=%d but embs is NULL", s->v.d_emb);
+  if (static_cast<int64_t>(s->v.n) + n > s->v.cap)
+    return fail(FM_ERR_FULL, "inserting %d into a store holding %d of %d", n, s->v.n, s->v.cap);
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(FM_ERR_HIP, "cannot select the store's device %d", s->device);
+  hipError_t e = fm::launch_insert(s->v, maps, embs, n, slots_out, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "insert launch");
+  s->v.n += n;
+  return ok();
+}
+
+fm_status fm_store_size(const fm_store* s, int32_t* n_out) {
+  if (fm_status st = check_store(s)) return st;
+  if (n_out == nullptr) return fail(FM_ERR_INVALID, "n_out is NULL");
+  *n_out = s->v.n;
+  return ok();
+}
+
+fm_status fm_store_check(fm_store* s, void* stream, uint32_t* flags_out) {
+  if (fm_status st = check_store(s)) return st;
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(FM_ERR_HIP, "cannot select the store's device %d", s->device);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint32_t flags = 0;
+  hipError_t e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  e = hipMemcpy(&flags, s->v.flags, sizeof(flags), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpy(flags)");
+  e = hipMemset(s->v.flags, 0, sizeof(uint32_t));
+  if (e != hipSuccess) return hip_fail(e, "hipMemset(flags)");
+  if (flags_out != nullptr) *flags_out = flags;
+  if (flags != 0) return fail(FM_ERR_DEVICE, "device flags 0x%x (1: depth clamped, 2: index out of range)", flags);
+  return ok();
+}
+
+fm_status fm_store_destroy(fm_store* s) {
+  if (fm_status st = check_store(s)) return st;
+  delete s;
+  return ok();
+}
+
+static fm_status check_match_common(const fm_store* s, int32_t B, int32_t k, const int32_t* idx_out,
+                                    const float* score_out, void* ws, size_t ws_bytes) {
+  if (fm_status st = check_store(s)) return st;
+  if (B < 1 || B > 65536) return fail(FM_ERR_INVALID, "B=%d outside [1, 65536]", B);
+  if (k < 1 || k > fm::kMaxK) return fail(FM_ERR_INVALID, "k=%d outside [1, %d]", k, fm::kMaxK);
+  if (idx_out == nullptr || score_out == nullptr) return fail(FM_ERR_INVALID, "idx_out and score_out must be non-NULL");
+  return check_workspace(ws, ws_bytes);
+}
+
+fm_status fm_match_semantic(const fm_store* s, const void* q, int32_t B, int32_t k, int32_t* idx_out,
+                            float* score_out, void* ws, size_t ws_bytes, void* stream) {
+  if (fm_status st = check_match_common(s, B, k, idx_out, score_out, ws, ws_bytes)) return st;
+  if (q == nullptr) return fail(FM_ERR_INVALID, "q is NULL");
+  if (s->v.d_emb == 0) return fail(FM_ERR_INVALID, "store has no embeddings (d_emb = 0)");
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(FM_ERR_HIP, "cannot select the store's device %d", s->device);
+  hipError_t e = fm::launch_match_semantic(s->v, q, B, k, idx_out, score_out, nullptr, fm::carve_workspace(ws),
+                                           static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "semantic match launch");
+  return ok();
+}
+
+fm_status fm_match_trajectory(const fm_store* s, const void* q, const int32_t* depth, int32_t max_depth,
+                              int32_t B, int32_t k, int32_t* idx_out, float* score_out, void* ws,
+                              size_t ws_bytes, void* stream) {
+  if (fm_status st = check_match_common(s, B, k, idx_out, score_out, ws, ws_bytes)) return st;
+  if (q == nullptr || depth == nullptr) return fail(FM_ERR_INVALID, "q and depth must be non-NULL");
+  if (max_depth < 1 || max_depth > s->v.L)
+    return fail(FM_ERR_INVALID, "max_depth=%d outside [1, L=%d]", max_depth, s->v.L);
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(FM_ERR_HIP, "cannot select the store's device %d", s->device);
+  hipError_t e = fm::launch_match_trajectory(s->v, q, depth, max_depth, B, k, idx_out, score_out, nullptr,
+                                             fm::carve_workspace(ws), static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "trajectory match launch");
+  return ok();
+}
+
+fm_status fm_select_prefetch(const fm_store* s, const int32_t* idx, const float* score, int32_t B, int32_t k,
+                             const int32_t* lb, const int32_t* le, const fm_select_params* p,
+                             uint64_t* mask_out, uint8_t* count_out, void* stream) {
+  if (fm_status st = check_store(s)) return st;
+  if (idx == nullptr || score == nullptr || lb == nullptr || le == nullptr || p == nullptr || mask_out == nullptr ||
+      count_out == nullptr)
+    return fail(FM_ERR_INVALID, "idx, score, layer_begin, layer_end, params, mask_out and count_out must be non-NULL");
+  if (B < 1 || B > 65536) return fail(FM_ERR_INVALID, "B=%d outside [1, 65536]", B);
+  if (k < 1 || k > fm::kMaxK) return fail(FM_ERR_INVALID, "k=%d outside [1, %d]", k, fm::kMaxK);
+  if (p->mode != FM_TAU_FIXED && p->mode != FM_TAU_DYNAMIC) return fail(FM_ERR_INVALID, "tau mode %d", p->mode);
+  if (p->blend != FM_BLEND_NONE && p->blend != FM_BLEND_SCORE) return fail(FM_ERR_INVALID, "blend %d", p->blend);
+  if (p->k_min < 0 || p->k_min > p->k_max || p->k_max > s->v.E)
+    return fail(FM_ERR_INVALID, "need 0 <= k_min (%d) <= k_max (%d) <= E (%d)", p->k_min, p->k_max, s->v.E);
+  if (p->mode == FM_TAU_FIXED && p->tau != p->tau) return fail(FM_ERR_INVALID, "tau is NaN");
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(FM_ERR_HIP, "cannot select the store's device %d", s->device);
+  hipError_t e = fm::launch_select(s->v, idx, score, B, k, lb, le, *p, mask_out, count_out,
+                                   static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "select launch");
+  return ok();
+}
+
+fm_status fm_debug_scores(const fm_store* s, const void* q, const int32_t* depth, int32_t max_depth,
+                          const void* q_sem, int32_t B, float* scores_out, void* ws, size_t ws_bytes,
+                          void* stream) {
+  if (fm_status st = check_store(s)) return st;
+  if ((q == nullptr) == (q_sem == nullptr)) return fail(FM_ERR_INVALID, "exactly one of q and q_sem must be non-NULL");
+  if (B < 1 || B > 65536) return fail(FM_ERR_INVALID, "B=%d outside [1, 65536]", B);
+  if (scores_out == nullptr) return fail(FM_ERR_INVALID, "scores_out is NULL");
+  if (fm_status st = check_workspace(ws, ws_bytes)) return st;
+  if (s->v.n == 0) return ok();
+  // Same kernels as the match calls; only the dense score output is written.
+  fm::Workspace w = fm::carve_workspace(ws);
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(FM_ERR_HIP, "cannot select the store's device %d", s->device);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  if (q != nullptr) {
+    if (depth == nullptr) return fail(FM_ERR_INVALID, "depth is NULL");
+    if (max_depth < 1 || max_depth > s->v.L)
+      return fail(FM_ERR_INVALID, "max_depth=%d outside [1, L=%d]", max_depth, s->v.L);
+    e = fm::launch_match_trajectory(s->v, q, depth, max_depth, B, 1, nullptr, nullptr, scores_out, w, st);
+  } else {
+    if (s->v.d_emb == 0) return fail(FM_ERR_INVALID, "store has no embeddings (d_emb = 0)");
+    e = fm::launch_match_semantic(s->v, q_sem, B, 1, nullptr, nullptr, scores_out, w, st);
+  }
+  if (e != hipSuccess) return hip_fail(e, "debug scores launch");
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,58 @@
+// Internal declarations shared by the host layer and the kernel sources of
+// libfinemoe_map.  Not part of the public ABI (include/finemoe_map.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "finemoe_map.h"
+
+namespace fm {
+
+constexpr int kMaxL = 64;            // layers per map
+constexpr int kMaxE = 64;            // experts per layer (mask width)
+constexpr int kMaxK = 8;             // matches kept per query
+constexpr int kChunkB = 1024;        // queries per scan launch
+constexpr size_t kAlign = 256;
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Device view of a store: layer-major map planes, embeddings and norms.
+struct StoreView {
+  void* planes;          // [L][cap][E] elements of map dtype; plane stride plane_elems
+  int64_t plane_elems;   // elements per plane (cap * E, padded to 256 bytes)
+  uint16_t* embs;        // [cap][d_emb] bf16
+  float* emb_norm;       // [cap]
+  uint32_t* flags;       // sticky FM_FLAG_* bits
+  int32_t cap, L, E, d_emb, n;
+  fm_dtype map_dtype;
+};
+
+// Layout of the per-call match workspace (byte offsets).
+struct Workspace {
+  uint64_t* keys;     // [kChunkB][kMaxK] packed (score, index) keys
+  uint32_t* counter;  // [4] completion counter and spare words
+  int32_t* perm;      // [kChunkB] query index at each depth-sorted position
+  int32_t* sdepth;    // [kChunkB] clamped depth at each sorted position
+  float* rq;          // [kChunkB] 1 / |query| (0 for a zero query), by original index
+};
+size_t workspace_bytes_needed();
+Workspace carve_workspace(void* base);
+
+// Launchers (return hipSuccess or the first HIP error).
+hipError_t launch_insert(const StoreView& s, const void* maps, const void* embs, int32_t n_new,
+                         int32_t* slots_out, hipStream_t st);
+hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int32_t* depth,
+                                   int32_t max_depth, int32_t B, int32_t k, int32_t* idx_out,
+                                   float* score_out, float* dbg_scores, const Workspace& ws,
+                                   hipStream_t st);
+hipError_t launch_match_semantic(const StoreView& s, const void* q, int32_t B, int32_t k,
+                                 int32_t* idx_out, float* score_out, float* dbg_scores,
+                                 const Workspace& ws, hipStream_t st);
+hipError_t launch_select(const StoreView& s, const int32_t* idx, const float* score, int32_t B,
+                         int32_t k, const int32_t* lb, const int32_t* le,
+                         const fm_select_params& p, uint64_t* mask_out, uint8_t* count_out,
+                         hipStream_t st);
+
+}  // namespace fm

@@ -1,0 +1,178 @@
+// Similarity-aware prefetch-set selection (Section 4.3, Eq. 6-8).
+//
+// One wavefront per (query, layer) row; lane j holds expert j (E <= 64).
+//   1. Guiding probabilities: the matched map's row (float64 widening of the
+//      stored value), or the similarity-weighted mean of the kept matches'
+//      rows, summed in match order with explicit float64 roundings.
+//   2. Threshold: fixed tau, or delta = Clip(1 - score, 0, 1).
+//   3. Rank of lane j = experts ahead of it in (probability descending,
+//      index ascending) order; NaN probabilities rank last.
+//   4. The running sum over that order is taken sequentially in float64; k*
+//      is the first prefix reaching the threshold (E if none), clamped to
+//      [k_min, k_max]; the mask is the ballot of lanes with rank < k.
+#include "fm_device.h"
+#include "fm_internal.h"
+
+namespace fm {
+
+namespace {
+
+struct SelArgs {
+  const void* planes;
+  int64_t plane_elems;
+  int32_t n, L, E;
+  fm_dtype dtype;
+  const int32_t* idx;
+  const float* score;
+  int32_t B, k;
+  const int32_t* lb;
+  const int32_t* le;
+  int32_t mode;
+  float tau;
+  int32_t k_min, k_max, blend;
+  uint64_t* mask_out;
+  uint8_t* count_out;
+  uint32_t* flags;
+};
+
+__device__ __forceinline__ double stored_prob(const SelArgs& a, int y, int l, int j) {
+  const int64_t off = static_cast<int64_t>(l) * a.plane_elems + static_cast<int64_t>(y) * a.E + j;
+  if (a.dtype == FM_F32) return static_cast<double>(static_cast<const float*>(a.planes)[off]);
+  return static_cast<double>(bf16_to_f32(static_cast<const uint16_t*>(a.planes)[off]));
+}
+
+// (p_i, i) is ahead of (p_j, j): larger probability, or equal and lower index;
+// NaN is behind every number and NaNs keep index order.
+__device__ __forceinline__ bool ahead(double pi, int i, double pj, int j) {
+  const bool ni = pi != pi, nj = pj != pj;
+  if (ni || nj) return (!ni && nj) || (ni && nj && i < j);
+  return pi > pj || (pi == pj && i < j);
+}
+
+}  // namespace
+
+__global__ void __launch_bounds__(256) k_select(SelArgs a) {
+  __shared__ double sorted[4][kMaxE];
+  const int lane = threadIdx.x % kWave;
+  const int wv = threadIdx.x / kWave;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + wv;
+  if (row >= static_cast<int64_t>(a.B) * a.L) return;
+  const int b = static_cast<int>(row / a.L);
+  const int l = static_cast<int>(row - static_cast<int64_t>(b) * a.L);
+
+  int lo = a.lb[b], hi = a.le[b];
+  lo = lo < 0 ? 0 : (lo > a.L ? a.L : lo);
+  hi = hi < 0 ? 0 : (hi > a.L ? a.L : hi);
+  const int y0 = a.idx[static_cast<int64_t>(b) * a.k];
+  bool live = l >= lo && l < hi && y0 >= 0;
+  if (live && y0 >= a.n) {
+    if (lane == 0) atomicOr(a.flags, static_cast<uint32_t>(FM_FLAG_INDEX_RANGE));
+    live = false;
+  }
+  if (!live) {
+    if (lane == 0) {
+      a.mask_out[row] = 0ull;
+      a.count_out[row] = 0;
+    }
+    return;
+  }
+
+  // 1. guiding probability of expert `lane`
+  double p = 0.0;
+  if (lane < a.E) {
+    if (a.blend == FM_BLEND_SCORE) {
+      double num = 0.0, den = 0.0;
+      bool any_pos = false;
+      for (int i = 0; i < a.k; ++i) {
+        int y = a.idx[static_cast<int64_t>(b) * a.k + i];
+        if (y < 0 || y >= a.n) continue;
+        double s = static_cast<double>(a.score[static_cast<int64_t>(b) * a.k + i]);
+        if (s > 0.0) any_pos = true;
+      }
+      for (int i = 0; i < a.k; ++i) {
+        int y = a.idx[static_cast<int64_t>(b) * a.k + i];
+        if (y < 0 || y >= a.n) continue;
+        double s = static_cast<double>(a.score[static_cast<int64_t>(b) * a.k + i]);
+        double wgt = any_pos ? (s > 0.0 ? s : 0.0) : 1.0;
+        num = __dadd_rn(num, __dmul_rn(wgt, stored_prob(a, y, l, lane)));
+        den = __dadd_rn(den, wgt);
+      }
+      p = __ddiv_rn(num, den);
+    } else {
+      p = stored_prob(a, y0, l, lane);
+    }
+  }
+
+  // 2. threshold
+  double tau;
+  if (a.mode == FM_TAU_DYNAMIC) {
+    const double s = static_cast<double>(a.score[static_cast<int64_t>(b) * a.k]);
+    if (s != s) tau = 1.0;
+    else {
+      double t = 1.0 - s;
+      tau = t < 0.0 ? 0.0 : (t > 1.0 ? 1.0 : t);
+    }
+  } else {
+    tau = static_cast<double>(a.tau);
+  }
+
+  // 3. rank
+  int rank = 0;
+  for (int i = 0; i < a.E; ++i) {
+    const double pi = __shfl(p, i, kWave);
+    if (i != lane && ahead(pi, i, p, lane)) ++rank;
+  }
+  if (lane < a.E) sorted[wv][rank] = p;
+  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_wave_barrier();
+
+  // 4. sequential float64 prefix sum in rank order
+  int kstar = a.E;
+  double run = 0.0;
+  for (int kk = 0; kk <= a.E; ++kk) {
+    if (run >= tau) {
+      kstar = kk;
+      break;
+    }
+    if (kk < a.E) run = __dadd_rn(run, sorted[wv][kk]);
+  }
+  int kk = kstar < a.k_min ? a.k_min : kstar;
+  kk = kk > a.k_max ? a.k_max : kk;
+  const uint64_t mask = __ballot(lane < a.E && rank < kk);
+  if (lane == 0) {
+    a.mask_out[row] = mask;
+    a.count_out[row] = static_cast<uint8_t>(kk);
+  }
+}
+
+hipError_t launch_select(const StoreView& s, const int32_t* idx, const float* score, int32_t B, int32_t k,
+                         const int32_t* lb, const int32_t* le, const fm_select_params& p, uint64_t* mask_out,
+                         uint8_t* count_out, hipStream_t st) {
+  SelArgs a;
+  a.planes = s.planes;
+  a.plane_elems = s.plane_elems;
+  a.n = s.n;
+  a.L = s.L;
+  a.E = s.E;
+  a.dtype = s.map_dtype;
+  a.idx = idx;
+  a.score = score;
+  a.B = B;
+  a.k = k;
+  a.lb = lb;
+  a.le = le;
+  a.mode = p.mode;
+  a.tau = p.tau;
+  a.k_min = p.k_min;
+  a.k_max = p.k_max;
+  a.blend = p.blend;
+  a.mask_out = mask_out;
+  a.count_out = count_out;
+  a.flags = s.flags;
+  const int64_t rows = static_cast<int64_t>(B) * s.L;
+  const int64_t blocks = (rows + 3) / 4;
+  hipLaunchKernelGGL(k_select, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace fm

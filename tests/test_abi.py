@@ -1,0 +1,99 @@
+"""The C-ABI library: it loads, exports every declared symbol, sizes buffers
+as documented and rejects invalid arguments before touching the GPU.  CPU
+only (no compute call is made)."""
+import ctypes as C
+import json
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "finemoe_map.h")
+
+
+def _lib():
+    from paper_2502_05370_amd import _lib as L
+    return L, L.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fm_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    L, lib = _lib()
+    names = declared_functions()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(lib, n), n
+        assert n in L.SIGNATURES, f"{n} has no ctypes signature"
+
+
+def test_store_footprint_matches_section_6_8():
+    L, lib = _lib()
+    g = json.load(open(os.path.join(ROOT, "tests", "golden", "models.json")))
+    cap = g["store_capacity_max"]
+    for name, m in g["models"].items():
+        got = lib.fm_map_bytes(cap, m["L"], m["E"], L.FM_F32)
+        assert got == g["fp32_map_store_bytes_at_capacity_max"][name]
+        assert lib.fm_store_bytes(cap, m["L"], m["E"], 0, L.FM_F32) < g["store_bytes_limit"]
+    assert lib.fm_map_bytes(1000, 32, 8, L.FM_BF16) == 32 * 16128
+    assert lib.fm_map_bytes(0, 32, 8, L.FM_F32) == 0
+    assert lib.fm_store_bytes(10, 4, 4, 128, 7) == 0
+
+
+def test_workspace_size():
+    L, lib = _lib()
+    assert lib.fm_workspace_bytes(1024, 8) > 1024 * 8 * 8
+    assert lib.fm_workspace_bytes(0, 1) == 0
+    assert lib.fm_workspace_bytes(16, 9) == 0
+
+
+def _build(lib, L, cap=16, Lr=4, E=8, d=0, dtype=0, buf=0x1000, nbytes=1 << 20):
+    desc = L.StoreDesc(cap, Lr, E, d, dtype, C.c_void_p(buf), nbytes)
+    h = C.c_void_p()
+    return lib.fm_store_build(C.byref(h), C.byref(desc)), h
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(cap=0), 1), (dict(Lr=0), 1), (dict(E=0), 1), (dict(E=65), 2), (dict(Lr=65), 2),
+    (dict(d=100), 2), (dict(d=-128), 1), (dict(dtype=5), 1), (dict(buf=0), 1), (dict(buf=0x1010), 1),
+    (dict(nbytes=100), 1),
+])
+def test_store_build_rejects_bad_arguments(kw, status):
+    L, lib = _lib()
+    st, h = _build(lib, L, **kw)
+    assert st == status
+    assert lib.fm_last_error().decode() != ""
+
+
+def test_null_handles_and_pointers_are_rejected():
+    L, lib = _lib()
+    assert lib.fm_store_build(None, None) == L.FM_ERR_INVALID
+    n = C.c_int32()
+    assert lib.fm_store_size(None, C.byref(n)) == L.FM_ERR_INVALID
+    assert lib.fm_store_destroy(None) == L.FM_ERR_INVALID
+    assert lib.fm_store_insert(None, None, None, 1, None, None) == L.FM_ERR_INVALID
+    p = L.SelectParams(0, 0.5, 1, 4, 0)
+    assert lib.fm_select_prefetch(None, None, None, 1, 1, None, None, C.byref(p), None, None, None) == L.FM_ERR_INVALID
+    assert lib.fm_match_semantic(None, None, 1, 1, None, None, None, 0, None) == L.FM_ERR_INVALID
+    assert lib.fm_match_trajectory(None, None, None, 1, 1, 1, None, None, None, 0, None) == L.FM_ERR_INVALID
+    assert "NULL" in lib.fm_last_error().decode()
+
+
+def test_no_device_is_a_hip_error_not_a_crash():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    L, lib = _lib()
+    st, h = _build(lib, L)
+    assert st == L.FM_ERR_HIP
+    assert "hip" in lib.fm_last_error().decode().lower()
+
+
+def test_version():
+    L, lib = _lib()
+    assert lib.fm_version() >> 16 == 1
