@@ -1,0 +1,226 @@
+"""Throughput of FineMoE expert-map matching + prefetch selection on one MI355X.
+
+One step = one pass of the whole hot path over one query batch that is
+already resident in HBM: the batched cosine search over the store (trajectory
+search, Eq. 5, and/or semantic search, Eq. 4, with ranking fused in), then the
+prefetch-set selection (Section 4.3, Eq. 6-8) for every (query, layer) row.
+
+Default workload: the Qwen1.5-MoE-shaped trajectory batch (50,000 stored maps
+of 24 x 60 float32, 64 queries with prefix depths U{1..23}, top-1, threshold
+0.8, at most 8 experts).  ``--config`` selects another workload.
+
+Prints ONE JSON line.  ``roofline`` refers to the match call (the dominant
+kernel) timed with HIP events on the stream it runs on; ``cpu_baseline`` is the
+CPU oracle timed on a bounded sample of the same batch.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_MFMA_PEAK_TFS = 2500.0    # dense bf16 MFMA
+FP32_MFMA_PEAK_TFS = 157.3     # dense fp32 MFMA
+
+# Measured HBM traffic of the dominant kernel (rocprofv3 FETCH_SIZE + WRITE_SIZE,
+# scaled by a plain copy kernel's counter reading), per launch, by workload.
+# None until counters are taken for the kernel as it stands.
+COUNTER_TRAFFIC_BYTES = {}
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    p.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle sample")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--graph", action="store_true", help="replay the step as a captured HIP graph")
+    return p.parse_args()
+
+
+def algorithmic_cost(s, a):
+    """Bytes and flops the method itself must move/compute for one batch."""
+    esz = 2 if s.map_dtype == "bf16" else 4
+    out = {"traj_bytes": 0, "traj_flops": 0, "sem_bytes": 0, "sem_flops": 0}
+    if s.B_traj:
+        d = np.clip(a["depth"], 1, s.L)
+        dmax = int(d.max())
+        out["traj_bytes"] = s.n * dmax * s.E * esz
+        out["traj_flops"] = int(2 * s.n * s.E * int(d.sum()) + 2 * s.n * dmax * s.E)
+    if s.B_sem:
+        out["sem_bytes"] = s.n * s.d_emb * 2 + 4 * s.n
+        out["sem_flops"] = 2 * s.B_sem * s.n * s.d_emb
+    return out
+
+
+def cpu_baseline(s, a, gpu_idx, budget_s):
+    """Oracle on a bounded sample of the batch: whole store, first queries."""
+    import oracle
+    from threadpoolctl import threadpool_info
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    rows = []
+    t_total = 0.0
+    mism = 0
+    order = list(range(s.B_sem)) + list(range(s.B_sem, s.B))
+    # alternate semantic and trajectory queries when both exist
+    if s.B_sem and s.B_traj:
+        order = [r for pair in zip(range(s.B_sem), range(s.B_sem, s.B)) for r in pair]
+    for r in order:
+        t0 = time.perf_counter()
+        if r < s.B_sem:
+            i, sc = oracle.match_semantic(a["embs"], a["q_sem"][r:r + 1], s.k)
+        else:
+            b = r - s.B_sem
+            i, sc = oracle.match_trajectory(a["maps"], s.map_dtype, a["q_traj"][b:b + 1], a["depth"][b:b + 1], s.k)
+        m, c = oracle.select_prefetch(a["maps"], s.map_dtype, i, sc, a["lb"][r:r + 1], a["le"][r:r + 1],
+                                      s.tau_mode, s.tau, s.k_min, s.k_max, s.blend)
+        t_total += time.perf_counter() - t0
+        rows.append(r)
+        if int(i[0, 0]) != int(gpu_idx[r, 0]):
+            mism += 1
+        if t_total >= budget_s:
+            break
+    return {"value": len(rows) / t_total, "unit": "queries/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{len(rows)} of {s.B} queries against the full {s.n}-map store, timed one query at a time",
+            "top1_index_mismatches_vs_gpu": mism}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}); "
+              "the store would shard by rows across GPUs but that path is not built", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    import paper_2502_05370_amd as fm
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from parity import to_device
+
+    s = synth.spec(args.config)
+    a = synth.generate(s)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    store = fm.Store(s.n, s.L, s.E, s.d_emb, s.map_dtype, device=dev)
+    store.insert(to_device(a["maps"], s.map_dtype), to_device(a["embs"], "bf16") if s.d_emb else None)
+    ws_sem = fm.Workspace(device=dev)
+    ws_traj = fm.Workspace(device=dev)
+    q_sem = to_device(a["q_sem"], "bf16") if s.B_sem else None
+    q_traj = to_device(a["q_traj"], s.map_dtype) if s.B_traj else None
+    depth = to_device(a["depth"], "i32") if s.B_traj else None
+    lb = to_device(a["lb"], "i32")
+    le = to_device(a["le"], "i32")
+    idx = torch.empty((s.B, s.k), dtype=torch.int32, device=dev)
+    score = torch.empty((s.B, s.k), dtype=torch.float32, device=dev)
+    mask = torch.empty((s.B, s.L), dtype=torch.int64, device=dev)
+    count = torch.empty((s.B, s.L), dtype=torch.uint8, device=dev)
+    max_depth = int(np.clip(a["depth"], 1, s.L).max()) if s.B_traj else s.L
+    stream = torch.cuda.current_stream()
+
+    def match():
+        if s.B_sem:
+            fm.match_semantic(store, q_sem, s.k, out=(idx[:s.B_sem], score[:s.B_sem]), workspace=ws_sem,
+                              stream=stream)
+        if s.B_traj:
+            fm.match_trajectory(store, q_traj, depth, s.k, max_depth=max_depth,
+                                out=(idx[s.B_sem:], score[s.B_sem:]), workspace=ws_traj, stream=stream)
+
+    def select():
+        fm.select_prefetch(store, idx, score, lb, le, tau=s.tau, k_min=s.k_min, k_max=s.k_max,
+                           mode=s.tau_mode, blend=s.blend, out=(mask, count), stream=stream)
+
+    for _ in range(args.warmup):
+        match()
+        select()
+    torch.cuda.synchronize()
+
+    graph = None
+    if args.graph:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            match()
+            select()
+        torch.cuda.synchronize()
+
+    # Timed region: K steps; HIP events bracket the match call of every step
+    # on the stream the kernels run on.
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        if graph is not None:
+            ev[i][0].record(stream)
+            graph.replay()
+            ev[i][1].record(stream)
+        else:
+            ev[i][0].record(stream)
+            match()
+            ev[i][1].record(stream)
+            select()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    elapsed = t1 - t0
+    match_ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
+
+    cost = algorithmic_cost(s, a)
+    if s.B_sem and not s.B_traj:
+        # semantic-only: balanced, report against HBM (the binding roofline at this shape)
+        achieved = cost["sem_bytes"] / (match_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS}
+        roof_kernel = "k_sem_scan"
+    elif s.config_no == 4:
+        achieved = cost["traj_flops"] / (match_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": FP32_MFMA_PEAK_TFS, "unit": "TFLOP/s",
+                "frac": achieved / FP32_MFMA_PEAK_TFS}
+        roof_kernel = "k_traj_scan"
+    else:
+        byts = cost["traj_bytes"] + cost["sem_bytes"]
+        achieved = byts / (match_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS}
+        roof_kernel = "k_traj_scan" if s.B_traj else "k_sem_scan"
+    roof["traffic"] = COUNTER_TRAFFIC_BYTES.get(s.name)
+    roof["kernel"] = roof_kernel
+    roof["duration_us"] = match_ms * 1e3
+    roof["algorithmic_bytes"] = cost["traj_bytes"] + cost["sem_bytes"]
+    roof["algorithmic_flops"] = cost["traj_flops"] + cost["sem_flops"]
+
+    value = s.B * args.steps / elapsed
+    gpu_idx = idx.cpu().numpy()
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(s, a, gpu_idx, args.cpu_seconds)
+
+    line = {
+        "metric": "expert-map queries/sec (match + prefetch select) at 1 GPU; % HBM/MFMA peak",
+        "value": value, "unit": "queries/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": elapsed / args.steps * 1e3, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32" if s.map_dtype == "f32" and not s.B_sem else
+        ("bf16" if s.map_dtype == "bf16" or not s.B_traj else "f32+bf16"),
+        "data": "synthetic",
+        "config": {"workload": s.name, "store_maps": s.n, "layers": s.L, "experts": s.E,
+                   "map_dtype": s.map_dtype, "d_emb": s.d_emb, "batch": s.B, "batch_semantic": s.B_sem,
+                   "batch_trajectory": s.B_traj, "top_k": s.k, "tau": s.tau, "k_max": s.k_max,
+                   "graph": bool(args.graph)},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -106,9 +106,11 @@ size_t fm_map_bytes(int32_t cap, int32_t L, int32_t E, fm_dtype map_dtype);
 size_t fm_store_bytes(int32_t cap, int32_t L, int32_t E, int32_t d_emb, fm_dtype map_dtype);
 
 /* Bytes of match workspace for batches of up to B_max queries keeping up to
- * k_max matches each.  The workspace must be zero-filled before its first use;
- * every completed match call leaves it zero-filled again.  Calls that share a
- * workspace must be ordered (same stream, or synchronised). */
+ * k_max matches each (device memory, 256-byte aligned, owned by the caller).
+ * It holds the cross-workgroup top-k lists and a completion counter.  It must
+ * be zero-filled once before its first use; every completed match call leaves
+ * it zero-filled again.  Calls that share a workspace must be ordered (same
+ * stream, or synchronised); concurrent calls on one workspace race. */
 size_t fm_workspace_bytes(int32_t B_max, int32_t k_max);
 
 /* Create a host handle over a caller-owned device buffer (Expert Map Store,

@@ -64,13 +64,15 @@ def workspace_bytes(B_max: int, k_max: int) -> int:
 
 
 class Workspace:
-    """Device scratch for match calls (contents need no initialisation)."""
+    """Device scratch for match calls: zero-filled here, and every completed
+    call leaves it zero-filled.  Calls sharing one workspace must be ordered."""
 
     def __init__(self, B_max: int = 1024, k_max: int = 8, device="cuda"):
         self.nbytes = workspace_bytes(B_max, k_max)
         if self.nbytes == 0:
             raise ValueError(f"invalid workspace request B_max={B_max} k_max={k_max}")
         self.buf = _aligned_bytes(self.nbytes, device)
+        self.buf.zero_()
 
     @property
     def ptr(self):
@@ -99,8 +101,8 @@ class Store:
 
     def __del__(self):
         h = getattr(self, "handle", None)
-        if h is not None and h.value:
-            _lib.load().fm_store_destroy(h)
+        if h is not None and h.value and _lib is not None and _lib._LIB is not None:
+            _lib._LIB.fm_store_destroy(h)
             self.handle = None
 
     @property

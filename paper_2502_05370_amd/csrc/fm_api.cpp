@@ -69,12 +69,7 @@ struct fm_store {
 namespace fm {
 
 size_t workspace_bytes_needed() {
-  size_t b = 0;
-  b += align_up(sizeof(uint64_t) * kChunkB * kMaxK, kAlign);
-  b += kAlign;  // counter
-  b += align_up(sizeof(int32_t) * kChunkB, kAlign) * 2;
-  b += align_up(sizeof(float) * kChunkB, kAlign);
-  return b;
+  return align_up(sizeof(uint64_t) * kChunkB * kMaxK, kAlign) + kAlign;
 }
 
 Workspace carve_workspace(void* base) {
@@ -83,12 +78,6 @@ Workspace carve_workspace(void* base) {
   w.keys = reinterpret_cast<uint64_t*>(p);
   p += align_up(sizeof(uint64_t) * kChunkB * kMaxK, kAlign);
   w.counter = reinterpret_cast<uint32_t*>(p);
-  p += kAlign;
-  w.perm = reinterpret_cast<int32_t*>(p);
-  p += align_up(sizeof(int32_t) * kChunkB, kAlign);
-  w.sdepth = reinterpret_cast<int32_t*>(p);
-  p += align_up(sizeof(int32_t) * kChunkB, kAlign);
-  w.rq = reinterpret_cast<float*>(p);
   return w;
 }
 

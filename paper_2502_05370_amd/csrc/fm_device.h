@@ -81,16 +81,19 @@ struct TopK {
 
 // Insert a descending list of candidate keys into a global top-k list
 // (k slots, descending, 0 = empty) shared by all workgroups.  Each slot only
-// grows; a displaced key moves to the next slot.  The final contents are the
-// k largest keys ever offered, independent of arrival order.
-__device__ __forceinline__ void global_topk_insert(uint64_t* slots, int k, const uint64_t* cand, int ncand) {
-  for (int c = 0; c < ncand; ++c) {
+// grows; a displaced key moves on to the next slot.  The final contents are
+// the k largest keys ever offered, whatever the arrival order.
+template <int KTOP>
+__device__ __forceinline__ void global_topk_insert(uint64_t* slots, int k, const uint64_t (&cand)[KTOP]) {
+#pragma unroll
+  for (int c = 0; c < KTOP; ++c) {
+    if (c >= k) return;
     uint64_t carry = cand[c];
     if (carry == 0) return;
-    uint64_t last = __hip_atomic_load(slots + (k - 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (carry <= last) return;  // list is descending: later candidates are smaller still
+    const uint64_t last = __hip_atomic_load(slots + (k - 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (carry <= last) return;  // the list is descending: later candidates are smaller still
     for (int j = 0; j < k && carry != 0; ++j) {
-      uint64_t old = __hip_atomic_fetch_max(slots + j, carry, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const uint64_t old = __hip_atomic_fetch_max(slots + j, carry, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       carry = old < carry ? old : carry;
     }
   }

@@ -29,13 +29,12 @@ struct StoreView {
   fm_dtype map_dtype;
 };
 
-// Layout of the per-call match workspace (byte offsets).
+// Match workspace: the global top-k lists of one launch and its completion
+// counter.  Zero between calls: the last workgroup of every launch clears
+// what the launch used.
 struct Workspace {
-  uint64_t* keys;     // [kChunkB][kMaxK] packed (score, index) keys
-  uint32_t* counter;  // [4] completion counter and spare words
-  int32_t* perm;      // [kChunkB] query index at each depth-sorted position
-  int32_t* sdepth;    // [kChunkB] clamped depth at each sorted position
-  float* rq;          // [kChunkB] 1 / |query| (0 for a zero query), by original index
+  uint64_t* keys;     // [kChunkB][kMaxK] packed (score, index) keys, 0 = empty
+  uint32_t* counter;  // workgroups finished in the current launch
 };
 size_t workspace_bytes_needed();
 Workspace carve_workspace(void* base);

@@ -5,15 +5,16 @@
 // contraction over the hidden size, so it runs on bf16 MFMA
 // (v_mfma_f32_16x16x32_bf16: exact bf16 products, float32 accumulation):
 //
-//   k_sem_prep  computes 1/|q[b]| in float64 and clears the result keys.
 //   k_sem_scan  each workgroup owns a 128-map x (16*TQ)-query output tile
 //               and walks the hidden dimension in chunks of 64, staging both
 //               operands in LDS.  Four waves split the tile 2 x 2 (or 4 x 1
 //               for a single query tile).  The epilogue scales by the stored
 //               norms, keeps a per-lane top-K, merges it across the
 //               workgroup and inserts it into the global top-k list; the last
-//               workgroup to finish writes idx/score.  The B x n score matrix
-//               is never written (except into the optional debug output).
+//               workgroup to finish writes idx/score and clears the list.
+//               Query norms are summed in float64 from the staged chunks.  The
+//               B x n score matrix is never written (except into the optional
+//               debug output).
 #include "fm_device.h"
 #include "fm_internal.h"
 
@@ -40,34 +41,6 @@ struct SemArgs {
 };
 
 }  // namespace
-
-__global__ void __launch_bounds__(256) k_sem_prep(const uint16_t* __restrict__ q, int32_t B, int32_t d,
-                                                  Workspace ws) {
-  const int tid = threadIdx.x;
-  if (blockIdx.x == 0) {
-    for (int i = tid; i < kChunkB * kMaxK; i += 256) ws.keys[i] = 0ull;
-    if (tid == 0) ws.counter[0] = 0u;
-    return;
-  }
-  const int lane = tid % kWave;
-  const int b = (blockIdx.x - 1) * kWaves + tid / kWave;
-  if (b >= B) return;
-  const uint16_t* row = q + static_cast<int64_t>(b) * d;
-  double acc = 0.0;
-  for (int j = lane; j < d; j += kWave) {
-    double v = static_cast<double>(bf16_to_f32(row[j]));
-    acc += v * v;
-  }
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, kWave);
-  if (lane == 0) {
-    float r;
-    if (acc != acc) r = __uint_as_float(0x7fc00000u);
-    else if (acc == 0.0) r = 0.0f;
-    else r = static_cast<float>(1.0 / sqrt(acc));
-    ws.rq[b] = r;
-  }
-}
 
 template <int TQ, int WN, int KTOP>
 __global__ void __launch_bounds__(256) k_sem_scan(SemArgs a) {
@@ -101,7 +74,7 @@ __global__ void __launch_bounds__(256) k_sem_scan(SemArgs a) {
   const int y0 = tile * kTileMaps;
   const int b0 = qgrp * QT;
 
-  for (int r = tid; r < QT; r += kThreads) grq[r] = (active && b0 + r < a.B) ? a.ws.rq[b0 + r] : 0.0f;
+  for (int r = tid; r < QT; r += kThreads) grq[r] = 0.0f;
 
   TopK<KTOP> best[NBW];
 #pragma unroll
@@ -117,6 +90,9 @@ __global__ void __launch_bounds__(256) k_sem_scan(SemArgs a) {
     // Register prefetch of one chunk of both operands.
     u16x8 xr[XU];
     u16x8 qr[QU];
+    double qn2[QU];
+#pragma unroll
+    for (int i = 0; i < QU; ++i) qn2[i] = 0.0;
     auto load_chunk = [&](int kc) {
 #pragma unroll
       for (int i = 0; i < XU; ++i) {
@@ -153,6 +129,11 @@ __global__ void __launch_bounds__(256) k_sem_scan(SemArgs a) {
         int row = unit / (kChunk / 8);
         int part = unit % (kChunk / 8);
         if (row < QT) *reinterpret_cast<u16x8*>(qs + row * kRow + part * 8) = qr[i];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const double f = static_cast<double>(bf16_to_f32(qr[i][j]));
+          qn2[i] += f * f;
+        }
       }
     };
 
@@ -178,6 +159,25 @@ __global__ void __launch_bounds__(256) k_sem_scan(SemArgs a) {
       }
       __syncthreads();
     }
+
+    // query norms: the 8 parts of a row sit in 8 consecutive lanes (fixed order)
+#pragma unroll
+    for (int i = 0; i < QU; ++i) {
+      double v = qn2[i];
+      v += __shfl_xor(v, 1, kWave);
+      v += __shfl_xor(v, 2, kWave);
+      v += __shfl_xor(v, 4, kWave);
+      const int unit = tid + i * kThreads;
+      const int row = unit / (kChunk / 8);
+      if (row < QT && unit % (kChunk / 8) == 0) {
+        float r;
+        if (v != v) r = __uint_as_float(0x7fc00000u);
+        else if (v == 0.0) r = 0.0f;
+        else r = static_cast<float>(1.0 / sqrt(v));
+        grq[row] = r;
+      }
+    }
+    __syncthreads();
 
     // Epilogue: lane (g, c) holds maps 4g+i of each 16-map block for query c of each query block.
 #pragma unroll
@@ -223,7 +223,7 @@ __global__ void __launch_bounds__(256) k_sem_scan(SemArgs a) {
     m.clear();
 #pragma unroll
     for (int ww = 0; ww < WM; ++ww) m.merge(&mbuf[ww][r][0]);
-    global_topk_insert(a.ws.keys + static_cast<int64_t>(b0 + r) * kMaxK, a.k, m.v, KTOP < a.k ? KTOP : a.k);
+    global_topk_insert<KTOP>(a.ws.keys + static_cast<int64_t>(b0 + r) * kMaxK, a.k, m.v);
   }
 
   __threadfence();
@@ -233,16 +233,20 @@ __global__ void __launch_bounds__(256) k_sem_scan(SemArgs a) {
     s_last = (ticket == static_cast<uint32_t>(a.grid - 1)) ? 1 : 0;
   }
   __syncthreads();
-  if (s_last && a.idx_out != nullptr) {
+  if (s_last) {
     __threadfence();
     for (int i = tid; i < a.B * a.k; i += kThreads) {
-      int b = i / a.k;
-      int j = i - b * a.k;
-      uint64_t key = __hip_atomic_load(a.ws.keys + static_cast<int64_t>(b) * kMaxK + j, __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT);
-      a.idx_out[i] = key_index(key);
-      a.score_out[i] = key_score(key);
+      const int b = i / a.k;
+      const int j = i - b * a.k;
+      uint64_t* slot = a.ws.keys + static_cast<int64_t>(b) * kMaxK + j;
+      const uint64_t key = __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (a.idx_out != nullptr) {
+        a.idx_out[i] = key_index(key);
+        a.score_out[i] = key_score(key);
+      }
+      __hip_atomic_store(slot, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+    if (tid == 0) __hip_atomic_store(a.ws.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
@@ -259,9 +263,7 @@ hipError_t launch_match_semantic(const StoreView& s, const void* q, int32_t B, i
   for (int b0 = 0; b0 < B; b0 += kChunkB) {
     const int Bc = (B - b0) < kChunkB ? (B - b0) : kChunkB;
     const uint16_t* qc = static_cast<const uint16_t*>(q) + static_cast<int64_t>(b0) * s.d_emb;
-    hipLaunchKernelGGL(k_sem_prep, dim3(1 + (Bc + kWaves - 1) / kWaves), dim3(256), 0, st, qc, Bc, s.d_emb, ws);
-    hipError_t err = hipGetLastError();
-    if (err != hipSuccess) return err;
+    hipError_t err = hipSuccess;
     int TQ = 1;
     while (16 * TQ < Bc && TQ < tq_max) TQ *= 2;
     const int n_qg = (Bc + 16 * TQ - 1) / (16 * TQ);
