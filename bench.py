@@ -116,8 +116,8 @@ def main():
 
     store = fm.Store(s.n, s.L, s.E, s.d_emb, s.map_dtype, device=dev)
     store.insert(to_device(a["maps"], s.map_dtype), to_device(a["embs"], "bf16") if s.d_emb else None)
-    ws_sem = fm.Workspace(device=dev)
-    ws_traj = fm.Workspace(device=dev)
+    ws_sem = fm.Workspace(store)
+    ws_traj = fm.Workspace(store)
     q_sem = to_device(a["q_sem"], "bf16") if s.B_sem else None
     q_traj = to_device(a["q_traj"], s.map_dtype) if s.B_traj else None
     depth = to_device(a["depth"], "i32") if s.B_traj else None

@@ -105,20 +105,26 @@ size_t fm_map_bytes(int32_t cap, int32_t L, int32_t E, fm_dtype map_dtype);
  * each part 256-byte aligned.  Returns 0 for invalid sizes. */
 size_t fm_store_bytes(int32_t cap, int32_t L, int32_t E, int32_t d_emb, fm_dtype map_dtype);
 
-/* Bytes of match workspace for batches of up to B_max queries keeping up to
- * k_max matches each (device memory, 256-byte aligned, owned by the caller).
- * It holds the cross-workgroup top-k lists and a completion counter.  It must
- * be zero-filled once before its first use; every completed match call leaves
- * it zero-filled again.  Calls that share a workspace must be ordered (same
- * stream, or synchronised); concurrent calls on one workspace race. */
-size_t fm_workspace_bytes(int32_t B_max, int32_t k_max);
+/* Bytes of match workspace for a store of L layers of E experts (map_dtype)
+ * and batches of up to B_max queries keeping up to k_max matches each (device
+ * memory, 256-byte aligned, owned by the caller).  It holds the staged,
+ * depth-sorted query rows, the per-workgroup partial top-k lists, and the
+ * top-k slots and completion counter of the semantic scan.  It must be
+ * zero-filled once before its first use; every completed match call leaves
+ * the slots and the counter zero again.  Calls that share a workspace must be
+ * ordered (same stream, or synchronised); concurrent calls on one workspace
+ * race.  Returns 0 for invalid arguments. */
+size_t fm_workspace_bytes(int32_t L, int32_t E, fm_dtype map_dtype, int32_t B_max, int32_t k_max);
 
 /* Create a host handle over a caller-owned device buffer (Expert Map Store,
  * Section 4.4).  The store starts empty.  The buffer contents are not read;
  * the current HIP device at this call is the store's device.  Errors:
  * FM_ERR_INVALID for NULL pointers, out-of-range sizes or a short or
- * misaligned buffer; FM_ERR_UNSUPPORTED for E or L above 64 or a d_emb that is
- * not a multiple of 128. */
+ * misaligned buffer; FM_ERR_UNSUPPORTED for E or L above 64, a d_emb that is
+ * not a multiple of 128, or map planes so large that one group of layer
+ * planes scanned together (32/E planes when E in {8, 16, 32}, else one)
+ * exceeds 0xF0000000 bytes (e.g. cap above ~15.7 million maps of 64 float32
+ * experts). */
 fm_status fm_store_build(fm_store** out, const fm_store_desc* desc);
 
 /* Append n iterations (Step 5 of Section 3.2: new expert maps enter the

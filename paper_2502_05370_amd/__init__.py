@@ -59,18 +59,19 @@ def store_bytes(cap: int, L: int, E: int, d_emb: int = 0, map_dtype: str = "f32"
     return int(_lib.load().fm_store_bytes(cap, L, E, d_emb, _DTYPES[map_dtype]))
 
 
-def workspace_bytes(B_max: int, k_max: int) -> int:
-    return int(_lib.load().fm_workspace_bytes(B_max, k_max))
+def workspace_bytes(L: int, E: int, map_dtype: str = "f32", B_max: int = 1024, k_max: int = 8) -> int:
+    return int(_lib.load().fm_workspace_bytes(L, E, _DTYPES[map_dtype], B_max, k_max))
 
 
 class Workspace:
     """Device scratch for match calls: zero-filled here, and every completed
     call leaves it zero-filled.  Calls sharing one workspace must be ordered."""
 
-    def __init__(self, B_max: int = 1024, k_max: int = 8, device="cuda"):
-        self.nbytes = workspace_bytes(B_max, k_max)
+    def __init__(self, store: "Store", B_max: int = 1024, k_max: int = 8, device=None):
+        self.nbytes = workspace_bytes(store.L, store.E, store.map_dtype, B_max, k_max)
         if self.nbytes == 0:
             raise ValueError(f"invalid workspace request B_max={B_max} k_max={k_max}")
+        device = store.device if device is None else device
         self.buf = _aligned_bytes(self.nbytes, device)
         self.buf.zero_()
 
@@ -139,7 +140,7 @@ class Store:
 
     def ensure_workspace(self) -> Workspace:
         if self.workspace is None:
-            self.workspace = Workspace(device=self.device)
+            self.workspace = Workspace(self)
         return self.workspace
 
 

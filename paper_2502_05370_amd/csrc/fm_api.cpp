@@ -38,6 +38,8 @@ size_t elem_size(fm_dtype t) { return t == FM_BF16 ? 2 : 4; }
 
 bool valid_dtype(int t) { return t == FM_F32 || t == FM_BF16; }
 
+constexpr size_t kMaxGroupBytes = 0xF0000000u;
+
 struct Layout {
   size_t plane_bytes, maps, embs, norms, flags, total;
   int64_t plane_elems;
@@ -66,18 +68,52 @@ struct fm_store {
   int device;
 };
 
-namespace fm {
+namespace {
 
-size_t workspace_bytes_needed() {
-  return align_up(sizeof(uint64_t) * kChunkB * kMaxK, kAlign) + kAlign;
+fm_status check_workspace(const fm_store* s, void* ws, size_t bytes) {
+  if (ws == nullptr) return fail(FM_ERR_INVALID, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % fm::kAlign != 0)
+    return fail(FM_ERR_INVALID, "workspace must be %zu-byte aligned", fm::kAlign);
+  const size_t need = fm::workspace_bytes_needed(s->v.L, s->v.E, s->v.map_dtype);
+  if (bytes < need) return fail(FM_ERR_INVALID, "workspace of %zu bytes is smaller than the %zu bytes required", bytes, need);
+  return FM_OK;
 }
 
-Workspace carve_workspace(void* base) {
+fm::Workspace carve(const fm_store* s, void* ws) { return fm::carve_workspace(ws, s->v.L, s->v.E, s->v.map_dtype); }
+
+}  // namespace
+
+namespace fm {
+
+// Workspace layout: [keys][counter][partial][perm][sdep][rq][qrows], each
+// part 256-byte aligned.
+size_t workspace_bytes_needed(int32_t L, int32_t E, fm_dtype map_dtype) {
+  size_t b = align_up(sizeof(uint64_t) * kChunkB * kMaxK, kAlign) + kAlign;
+  b += align_up(sizeof(uint64_t) * kChunkB * kMaxPartials * kMaxK, kAlign);
+  b += 3 * align_up(sizeof(int32_t) * kChunkB, kAlign);
+  b += align_up(traj_qrows_bytes(L, E, map_dtype, kChunkB), kAlign);
+  return b;
+}
+
+Workspace carve_workspace(void* base, int32_t L, int32_t E, fm_dtype map_dtype) {
+  (void)L;
+  (void)E;
+  (void)map_dtype;
   char* p = static_cast<char*>(base);
   Workspace w;
   w.keys = reinterpret_cast<uint64_t*>(p);
   p += align_up(sizeof(uint64_t) * kChunkB * kMaxK, kAlign);
   w.counter = reinterpret_cast<uint32_t*>(p);
+  p += kAlign;
+  w.partial = reinterpret_cast<uint64_t*>(p);
+  p += align_up(sizeof(uint64_t) * kChunkB * kMaxPartials * kMaxK, kAlign);
+  w.perm = reinterpret_cast<int32_t*>(p);
+  p += align_up(sizeof(int32_t) * kChunkB, kAlign);
+  w.sdep = reinterpret_cast<int32_t*>(p);
+  p += align_up(sizeof(int32_t) * kChunkB, kAlign);
+  w.rq = reinterpret_cast<float*>(p);
+  p += align_up(sizeof(float) * kChunkB, kAlign);
+  w.qrows = p;
   return w;
 }
 
@@ -90,15 +126,7 @@ fm_status check_store(const fm_store* s) {
   return FM_OK;
 }
 
-fm_status check_workspace(void* ws, size_t bytes) {
-  if (ws == nullptr) return fail(FM_ERR_INVALID, "workspace is NULL");
-  if (reinterpret_cast<uintptr_t>(ws) % fm::kAlign != 0)
-    return fail(FM_ERR_INVALID, "workspace must be %zu-byte aligned", fm::kAlign);
-  if (bytes < fm::workspace_bytes_needed())
-    return fail(FM_ERR_INVALID, "workspace of %zu bytes is smaller than the %zu bytes required", bytes,
-                fm::workspace_bytes_needed());
-  return FM_OK;
-}
+fm_status check_workspace(const fm_store* s, void* ws, size_t bytes);
 
 // The kernels run on the store's device; make it current for the enqueue.
 struct DeviceGuard {
@@ -137,9 +165,10 @@ size_t fm_store_bytes(int32_t cap, int32_t L, int32_t E, int32_t d_emb, fm_dtype
   return ly.total;
 }
 
-size_t fm_workspace_bytes(int32_t B_max, int32_t k_max) {
+size_t fm_workspace_bytes(int32_t L, int32_t E, fm_dtype map_dtype, int32_t B_max, int32_t k_max) {
+  if (L < 1 || L > fm::kMaxL || E < 1 || E > fm::kMaxE || !valid_dtype(map_dtype)) return 0;
   if (B_max < 1 || k_max < 1 || k_max > fm::kMaxK) return 0;
-  return fm::workspace_bytes_needed();
+  return fm::workspace_bytes_needed(L, E, map_dtype);
 }
 
 fm_status fm_store_build(fm_store** out, const fm_store_desc* d) {
@@ -155,6 +184,12 @@ fm_status fm_store_build(fm_store** out, const fm_store_desc* d) {
     return fail(FM_ERR_UNSUPPORTED, "cap*E exceeds 2^31-1");
   Layout ly;
   make_layout(d->cap, d->L, d->E, d->d_emb, d->map_dtype, &ly);
+  // The trajectory scan addresses one group of up to 32/E layer planes with
+  // 32-bit byte offsets.
+  const size_t group_planes = (d->E >= 8 && 32 % d->E == 0) ? static_cast<size_t>(32 / d->E) : 1;
+  if (ly.plane_bytes * group_planes > kMaxGroupBytes)
+    return fail(FM_ERR_UNSUPPORTED, "cap=%d: %zu bytes per layer group of map planes exceed %zu", d->cap,
+                ly.plane_bytes * group_planes, kMaxGroupBytes);
   if (d->buffer == nullptr) return fail(FM_ERR_INVALID, "buffer is NULL");
   if (reinterpret_cast<uintptr_t>(d->buffer) % fm::kAlign != 0)
     return fail(FM_ERR_INVALID, "buffer must be %zu-byte aligned", fm::kAlign);
@@ -241,7 +276,7 @@ static fm_status check_match_common(const fm_store* s, int32_t B, int32_t k, con
   if (B < 1 || B > 65536) return fail(FM_ERR_INVALID, "B=%d outside [1, 65536]", B);
   if (k < 1 || k > fm::kMaxK) return fail(FM_ERR_INVALID, "k=%d outside [1, %d]", k, fm::kMaxK);
   if (idx_out == nullptr || score_out == nullptr) return fail(FM_ERR_INVALID, "idx_out and score_out must be non-NULL");
-  return check_workspace(ws, ws_bytes);
+  return check_workspace(s, ws, ws_bytes);
 }
 
 fm_status fm_match_semantic(const fm_store* s, const void* q, int32_t B, int32_t k, int32_t* idx_out,
@@ -251,7 +286,7 @@ fm_status fm_match_semantic(const fm_store* s, const void* q, int32_t B, int32_t
   if (s->v.d_emb == 0) return fail(FM_ERR_INVALID, "store has no embeddings (d_emb = 0)");
   DeviceGuard dg(s->device);
   if (!dg.ok) return fail(FM_ERR_HIP, "cannot select the store's device %d", s->device);
-  hipError_t e = fm::launch_match_semantic(s->v, q, B, k, idx_out, score_out, nullptr, fm::carve_workspace(ws),
+  hipError_t e = fm::launch_match_semantic(s->v, q, B, k, idx_out, score_out, nullptr, carve(s, ws),
                                            static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "semantic match launch");
   return ok();
@@ -267,7 +302,7 @@ fm_status fm_match_trajectory(const fm_store* s, const void* q, const int32_t* d
   DeviceGuard dg(s->device);
   if (!dg.ok) return fail(FM_ERR_HIP, "cannot select the store's device %d", s->device);
   hipError_t e = fm::launch_match_trajectory(s->v, q, depth, max_depth, B, k, idx_out, score_out, nullptr,
-                                             fm::carve_workspace(ws), static_cast<hipStream_t>(stream));
+                                             carve(s, ws), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "trajectory match launch");
   return ok();
 }
@@ -301,10 +336,10 @@ fm_status fm_debug_scores(const fm_store* s, const void* q, const int32_t* depth
   if ((q == nullptr) == (q_sem == nullptr)) return fail(FM_ERR_INVALID, "exactly one of q and q_sem must be non-NULL");
   if (B < 1 || B > 65536) return fail(FM_ERR_INVALID, "B=%d outside [1, 65536]", B);
   if (scores_out == nullptr) return fail(FM_ERR_INVALID, "scores_out is NULL");
-  if (fm_status st = check_workspace(ws, ws_bytes)) return st;
+  if (fm_status st = check_workspace(s, ws, ws_bytes)) return st;
   if (s->v.n == 0) return ok();
   // Same kernels as the match calls; only the dense score output is written.
-  fm::Workspace w = fm::carve_workspace(ws);
+  fm::Workspace w = carve(s, ws);
   DeviceGuard dg(s->device);
   if (!dg.ok) return fail(FM_ERR_HIP, "cannot select the store's device %d", s->device);
   hipStream_t st = static_cast<hipStream_t>(stream);

@@ -14,6 +14,7 @@ constexpr int kMaxL = 64;            // layers per map
 constexpr int kMaxE = 64;            // experts per layer (mask width)
 constexpr int kMaxK = 8;             // matches kept per query
 constexpr int kChunkB = 1024;        // queries per scan launch
+constexpr int kMaxPartials = 256;    // partial top-k lists per query (workgroups per query group)
 constexpr size_t kAlign = 256;
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -35,9 +36,15 @@ struct StoreView {
 struct Workspace {
   uint64_t* keys;     // [kChunkB][kMaxK] packed (score, index) keys, 0 = empty
   uint32_t* counter;  // workgroups finished in the current launch
+  uint64_t* partial;  // [kChunkB][kMaxPartials][kMaxK] per-workgroup top-k keys
+  int32_t* perm;      // [kChunkB] query index at each depth-sorted position (-1: padding)
+  int32_t* sdep;      // [kChunkB] clamped depth at each position (0: padding)
+  float* rq;          // [kChunkB] 1/|query prefix| at each position
+  void* qrows;        // staged query rows of every layer group (trajectory)
 };
-size_t workspace_bytes_needed();
-Workspace carve_workspace(void* base);
+size_t workspace_bytes_needed(int32_t L, int32_t E, fm_dtype map_dtype);
+Workspace carve_workspace(void* base, int32_t L, int32_t E, fm_dtype map_dtype);
+size_t traj_qrows_bytes(int L, int E, fm_dtype dt, int b_pad);
 
 // Launchers (return hipSuccess or the first HIP error).
 hipError_t launch_insert(const StoreView& s, const void* maps, const void* embs, int32_t n_new,

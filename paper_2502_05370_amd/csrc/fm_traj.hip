@@ -2,33 +2,34 @@
 //
 // Query b has observed the gate distributions of its first p_b layers; its
 // score against stored iteration y is the cosine between the flattened
-// prefixes q[b][0:p_b] and x[y][0:p_b].  One kernel launch serves a batch of
-// up to 1024 queries with a single pass over the layer-major store planes:
+// prefixes q[b][0:p_b] and x[y][0:p_b].  A batch of up to 1024 queries is
+// served by three launches and one pass over the layer-major store planes:
 //
-//  * Every workgroup sorts the batch by depth (deepest first, stable, hence
-//    the same order in every workgroup) and takes one group of 16*TQ queries
-//    and one slice of 64*NBA stored maps (4 waves x NBA blocks of 16 maps).
-//  * The contraction runs over "slots": each layer's E experts padded to a
-//    multiple of 32, or LPG = 32/E layers per 32 slots when E divides 32.
-//    A query tile (16 queries) stops at the layer group of its deepest
-//    member, and rows beyond each query's own depth are staged as zeros, so
-//    each query is scored on exactly its own prefix.
-//  * Map rows go straight from HBM into registers (each wave owns its maps);
-//    query rows are staged in LDS once per layer group for all four waves.
-//    The next layer group's loads are in flight while the MFMAs of the
-//    current one run.
-//  * Products use v_mfma_f32_16x16x32_bf16.  A float32 value a is split into
-//    three bf16 parts a = a1 + a2 + a3 + r, |r| <= 2^-27 |a| (round to
-//    nearest at each step), and a.b is accumulated as the six terms
-//    a1b1 + a1b2 + a2b1 + a1b3 + a2b2 + a3b1 (every dropped term is below
-//    2^-25 |ab|) in float32 accumulators.  bf16 stores take one MFMA.
-//  * Squared map-row norms come from the same loaded float32 values, giving
-//    every map's prefix norm at every depth; query norms are summed in
-//    float64 while staging.
-//  * The epilogue forms the cosine, keeps a per-lane top-K of packed
-//    (score, index) keys, merges it across the workgroup and inserts it into
-//    the global top-k list (monotone atomic-max slots).  The last workgroup
-//    to finish writes idx/score and clears the list and the counter.
+//  k_traj_prep      sorts the batch by depth (deepest first, stable), writes
+//                   1/|q[b][0:p_b]| (float64 sum) and, for every "layer
+//                   group", the sorted query rows as MFMA-ready bf16 planes
+//                   (three parts of each float32 value, one plane for bf16
+//                   stores), zero beyond each query's depth and padded, so
+//                   the scan copies them verbatim.
+//  k_traj_scan      workgroup = one group of 16*TQ sorted queries x a range
+//                   of map slices (64*NBA maps each).  Map rows and query rows
+//                   of upcoming layer groups stream into an LDS ring of D+1
+//                   stages with direct global->LDS loads, D stages ahead of
+//                   the MFMAs.  A query tile (16 queries) stops at the layer
+//                   group of its deepest member.  float32 operands are split
+//                   into three bf16 parts a = a1 + a2 + a3 + r (|r| <= 2^-27
+//                   |a|) and a.b accumulates the six terms
+//                   a1b1 + a1b2 + a2b1 + a1b3 + a2b2 + a3b1 on
+//                   v_mfma_f32_16x16x32_bf16 (dropped terms < 2^-25 |ab|);
+//                   bf16 stores take one MFMA.  Squared map-row norms come
+//                   from the same operands, giving every map's prefix norm at
+//                   every depth.  A per-lane top-K of packed (score, index)
+//                   keys is merged across the workgroup and stored (plain
+//                   stores) as this workgroup's partial list per query.
+//  k_finalize       merges the partial lists of each query into idx/score.
+//
+// "Slots": each layer's E experts padded to a multiple of 32, or LPG = 32/E
+// layers per 32 slots when E (>= 8) divides 32.
 #include <type_traits>
 
 #include "fm_device.h"
@@ -46,27 +47,92 @@ typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float float2v __attribute__((ext_vector_type(2)));
 typedef uint32_t uint32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t uint32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void* lds_vp;
+typedef __attribute__((address_space(1))) void* gbl_vp;
 
-struct TrajArgs {
-  const void* planes;
-  int64_t plane_elems;
+// Fourth word of a raw buffer descriptor (32-bit data format, no swizzle), and
+// a byte offset beyond every descriptor's range: loads there return zeros.
+constexpr int kBufWord3 = 0x00020000;
+constexpr uint32_t kOutside = 0xFFFFF000u;
+
+// Slot geometry of a store (host-computed).
+struct Geo {
+  int32_t spl;   // slots per layer: E when LPG > 1, else E rounded up to 32
+  int32_t lpg;   // layers per layer group
+  int32_t ksg;   // 32-slot k-steps per layer group
+};
+
+// Bytes of one staged query plane row: 32*ksg bf16 slots plus one 16-byte pad
+// (a 16-byte-unit stride that is odd, so 16 consecutive rows read at the same
+// column hit distinct LDS banks).
+__host__ __device__ __forceinline__ int qrow_bytes(int ksg) { return 64 * ksg + 16; }
+
+struct PrepArgs {
   const void* q;
   const int32_t* depth;
-  int32_t n, L, E;
-  int32_t spl;      // slots per layer: E when LPG > 1, else E rounded up to 32
-  int32_t lpg;      // layers per layer group
-  int32_t ksg;      // 32-slot k-steps per layer group
-  int32_t B, k;
-  int32_t n_qg;     // query groups
-  int32_t n_units;  // (map slices) x (query groups)
-  int32_t grid;
-  int32_t dmax;     // bound on depths (max_depth)
+  int32_t B, L, E, dmax;
+  Geo geo;
+  int32_t nlg;        // layer groups staged (ceil(dmax / lpg))
+  int32_t b_pad;      // positions per staged layer group (multiple of the group size)
+  int32_t qg;         // queries per group (16 * TQ)
   Workspace ws;
   uint32_t* flags;
-  int32_t* idx_out;
-  float* score_out;
-  float* dbg;       // optional dense scores [B][n]
 };
+
+struct ScanArgs {
+  const void* planes;
+  int64_t plane_bytes;
+  int32_t n, L, E;
+  Geo geo;
+  int32_t B, b_pad, dmax;
+  int32_t n_qg;       // query groups
+  int32_t R;          // workgroups per query group
+  int32_t slices;     // map slices of 64*NBA maps
+  int32_t grid;
+  Workspace ws;
+  float* dbg;         // optional dense scores [B][n]
+};
+
+// Stable sort of the batch by depth, deepest first.  A query's position is
+// (queries deeper) + (queries of equal depth with a lower index): the same
+// in every workgroup.  bits: LDS [kMaxL][16] words; start: LDS [kMaxL].
+__device__ void depth_buckets(const int32_t* depth, int B, int dmax, unsigned long long* bits, int32_t* start) {
+  const int tid = threadIdx.x;
+  const int lane = tid % kWave;
+  for (int i = tid; i < kMaxL * 16; i += blockDim.x) bits[i] = 0ull;
+  __syncthreads();
+  for (int b = tid; b < B; b += blockDim.x) {
+    const int d = depth[b];
+    const int dc = d < 1 ? 1 : (d > dmax ? dmax : d);
+    atomicOr(&bits[(dc - 1) * 16 + b / 64], 1ull << (b % 64));
+  }
+  __syncthreads();
+  if (tid < kWave) {
+    int cnt = 0;
+    if (lane < dmax) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) cnt += __popcll(bits[lane * 16 + i]);
+    }
+    int incl = cnt;  // inclusive suffix sum over buckets lane .. 63
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int o = __shfl_down(incl, off, kWave);
+      if (lane + off < 64) incl += o;
+    }
+    start[lane] = incl - cnt;
+  }
+  __syncthreads();
+}
+
+__device__ __forceinline__ int position_of(int b, int dc, const unsigned long long* bits, const int32_t* start) {
+  const unsigned long long* row = bits + (dc - 1) * 16;
+  const int wd = b / 64;
+  int r = 0;
+  for (int i = 0; i < wd; ++i) r += __popcll(row[i]);
+  r += __popcll(row[wd] & ((1ull << (b % 64)) - 1ull));
+  return start[dc - 1] + r;
+}
 
 // float32 -> three bf16 parts (bit patterns), each rounded to nearest even.
 // Pairs are converted with one packed conversion and read back as a whole
@@ -95,320 +161,412 @@ __device__ __forceinline__ floatx4 mfma_bf16(const u16x8& a, const u16x8& b, flo
                                                  0, 0, 0);
 }
 
+// Raw s_waitcnt bounding only the vector-memory counter (gfx9 encoding:
+// vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt field is 6 bits");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
+  asm volatile("" ::: "memory");
+}
+__device__ __forceinline__ void wait_lgkm0() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xF | (0x7 << 4) | (0x0 << 8) | (0x3 << 14));
+  asm volatile("" ::: "memory");
+}
+// Workgroup barrier without the implicit release/acquire fence (which would
+// wait for every outstanding global->LDS load); callers wait explicitly.
+__device__ __forceinline__ void raw_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// 16 bytes per lane from src into LDS at lds_base + 16 * lane.
+__device__ __forceinline__ void dma16(const void* src, void* lds_base) {
+  __builtin_amdgcn_global_load_lds((gbl_vp)(const_cast<void*>(src)), (lds_vp)(lds_base), 16, 0, 0);
+}
+
 }  // namespace
 
-template <bool BF, int TQ, int NBA, int KSG, int KTOP>
-__global__ void __launch_bounds__(256) k_traj_scan(TrajArgs a) {
-  constexpr int QG = 16 * TQ;                 // queries per group
-  constexpr int MW = 16 * NBA;                // maps per wave
-  constexpr int NP = BF ? 1 : 3;              // bf16 planes per operand
-  constexpr int kMaxQU = (TQ * KSG + 3) / 4;  // staged 8-slot query units per thread
-  constexpr int TC = TQ < 2 ? TQ : 2;         // query tiles whose operands are held at once
+// ----------------------------------------------------------------------------- prep
+
+// grid = (b_pad / 16, nlg + 4).  Block (x, y < nlg) stages layer group y of
+// sorted positions 16x .. 16x+15; blocks (x, nlg .. nlg+3) write their perm,
+// depth and 1/|q| entries.
+template <bool BF>
+__global__ void __launch_bounds__(256) k_traj_prep(PrepArgs a) {
+  using T = typename std::conditional<BF, uint16_t, float>::type;
+  constexpr int esz = sizeof(T);
+  __shared__ unsigned long long bits[kMaxL * 16];
+  __shared__ int32_t start[kMaxL];
+  __shared__ int32_t s_b[16];
+  __shared__ int32_t s_d[16];
+  const int tid = threadIdx.x;
+  if (tid < 16) {
+    s_b[tid] = -1;
+    s_d[tid] = 0;
+  }
+  depth_buckets(a.depth, a.B, a.dmax, bits, start);
+  const int p0 = blockIdx.x * 16;
+  for (int b = tid; b < a.B; b += kThreads) {
+    const int d = a.depth[b];
+    const int dc = d < 1 ? 1 : (d > a.dmax ? a.dmax : d);
+    const int pos = position_of(b, dc, bits, start);
+    if (pos >= p0 && pos < p0 + 16) {
+      s_b[pos - p0] = b;
+      s_d[pos - p0] = dc;
+    }
+    if (blockIdx.x == 0 && blockIdx.y == 0 && dc != d) atomicOr(a.flags, static_cast<uint32_t>(FM_FLAG_DEPTH_CLAMPED));
+  }
+  __syncthreads();
+  const T* q = static_cast<const T*>(a.q);
+  if (static_cast<int>(blockIdx.y) < a.nlg) {
+    // one thread per (row, 8-slot unit); unit 4*ksg of a row is the pad
+    const int lg = blockIdx.y;
+    const int upr = 4 * a.geo.ksg + 1;
+    const int rb = qrow_bytes(a.geo.ksg);
+    constexpr int NP = BF ? 1 : 3;
+    const int64_t plane_pitch = static_cast<int64_t>(a.qg) * rb;              // one plane of a group slab
+    const int grp = p0 / a.qg;
+    char* slab = static_cast<char*>(a.ws.qrows) + (static_cast<int64_t>(lg) * a.b_pad + grp * a.qg) * NP * rb;
+    const int i = tid;
+    if (i < 16 * upr) {
+      const int r = i / upr;
+      const int unit = i - r * upr;
+      const int row_in_grp = p0 - grp * a.qg + r;
+      u16x8 h = u16x8{}, m = u16x8{}, l = u16x8{};
+      const int b = s_b[r];
+      if (b >= 0 && unit < 4 * a.geo.ksg) {
+        const int s0 = 8 * unit;
+        const int li = s0 / a.geo.spl;
+        const int e0 = s0 - li * a.geo.spl;
+        const int layer = lg * a.geo.lpg + li;
+        if (layer < s_d[r] && e0 < a.E) {
+          const T* src = q + (static_cast<int64_t>(b) * a.L + layer) * a.E + e0;
+          const int nv = a.E - e0 < 8 ? a.E - e0 : 8;
+          if constexpr (BF) {
+            if (nv == 8 && a.E % 4 == 0) {
+              const u16x4 lo = *reinterpret_cast<const u16x4*>(src);
+              const u16x4 hi = *reinterpret_cast<const u16x4*>(src + 4);
+              h = u16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            } else {
+              for (int k = 0; k < nv; ++k) h[k] = src[k];
+            }
+          } else {
+            floatx8 v = floatx8{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+            if (nv == 8 && a.E % 4 == 0) {
+              const floatx4 lo = *reinterpret_cast<const floatx4*>(src);
+              const floatx4 hi = *reinterpret_cast<const floatx4*>(src + 4);
+              v = floatx8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            } else {
+              for (int k = 0; k < nv; ++k) v[k] = src[k];
+            }
+            split3(v, h, m, l);
+          }
+        }
+      }
+      char* dst = slab + static_cast<int64_t>(row_in_grp) * rb + 16 * unit;
+      *reinterpret_cast<u16x8*>(dst) = h;
+      if constexpr (!BF) {
+        *reinterpret_cast<u16x8*>(dst + plane_pitch) = m;
+        *reinterpret_cast<u16x8*>(dst + 2 * plane_pitch) = l;
+      }
+    }
+    return;
+  }
+  // perm, depth and 1/|q[b][0:p]| of the 16 positions: blocks y = nlg ..
+  // nlg+3 take four rows each, one wave per row
+  const int lane = tid % kWave;
+  const int r = (static_cast<int>(blockIdx.y) - a.nlg) * 4 + tid / kWave;
+  const int pos = p0 + r;
+  const int b = s_b[r];
+  double acc = 0.0;
+  if (b >= 0) {
+    // sixteen independent loads in flight per lane
+    constexpr int U = 16;
+    const int cnt = s_d[r] * a.E;
+    const T* row = q + static_cast<int64_t>(b) * a.L * a.E;
+    double part[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) part[u] = 0.0;
+    for (int j0 = lane; j0 < cnt; j0 += U * kWave) {
+      double f[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int j = j0 + u * kWave;
+        f[u] = 0.0;
+        if (j < cnt) {
+          if constexpr (BF) f[u] = static_cast<double>(bf16_to_f32(row[j]));
+          else f[u] = static_cast<double>(row[j]);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) part[u] += f[u] * f[u];
+    }
+#pragma unroll
+    for (int u = 1; u < U; ++u) part[0] += part[u];
+    acc = part[0];
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, kWave);
+  if (lane == 0) {
+    float rqv;
+    if (acc != acc) rqv = __uint_as_float(0x7fc00000u);
+    else if (acc == 0.0) rqv = 0.0f;
+    else rqv = static_cast<float>(1.0 / sqrt(acc));
+    a.ws.rq[pos] = b >= 0 ? rqv : 0.0f;
+    a.ws.perm[pos] = b;
+    a.ws.sdep[pos] = b >= 0 ? s_d[r] : 0;
+  }
+}
+
+// ----------------------------------------------------------------------------- scan
+
+// 8 waves; wave w owns NBA blocks of 16 maps of every slice.  Stage j of a
+// workgroup = (slice s_begin + j / NLG, layer group j % NLG).  Map operands of
+// stage j+3 are loaded into registers while stage j computes; the query
+// planes of stage j+3 are copied into LDS ring slot (j+3) % 4 by direct
+// global->LDS loads.  Every wave issues the same number of loads per stage
+// (stand-in addresses keep the count fixed), so "stage j has landed" is
+// vmcnt <= 3 * (loads per stage).
+template <bool BF, int TQ, int NBA, int KSG, int KTOP, bool DBG>
+__global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
+  using T = typename std::conditional<BF, uint16_t, float>::type;
   using Raw = typename std::conditional<BF, u16x8, floatx8>::type;
+  constexpr int W = 8;                        // waves per workgroup
+  constexpr int D = 3;                        // stages in flight
+  constexpr int NS = D + 1;                   // LDS ring slots
+  constexpr int esz = sizeof(T);
+  constexpr int QG = 16 * TQ;                 // queries per group
+  constexpr int MW = 16 * NBA;                // maps per wave and slice
+  constexpr int NP = BF ? 1 : 3;              // bf16 parts per operand
+  constexpr int TC = TQ < 4 ? TQ : 4;         // query tiles per MFMA chunk
+  constexpr int RB = 64 * KSG + 16;           // staged query plane row bytes
+  constexpr int NI_Q = (NP * QG * RB + W * 1024 - 1) / (W * 1024);  // 1 KB query loads per wave and stage
+  constexpr int Q_STAGE = W * NI_Q * 1024;
+  constexpr int LA = BF ? 1 : 2;              // 16-byte map loads per (block, k-step)
+  constexpr int NI_A = NBA * KSG * LA;        // map load instructions per wave and stage
+  constexpr int NI = NI_A + NI_Q;
+  static_assert((D - 1) * NI < 64, "vmcnt field is 6 bits");
 
   extern __shared__ __align__(16) unsigned char smem[];
-  __shared__ int32_t s_last;
-  __shared__ int32_t s_start[kMaxL];
+  unsigned char* ring = smem;                                              // [NS][Q_STAGE]
+  float* cum = reinterpret_cast<float*>(smem + NS * Q_STAGE);             // [W][dmax][MW]
+  int32_t* gperm = reinterpret_cast<int32_t*>(cum + W * a.dmax * MW);      // [QG]
+  int32_t* gdep = gperm + QG;                                              // [QG]
+  float* grq = reinterpret_cast<float*>(gdep + QG);                        // [QG]
+  uint64_t* mbuf = reinterpret_cast<uint64_t*>(smem);                      // after the loop: [W][QG][KTOP]
 
   const int tid = threadIdx.x;
   const int w = tid / kWave;
   const int lane = tid % kWave;
   const int g = lane / 16;
   const int c = lane % 16;
-  const int qrow = 32 * KSG + 8;              // LDS row stride of staged queries (bf16 elements)
 
-  // LDS carve-up
-  uint16_t* qs = reinterpret_cast<uint16_t*>(smem);                        // [NP][QG][qrow]
-  float* cum = reinterpret_cast<float*>(qs + NP * QG * qrow);              // [4][dmax][MW]
-  int32_t* gperm = reinterpret_cast<int32_t*>(cum + kWaves * a.dmax * MW); // [QG]
-  int32_t* gdep = gperm + QG;                                              // [QG]
-  float* grq = reinterpret_cast<float*>(gdep + QG);                        // [QG]
-  uint64_t* mbuf = reinterpret_cast<uint64_t*>(
-      (reinterpret_cast<uintptr_t>(grq + QG) + 7) & ~static_cast<uintptr_t>(7));  // [4][QG][KTOP]
-  unsigned long long* bits = reinterpret_cast<unsigned long long*>(mbuf);  // prologue only: [kMaxL][16]
-
-  // workgroup -> (map slice, query group); consecutive units share an XCD
+  // workgroup -> (query group, slice range); the n_qg workgroups sharing a
+  // slice range are consecutive, hence on one XCD and its L2
   const int bid = blockIdx.x;
   const int u = (bid % 8) * (a.grid / 8) + bid / 8;
-  const bool active = u < a.n_units;
-  const int slice = active ? u / a.n_qg : 0;
+  const bool active = u < a.n_qg * a.R;
   const int qgrp = active ? u % a.n_qg : 0;
+  const int rr = active ? u / a.n_qg : 0;
+  const int s_begin = active ? static_cast<int>((static_cast<int64_t>(rr) * a.slices) / a.R) : 0;
+  const int s_end = active ? static_cast<int>((static_cast<int64_t>(rr + 1) * a.slices) / a.R) : 0;
   const int g0 = qgrp * QG;
-  const int y_slice = slice * (kWaves * MW);
-  const int y_wave = y_slice + w * MW;
 
-  // ---- stable depth sort, deepest first: position of query b = queries
-  // deeper than b + queries of equal depth with a lower index
-  for (int i = tid; i < kMaxL * 16; i += kThreads) bits[i] = 0ull;
-  for (int r = tid; r < QG; r += kThreads) {
-    gdep[r] = 0;
-    gperm[r] = 0;
-    grq[r] = 0.0f;
+  for (int r = tid; r < QG; r += W * kWave) {
+    const int pos = g0 + r;
+    gperm[r] = a.ws.perm[pos];
+    gdep[r] = a.ws.sdep[pos];
+    grq[r] = a.ws.rq[pos];
   }
   __syncthreads();
-  for (int b = tid; b < a.B; b += kThreads) {
-    const int d = a.depth[b];
-    const int dc = d < 1 ? 1 : (d > a.dmax ? a.dmax : d);
-    if (dc != d && bid == 0) atomicOr(a.flags, static_cast<uint32_t>(FM_FLAG_DEPTH_CLAMPED));
-    atomicOr(&bits[(dc - 1) * 16 + b / 64], 1ull << (b % 64));
-  }
-  __syncthreads();
-  if (w == 0) {
-    int cnt = 0;
-    if (lane < a.dmax) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) cnt += __popcll(bits[lane * 16 + i]);
-    }
-    int incl = cnt;  // inclusive suffix sum over buckets lane .. 63
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int o = __shfl_down(incl, off, kWave);
-      if (lane + off < 64) incl += o;
-    }
-    s_start[lane] = incl - cnt;
-  }
-  __syncthreads();
-  for (int b = tid; b < a.B; b += kThreads) {
-    const int d = a.depth[b];
-    const int dc = d < 1 ? 1 : (d > a.dmax ? a.dmax : d);
-    const unsigned long long* row = bits + (dc - 1) * 16;
-    const int wd = b / 64;
-    int r = 0;
-    for (int i = 0; i < wd; ++i) r += __popcll(row[i]);
-    r += __popcll(row[wd] & ((1ull << (b % 64)) - 1ull));
-    const int pos = s_start[dc - 1] + r - g0;
-    if (pos >= 0 && pos < QG) {
-      gperm[pos] = b;
-      gdep[pos] = dc;
-    }
-  }
-  __syncthreads();
-
   int tmd[TQ];
 #pragma unroll
-  for (int t = 0; t < TQ; ++t) tmd[t] = active ? gdep[16 * t] : 0;
-  const int D = tmd[0];
-  const int NLG = (D + a.lpg - 1) / a.lpg;
+  for (int t = 0; t < TQ; ++t) tmd[t] = gdep[16 * t];
+  const int NLG = (tmd[0] + a.geo.lpg - 1) / a.geo.lpg;
+  const int nstages = (s_end - s_begin) * NLG;
 
   TopK<KTOP> best[TQ];
 #pragma unroll
   for (int t = 0; t < TQ; ++t) best[t].clear();
 
-  if (active && D > 0 && y_slice < a.n) {
-    // ---- query staging units of this thread: unit = (row, 8-slot part).
-    // What stays fixed from one layer group to the next is computed once:
-    // the unit's element offset at layer group 0, its layer within the
-    // group, how many of its 8 slots are real experts and its query's depth.
-    constexpr int upr = 4 * KSG;              // units per row (4 or 8)
-    const int nunits = QG * upr;
-    const bool vec_ok = (a.E % 4) == 0;       // 8-slot runs start 16-byte (f32) / 8-byte (bf16) aligned
-    int q_lds[kMaxQU], q_li[kMaxQU], q_nv[kMaxQU], q_p[kMaxQU];
-    int64_t q_off[kMaxQU];
-#pragma unroll
-    for (int i = 0; i < kMaxQU; ++i) {
-      const int id = tid + i * kThreads;
-      q_lds[i] = -1;
-      q_li[i] = 0;
-      q_nv[i] = 0;
-      q_p[i] = 0;
-      q_off[i] = 0;
-      if (id < nunits) {
-        const int r = id / upr;
-        const int s0 = 8 * (id % upr);
-        const int li = s0 / a.spl;
-        const int e0 = s0 - li * a.spl;
-        const int nv = a.E - e0;
-        q_lds[i] = r * qrow + s0;
-        q_li[i] = li;
-        q_nv[i] = nv < 0 ? 0 : (nv > 8 ? 8 : nv);
-        q_p[i] = (g0 + r < a.B) ? gdep[r] : 0;
-        q_off[i] = static_cast<int64_t>(gperm[r]) * a.L * a.E + li * a.E + e0;
-      }
-    }
-    const int64_t q_step = static_cast<int64_t>(a.lpg) * a.E;
-    double qn2[kMaxQU];
-#pragma unroll
-    for (int i = 0; i < kMaxQU; ++i) qn2[i] = 0.0;
-
-    Raw qraw[kMaxQU];
-    auto load_q = [&](int lg) {
-#pragma unroll
-      for (int i = 0; i < kMaxQU; ++i) {
-        Raw v;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = 0;
-        if (lg * a.lpg + q_li[i] < q_p[i]) {   // a real query that observed this layer
-          const int64_t off = q_off[i] + lg * q_step;
-          if constexpr (BF) {
-            const uint16_t* p = static_cast<const uint16_t*>(a.q) + off;
-            if (q_nv[i] == 8 && vec_ok) {
-              const u16x4 lo = *reinterpret_cast<const u16x4*>(p);
-              const u16x4 hi = *reinterpret_cast<const u16x4*>(p + 4);
-              v = u16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-            } else {
-#pragma unroll
-              for (int j = 0; j < 8; ++j)
-                if (j < q_nv[i]) v[j] = p[j];
-            }
-          } else {
-            const float* p = static_cast<const float*>(a.q) + off;
-            if (q_nv[i] == 8 && vec_ok) {
-              const floatx4 lo = *reinterpret_cast<const floatx4*>(p);
-              const floatx4 hi = *reinterpret_cast<const floatx4*>(p + 4);
-              v = floatx8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-            } else {
-#pragma unroll
-              for (int j = 0; j < 8; ++j)
-                if (j < q_nv[i]) v[j] = p[j];
-            }
-          }
-        }
-        qraw[i] = v;
-      }
-    };
-    auto store_q = [&]() {
-#pragma unroll
-      for (int i = 0; i < kMaxQU; ++i) {
-        if (q_lds[i] < 0) continue;
-        uint16_t* dst = qs + q_lds[i];
-        if constexpr (BF) {
-          *reinterpret_cast<u16x8*>(dst) = qraw[i];
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const double f = static_cast<double>(bf16_to_f32(qraw[i][j]));
-            qn2[i] += f * f;
-          }
-        } else {
-          u16x8 h, m, l;
-          split3(qraw[i], h, m, l);
-          *reinterpret_cast<u16x8*>(dst) = h;
-          *reinterpret_cast<u16x8*>(dst + QG * qrow) = m;
-          *reinterpret_cast<u16x8*>(dst + 2 * QG * qrow) = l;
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const double f = static_cast<double>(qraw[i][j]);
-            qn2[i] += f * f;
-          }
-        }
-      }
-    };
-
-    // ---- this lane's map operand: rows y_wave + 16*nb + c, slots 32*ks + 8*g .. +7
-    int a_li[KSG], a_nv[KSG];
-    int64_t a_off[NBA][KSG];
-    bool a_ok[NBA];
+  if (active && nstages > 0) {
+    // lane constants: slot run 32*ks + 8*g of the lane's map row
+    int r_li[KSG], r_e0[KSG], r_nv[KSG];
 #pragma unroll
     for (int ks = 0; ks < KSG; ++ks) {
       const int s0 = 32 * ks + 8 * g;
-      const int li = s0 / a.spl;
-      const int e0 = s0 - li * a.spl;
+      const int li = s0 / a.geo.spl;
+      const int e0 = s0 - li * a.geo.spl;
       const int nv = a.E - e0;
-      a_li[ks] = li;
-      a_nv[ks] = nv < 0 ? 0 : (nv > 8 ? 8 : nv);
-#pragma unroll
-      for (int nb = 0; nb < NBA; ++nb)
-        a_off[nb][ks] = li * a.plane_elems + static_cast<int64_t>(y_wave + 16 * nb + c) * a.E + e0;
+      r_li[ks] = li;
+      r_e0[ks] = e0;
+      r_nv[ks] = nv < 0 ? 0 : (nv > 8 ? 8 : nv);
     }
+    // Map rows are read with raw buffer loads over the planes of one layer
+    // group.  Rows past the store, padding units, the upper half of a unit
+    // holding at most 4 experts and layers at or past L use offsets beyond
+    // the descriptor's range and read as zeros without touching memory.
+    const char* planes = static_cast<const char*>(a.planes);
+    uint32_t lane_off[KSG];
 #pragma unroll
-    for (int nb = 0; nb < NBA; ++nb) a_ok[nb] = y_wave + 16 * nb + c < a.n;
-    const int64_t a_step = static_cast<int64_t>(a.lpg) * a.plane_elems;
+    for (int ks = 0; ks < KSG; ++ks)
+      lane_off[ks] = static_cast<uint32_t>(r_li[ks]) * static_cast<uint32_t>(a.plane_bytes) +
+                     static_cast<uint32_t>(r_e0[ks] * esz);
+    const uint32_t row_bytes = static_cast<uint32_t>(a.E * esz);
+    const char* qrows = static_cast<const char*>(a.ws.qrows);
 
-    Raw araw[NBA][KSG];
-    auto load_a = [&](int lg) {
+    auto load_a = [&](int j, Raw (&dst)[NBA][KSG]) {
+      const bool real = j < nstages;
+      const int si = real ? s_begin + j / NLG : s_begin;
+      const int lg = real ? j % NLG : 0;
+      const int l0 = lg * a.geo.lpg;
+      const int nl = a.L - l0 < a.geo.lpg ? a.L - l0 : a.geo.lpg;
+      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<char*>(planes + l0 * a.plane_bytes), static_cast<short>(0),
+          static_cast<int>(static_cast<uint32_t>(nl) * static_cast<uint32_t>(a.plane_bytes)), kBufWord3);
 #pragma unroll
       for (int nb = 0; nb < NBA; ++nb) {
+        const int y = si * (W * MW) + w * MW + 16 * nb + c;
+        const bool row_ok = real && y < a.n;
+        const uint32_t row_off = static_cast<uint32_t>(y) * row_bytes;
 #pragma unroll
         for (int ks = 0; ks < KSG; ++ks) {
-          Raw v;
-#pragma unroll
-          for (int j = 0; j < 8; ++j) v[j] = 0;
-          if (a_ok[nb] && lg * a.lpg + a_li[ks] < a.L) {
-            const int64_t off = a_off[nb][ks] + lg * a_step;
-            const int nv = a_nv[ks];
-            if constexpr (BF) {
-              const uint16_t* p = static_cast<const uint16_t*>(a.planes) + off;
-              if (vec_ok && nv >= 4) {
-                const u16x4 lo = *reinterpret_cast<const u16x4*>(p);
-                u16x4 hi = u16x4{0, 0, 0, 0};
-                if (nv == 8) hi = *reinterpret_cast<const u16x4*>(p + 4);
-                v = u16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-              } else {
-#pragma unroll
-                for (int j = 0; j < 8; ++j)
-                  if (j < nv) v[j] = p[j];
-              }
-            } else {
-              const float* p = static_cast<const float*>(a.planes) + off;
-              if (vec_ok && nv >= 4) {
-                const floatx4 lo = *reinterpret_cast<const floatx4*>(p);
-                floatx4 hi = floatx4{0.f, 0.f, 0.f, 0.f};
-                if (nv == 8) hi = *reinterpret_cast<const floatx4*>(p + 4);
-                v = floatx8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-              } else {
-#pragma unroll
-                for (int j = 0; j < 8; ++j)
-                  if (j < nv) v[j] = p[j];
-              }
-            }
+          const uint32_t lo = row_ok && r_nv[ks] > 0 ? lane_off[ks] + row_off : kOutside;
+          const uint32_t hi = r_nv[ks] > 4 ? lo + 4 * esz : kOutside;
+          if constexpr (BF) {
+            const uint32x2 vl = __builtin_amdgcn_raw_buffer_load_b64(rs, static_cast<int>(lo), 0, 0);
+            const uint32x2 vh = __builtin_amdgcn_raw_buffer_load_b64(rs, static_cast<int>(hi), 0, 0);
+            dst[nb][ks] = __builtin_bit_cast(u16x8, uint32x4{vl[0], vl[1], vh[0], vh[1]});
+          } else {
+            const uint32x4 vl = __builtin_amdgcn_raw_buffer_load_b128(rs, static_cast<int>(lo), 0, 0);
+            const uint32x4 vh = __builtin_amdgcn_raw_buffer_load_b128(rs, static_cast<int>(hi), 0, 0);
+            dst[nb][ks] = floatx8{__uint_as_float(vl[0]), __uint_as_float(vl[1]), __uint_as_float(vl[2]),
+                                  __uint_as_float(vl[3]), __uint_as_float(vh[0]), __uint_as_float(vh[1]),
+                                  __uint_as_float(vh[2]), __uint_as_float(vh[3])};
           }
-          araw[nb][ks] = v;
         }
       }
     };
+    auto load_q = [&](int j) {
+      const bool real = j < nstages;
+      const int lg = real ? j % NLG : 0;
+      unsigned char* st = ring + (j % NS) * Q_STAGE;
+      const char* qsl = qrows + (static_cast<int64_t>(lg) * a.b_pad + g0) * NP * RB;
+#pragma unroll
+      for (int i = 0; i < NI_Q; ++i) dma16(qsl + (w * NI_Q + i) * 1024 + lane * 16, st + (w * NI_Q + i) * 1024);
+    };
 
     floatx4 acc[NBA][TQ];
-#pragma unroll
-    for (int nb = 0; nb < NBA; ++nb)
-#pragma unroll
-      for (int t = 0; t < TQ; ++t) acc[nb][t] = floatx4{0.f, 0.f, 0.f, 0.f};
     float cumsq[NBA];
 #pragma unroll
-    for (int nb = 0; nb < NBA; ++nb) cumsq[nb] = 0.0f;
+    for (int nb = 0; nb < NBA; ++nb) {
+      cumsq[nb] = 0.0f;
+#pragma unroll
+      for (int t = 0; t < TQ; ++t) acc[nb][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
 
-    // the padding columns of the staged rows are never written by staging
-    for (int r = tid; r < NP * QG; r += kThreads) *reinterpret_cast<u16x8*>(qs + r * qrow + 32 * KSG) = u16x8{};
-
+    Raw ar0[NBA][KSG], ar1[NBA][KSG], ar2[NBA][KSG];
+    load_a(0, ar0);
     load_q(0);
-    load_a(0);
-    for (int lg = 0; lg < NLG; ++lg) {
-      store_q();
-      // bf16 operand planes of this lane's map rows; squared norms per layer
-      u16x8 ap[NP][NBA][KSG];
+    load_a(1, ar1);
+    load_q(1);
+    load_a(2, ar2);
+    load_q(2);
+
+    auto stage = [&](int j, Raw (&cur)[NBA][KSG]) {
+      const int si = s_begin + j / NLG;
+      const int lg = j % NLG;
+      const int y_wave = si * (W * MW) + w * MW;
+      const unsigned char* sq = ring + (j % NS) * Q_STAGE;
+
+      // query planes of stage j are in LDS once every wave's loads of it
+      // landed (only stages j+1 and j+2 may still be in flight)
+      wait_vmcnt<(D - 1) * NI>();
+      raw_barrier();
+
+      // Per k-step: the map operand (already zero outside the store and past
+      // L; a unit ending inside a 4-element half is masked here), its squared
+      // norms and bf16 parts, then the MFMAs.  Tiles are sorted by depth
+      // (deepest first); a chunk of TC tiles runs while its first tile is
+      // active, and inactive tiles inside a chunk only add zeros (their staged
+      // rows are zero).
+      const int l_first = lg * a.geo.lpg;
+      const bool ragged = (a.E & 3) != 0;
       float lsq[NBA];
 #pragma unroll
-      for (int nb = 0; nb < NBA; ++nb) {
-        lsq[nb] = 0.0f;
+      for (int nb = 0; nb < NBA; ++nb) lsq[nb] = 0.0f;
 #pragma unroll
-        for (int ks = 0; ks < KSG; ++ks) {
+      for (int ks = 0; ks < KSG; ++ks) {
+        u16x8 ap[NP][NBA];
+#pragma unroll
+        for (int nb = 0; nb < NBA; ++nb) {
+          Raw v = cur[nb][ks];
+          if (ragged) {
+#pragma unroll
+            for (int jj = 0; jj < 8; ++jj)
+              if (jj >= r_nv[ks]) v[jj] = 0;
+          }
           if constexpr (BF) {
-            ap[0][nb][ks] = araw[nb][ks];
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-              const float f = bf16_to_f32(araw[nb][ks][j]);
+            for (int jj = 0; jj < 8; ++jj) {
+              const float f = bf16_to_f32(v[jj]);
               lsq[nb] = fmaf(f, f, lsq[nb]);
             }
+            ap[0][nb] = v;
           } else {
-            split3(araw[nb][ks], ap[0][nb][ks], ap[1][nb][ks], ap[2][nb][ks]);
 #pragma unroll
-            for (int j = 0; j < 8; ++j) lsq[nb] = fmaf(araw[nb][ks][j], araw[nb][ks][j], lsq[nb]);
+            for (int jj = 0; jj < 8; ++jj) lsq[nb] = fmaf(v[jj], v[jj], lsq[nb]);
+            split3(v, ap[0][nb], ap[1][nb], ap[2][nb]);
+          }
+        }
+#pragma unroll
+        for (int tc = 0; tc < TQ; tc += TC) {
+          if (tmd[tc] <= l_first) break;
+          u16x8 bq[NP][TC];
+#pragma unroll
+          for (int tt = 0; tt < TC; ++tt) {
+#pragma unroll
+            for (int pl = 0; pl < NP; ++pl)
+              bq[pl][tt] = *reinterpret_cast<const u16x8*>(sq + (pl * QG + 16 * (tc + tt) + c) * RB + (32 * ks + 8 * g) * 2);
+          }
+          if constexpr (BF) {
+#pragma unroll
+            for (int tt = 0; tt < TC; ++tt)
+#pragma unroll
+              for (int nb = 0; nb < NBA; ++nb) acc[nb][tc + tt] = mfma_bf16(ap[0][nb], bq[0][tt], acc[nb][tc + tt]);
+          } else {
+            // the six cross terms, smallest first
+            constexpr int TA[6] = {2, 1, 0, 1, 0, 0};
+            constexpr int TB[6] = {0, 1, 2, 0, 1, 0};
+#pragma unroll
+            for (int term = 0; term < 6; ++term)
+#pragma unroll
+              for (int tt = 0; tt < TC; ++tt)
+#pragma unroll
+                for (int nb = 0; nb < NBA; ++nb)
+                  acc[nb][tc + tt] = mfma_bf16(ap[TA[term]][nb], bq[TB[term]][tt], acc[nb][tc + tt]);
           }
         }
       }
-      // Per-layer sums.  With LPG == 1 all four lane groups hold one layer;
-      // with LPG > 1 layer li of the group occupies lane groups
-      // [li*E/8, (li+1)*E/8).
+
+      // per-layer sums: with LPG == 1 all four lane groups hold one layer;
+      // with LPG > 1 layer li occupies lane groups [li*E/8, (li+1)*E/8)
 #pragma unroll
       for (int nb = 0; nb < NBA; ++nb) {
-        if (a.lpg == 1 || a.E == 32) {
+        if (a.geo.lpg == 1 || a.E == 32) {
           lsq[nb] += __shfl_xor(lsq[nb], 16, kWave);
           lsq[nb] += __shfl_xor(lsq[nb], 32, kWave);
         } else if (a.E == 16) {
           lsq[nb] += __shfl_xor(lsq[nb], 16, kWave);
         }
       }
-      for (int li = 0; li < a.lpg; ++li) {
-        const int l = lg * a.lpg + li;
-        const int src = c + 16 * (a.lpg == 1 ? 0 : (li * a.E) / 8);
+      for (int li = 0; li < a.geo.lpg; ++li) {
+        const int l = lg * a.geo.lpg + li;
+        const int src = c + 16 * (a.geo.lpg == 1 ? 0 : (li * a.E) / 8);
 #pragma unroll
         for (int nb = 0; nb < NBA; ++nb) {
           const float v = __shfl(lsq[nb], src, kWave);
@@ -416,97 +574,76 @@ __global__ void __launch_bounds__(256) k_traj_scan(TrajArgs a) {
           if (g == 0 && l < a.dmax) cum[(w * a.dmax + l) * MW + 16 * nb + c] = cumsq[nb];
         }
       }
-      __syncthreads();
-      if (lg + 1 < NLG) {
-        load_q(lg + 1);
-        load_a(lg + 1);
-      }
-      // MFMAs of this layer group for the active query tiles
-      const int l_first = lg * a.lpg;
+
+      if (lg == NLG - 1) {
+        // end of a slice: 1/|x[y][0:p]| at every depth of this wave's maps
+        // (the table is per wave), cosine, optional dense output, top-K
+        const int D_g = tmd[0];
+        wait_lgkm0();
+        for (int i = lane; i < D_g * MW; i += kWave) {
+          const float v = cum[w * a.dmax * MW + i];
+          cum[w * a.dmax * MW + i] = v > 0.0f ? 1.0f / sqrtf(v) : (v != v ? v : 0.0f);
+        }
+        wait_lgkm0();
 #pragma unroll
-      for (int ks = 0; ks < KSG; ++ks) {
+        for (int t = 0; t < TQ; ++t) {
+          const int r = 16 * t + c;
+          const int p = gdep[r];
+          if (p == 0) continue;
+          const float rq = grq[r];
 #pragma unroll
-        for (int tc = 0; tc < TQ; tc += TC) {
-          if (tmd[tc] <= l_first) break;  // tiles are sorted by depth, deepest first
-          u16x8 bq[NP][TC];
+          for (int nb = 0; nb < NBA; ++nb) {
 #pragma unroll
-          for (int tt = 0; tt < TC; ++tt) {
-#pragma unroll
-            for (int pl = 0; pl < NP; ++pl)
-              bq[pl][tt] = *reinterpret_cast<const u16x8*>(qs + (pl * QG + 16 * (tc + tt) + c) * qrow + 32 * ks + 8 * g);
-          }
-          if constexpr (BF) {
-#pragma unroll
-            for (int tt = 0; tt < TC; ++tt) {
-              if (tmd[tc + tt] > l_first) {
-#pragma unroll
-                for (int nb = 0; nb < NBA; ++nb)
-                  acc[nb][tc + tt] = mfma_bf16(ap[0][nb][ks], bq[0][tt], acc[nb][tc + tt]);
-              }
-            }
-          } else {
-            // the six cross terms, smallest first
-            constexpr int TA[6] = {2, 1, 0, 1, 0, 0};
-            constexpr int TB[6] = {0, 1, 2, 0, 1, 0};
-#pragma unroll
-            for (int term = 0; term < 6; ++term) {
-#pragma unroll
-              for (int tt = 0; tt < TC; ++tt) {
-                if (tmd[tc + tt] > l_first) {
-#pragma unroll
-                  for (int nb = 0; nb < NBA; ++nb)
-                    acc[nb][tc + tt] = mfma_bf16(ap[TA[term]][nb][ks], bq[TB[term]][tt], acc[nb][tc + tt]);
-                }
-              }
+            for (int i = 0; i < 4; ++i) {
+              const int jm = 16 * nb + 4 * g + i;
+              const int y = y_wave + jm;
+              if (y >= a.n) continue;
+              const float rs = cum[(w * a.dmax + (p - 1)) * MW + jm];
+              const float s = acc[nb][t][i] * rq * rs;
+              if constexpr (DBG) a.dbg[static_cast<int64_t>(gperm[r]) * a.n + y] = s;
+              best[t].push(make_key(s, y));
             }
           }
         }
-      }
-      __syncthreads();
-    }
-
-    // query norms: combine the partial sums of each row's units (fixed order)
 #pragma unroll
-    for (int i = 0; i < kMaxQU; ++i) {
-      double v = qn2[i];
-      for (int m = 1; m < upr; m <<= 1) v += __shfl_xor(v, m, kWave);
-      const int id = tid + i * kThreads;
-      if (id < nunits && id % upr == 0) {
-        float r;
-        if (v != v) r = __uint_as_float(0x7fc00000u);
-        else if (v == 0.0) r = 0.0f;
-        else r = static_cast<float>(1.0 / sqrt(v));
-        grq[id / upr] = r;
+        for (int nb = 0; nb < NBA; ++nb) {
+          cumsq[nb] = 0.0f;
+#pragma unroll
+          for (int t = 0; t < TQ; ++t) acc[nb][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+        }
       }
+      wait_lgkm0();
+      raw_barrier();   // every wave is done with ring slot j % NS
+    };
+
+    // three-stage register rotation: stage j computes from ar[j % 3] and
+    // then reloads it with stage j + 3
+    int j = 0;
+    for (; j + 3 <= nstages; j += 3) {
+      stage(j, ar0);
+      load_a(j + 3, ar0);
+      load_q(j + 3);
+      stage(j + 1, ar1);
+      load_a(j + 4, ar1);
+      load_q(j + 4);
+      stage(j + 2, ar2);
+      load_a(j + 5, ar2);
+      load_q(j + 5);
     }
-    // 1/|x[y][0:p]| for every depth p <= D of this wave's maps
-    for (int i = lane; i < D * MW; i += kWave) {
-      const float v = cum[w * a.dmax * MW + i];
-      cum[w * a.dmax * MW + i] = v > 0.0f ? 1.0f / sqrtf(v) : (v != v ? v : 0.0f);
+    if (j < nstages) {
+      stage(j, ar0);
+      load_a(j + 3, ar0);
+      load_q(j + 3);
+      ++j;
     }
+    if (j < nstages) {
+      stage(j, ar1);
+      load_a(j + 3, ar1);
+      load_q(j + 3);
+      ++j;
+    }
+    wait_vmcnt<0>();   // drain the trailing stand-in loads
     __syncthreads();
-
-    // epilogue: cosine, optional dense output, per-lane top-K
-#pragma unroll
-    for (int t = 0; t < TQ; ++t) {
-      const int r = 16 * t + c;
-      const int p = gdep[r];
-      if (p == 0) continue;
-      const float rq = grq[r];
-#pragma unroll
-      for (int nb = 0; nb < NBA; ++nb) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int jm = 16 * nb + 4 * g + i;
-          const int y = y_wave + jm;
-          if (y >= a.n) continue;
-          const float rs = cum[(w * a.dmax + (p - 1)) * MW + jm];
-          const float s = acc[nb][t][i] * rq * rs;
-          if (a.dbg != nullptr) a.dbg[static_cast<int64_t>(gperm[r]) * a.n + y] = s;
-          best[t].push(make_key(s, y));
-        }
-      }
-    }
   }
 
   // merge the per-lane lists across the 4 lane groups, then across waves
@@ -516,109 +653,156 @@ __global__ void __launch_bounds__(256) k_traj_scan(TrajArgs a) {
     for (int m = 16; m <= 32; m <<= 1) {
       uint64_t o[KTOP];
 #pragma unroll
-      for (int j = 0; j < KTOP; ++j) o[j] = shfl_xor_u64(best[t].v[j], m);
+      for (int jj = 0; jj < KTOP; ++jj) o[jj] = shfl_xor_u64(best[t].v[jj], m);
       best[t].merge(o);
     }
   }
-  __syncthreads();  // the sort bitmask (aliasing mbuf) is dead from here on
+  __syncthreads();
   if (g == 0) {
 #pragma unroll
     for (int t = 0; t < TQ; ++t) {
 #pragma unroll
-      for (int j = 0; j < KTOP; ++j) mbuf[(w * QG + 16 * t + c) * KTOP + j] = best[t].v[j];
+      for (int jj = 0; jj < KTOP; ++jj) mbuf[(w * QG + 16 * t + c) * KTOP + jj] = best[t].v[jj];
     }
   }
   __syncthreads();
-  for (int r = tid; r < QG; r += kThreads) {
-    if (!active || g0 + r >= a.B || gdep[r] == 0) continue;
-    TopK<KTOP> m;
-    m.clear();
+  if (active) {
+    for (int r = tid; r < QG; r += W * kWave) {
+      TopK<KTOP> m;
+      m.clear();
 #pragma unroll
-    for (int ww = 0; ww < kWaves; ++ww) m.merge(mbuf + (ww * QG + r) * KTOP);
-    global_topk_insert<KTOP>(a.ws.keys + static_cast<int64_t>(gperm[r]) * kMaxK, a.k, m.v);
-  }
-
-  // the last workgroup to finish writes the results and clears the workspace
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) {
-    const uint32_t ticket = __hip_atomic_fetch_add(a.ws.counter, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    s_last = (ticket == static_cast<uint32_t>(a.grid - 1)) ? 1 : 0;
-  }
-  __syncthreads();
-  if (s_last) {
-    __threadfence();
-    for (int i = tid; i < a.B * a.k; i += kThreads) {
-      const int b = i / a.k;
-      const int j = i - b * a.k;
-      uint64_t* slot = a.ws.keys + static_cast<int64_t>(b) * kMaxK + j;
-      const uint64_t key = __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (a.idx_out != nullptr) {
-        a.idx_out[i] = key_index(key);
-        a.score_out[i] = key_score(key);
-      }
-      __hip_atomic_store(slot, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      for (int ww = 0; ww < W; ++ww) m.merge(mbuf + (ww * QG + r) * KTOP);
+      uint64_t* out = a.ws.partial + (static_cast<int64_t>(g0 + r) * a.R + rr) * KTOP;
+#pragma unroll
+      for (int jj = 0; jj < KTOP; ++jj) out[jj] = m.v[jj];
     }
-    if (tid == 0) __hip_atomic_store(a.ws.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
+}
+
+// ----------------------------------------------------------------------------- finalize
+
+// One wave per position: merge its R partial lists into the k best and write
+// them for query perm[pos] (or pos itself when perm is NULL).
+template <int KTOP>
+__global__ void __launch_bounds__(256) k_finalize(const uint64_t* __restrict__ partial, const int32_t* __restrict__ perm,
+                                                  int32_t B, int32_t R, int32_t k, int32_t* __restrict__ idx_out,
+                                                  float* __restrict__ score_out) {
+  const int lane = threadIdx.x % kWave;
+  const int pos = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+  if (pos >= B) return;
+  TopK<KTOP> m;
+  m.clear();
+  for (int r = lane; r < R; r += kWave) m.merge(partial + (static_cast<int64_t>(pos) * R + r) * KTOP);
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    uint64_t o[KTOP];
+#pragma unroll
+    for (int jj = 0; jj < KTOP; ++jj) o[jj] = shfl_xor_u64(m.v[jj], off);
+    m.merge(o);
+  }
+  if (lane == 0) {
+    const int b = perm != nullptr ? perm[pos] : pos;
+#pragma unroll
+    for (int jj = 0; jj < kMaxK; ++jj) {
+      if (jj >= k) break;
+      const uint64_t key = jj < KTOP ? m.v[jj < KTOP ? jj : 0] : 0ull;
+      idx_out[static_cast<int64_t>(b) * k + jj] = key_index(key);
+      score_out[static_cast<int64_t>(b) * k + jj] = key_score(key);
+    }
+  }
+}
+
+hipError_t launch_finalize(const uint64_t* partial, const int32_t* perm, int32_t B, int32_t R, int32_t k, int KTOP,
+                           int32_t* idx_out, float* score_out, hipStream_t st) {
+  const dim3 grid((B + kWaves - 1) / kWaves);
+  if (KTOP == 1) hipLaunchKernelGGL(k_finalize<1>, grid, dim3(kThreads), 0, st, partial, perm, B, R, k, idx_out, score_out);
+  else if (KTOP == 4) hipLaunchKernelGGL(k_finalize<4>, grid, dim3(kThreads), 0, st, partial, perm, B, R, k, idx_out, score_out);
+  else hipLaunchKernelGGL(k_finalize<8>, grid, dim3(kThreads), 0, st, partial, perm, B, R, k, idx_out, score_out);
+  return hipGetLastError();
 }
 
 // ----------------------------------------------------------------------------- launch
 
 namespace {
 
-template <bool BF, int TQ, int NBA, int KSG, int KTOP>
-hipError_t launch_on(const TrajArgs& a, size_t lds, hipStream_t st) {
-  auto kern = k_traj_scan<BF, TQ, NBA, KSG, KTOP>;
+Geo geometry(int E) {
+  Geo g;
+  if (E >= 8 && 32 % E == 0) {
+    g.spl = E;
+    g.lpg = 32 / E;
+    g.ksg = 1;
+  } else {
+    g.spl = (E + 31) / 32 * 32;
+    g.lpg = 1;
+    g.ksg = g.spl / 32;
+  }
+  return g;
+}
+
+// LDS of the scan: 4 ring slots of query planes (8 waves x NI_Q x 1 KB each),
+// the per-wave prefix-norm tables and the group's sorted query info; the
+// top-K merge buffer reuses the ring.
+size_t scan_lds(bool bf, int TQ, int NBA, int KSG, int KTOP, int dmax) {
+  const int NP = bf ? 1 : 3;
+  const int QG = 16 * TQ, MW = 16 * NBA;
+  const int RB = qrow_bytes(KSG);
+  const int ni_q = (NP * QG * RB + 8 * 1024 - 1) / (8 * 1024);
+  size_t ring = static_cast<size_t>(4) * 8 * ni_q * 1024;
+  const size_t merge = static_cast<size_t>(8) * QG * KTOP * 8;
+  if (merge > ring) ring = merge;
+  return ring + static_cast<size_t>(8) * dmax * MW * 4 + 3 * QG * 4 + 64;
+}
+
+template <bool BF, int TQ, int NBA, int KSG, int KTOP, bool DBG = false>
+hipError_t scan_launch(const ScanArgs& a, size_t lds, hipStream_t st) {
+  auto kern = k_traj_scan<BF, TQ, NBA, KSG, KTOP, DBG>;
   if (lds > 64 * 1024) {
     const hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
     if (err != hipSuccess) return err;
   }
-  hipLaunchKernelGGL(kern, dim3(a.grid), dim3(kThreads), lds, st, a);
+  hipLaunchKernelGGL(kern, dim3(a.grid), dim3(512), lds, st, a);
   return hipGetLastError();
 }
 
-template <bool BF, int KSG, int KTOP>
-hipError_t launch_tq(int TQ, int NBA, const TrajArgs& a, size_t lds, hipStream_t st) {
-  if (NBA == 2) {
-    switch (TQ) {
-      case 1: return launch_on<BF, 1, 2, KSG, KTOP>(a, lds, st);
-      case 2: return launch_on<BF, 2, 2, KSG, KTOP>(a, lds, st);
-      case 4: return launch_on<BF, 4, 2, KSG, KTOP>(a, lds, st);
-      default: break;
-    }
-  } else {
-    switch (TQ) {
-      case 8:
-        if constexpr (KTOP <= 4) return launch_on<BF, 8, 1, KSG, KTOP>(a, lds, st);
-        break;
-      case 16:
-        if constexpr (KTOP == 1) return launch_on<BF, 16, 1, KSG, KTOP>(a, lds, st);
-        break;
-      default: break;
-    }
-  }
+// Largest query-tile count per workgroup whose registers fit without spills
+// (512 threads leave 256 registers per lane).
+constexpr int tq_limit(bool bf, int ksg, int ktop) {
+  return ktop == 1 ? ((bf || ksg == 1) ? 16 : 8) : ktop == 4 ? ((bf || ksg == 1) ? 8 : 2) : ((bf || ksg == 1) ? 4 : 2);
+}
+
+// NBA (16-map blocks per wave) follows from TQ: 2 up to 4 query tiles, else 1.
+template <bool BF, int KSG, int KTOP, int TQ>
+hipError_t scan_tq1(const ScanArgs& a, size_t lds, hipStream_t st) {
+  if constexpr (TQ <= tq_limit(BF, KSG, KTOP)) return scan_launch<BF, TQ, (TQ <= 4 ? 2 : 1), KSG, KTOP>(a, lds, st);
   return hipErrorInvalidValue;
 }
 
+template <bool BF, int KSG, int KTOP>
+hipError_t scan_tq(int TQ, const ScanArgs& a, size_t lds, hipStream_t st) {
+  switch (TQ) {
+    case 1: return scan_tq1<BF, KSG, KTOP, 1>(a, lds, st);
+    case 2: return scan_tq1<BF, KSG, KTOP, 2>(a, lds, st);
+    case 4: return scan_tq1<BF, KSG, KTOP, 4>(a, lds, st);
+    case 8: return scan_tq1<BF, KSG, KTOP, 8>(a, lds, st);
+    case 16: return scan_tq1<BF, KSG, KTOP, 16>(a, lds, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 template <bool BF, int KTOP>
-hipError_t launch_ksg(int KSG, int TQ, int NBA, const TrajArgs& a, size_t lds, hipStream_t st) {
-  return KSG == 1 ? launch_tq<BF, 1, KTOP>(TQ, NBA, a, lds, st) : launch_tq<BF, 2, KTOP>(TQ, NBA, a, lds, st);
+hipError_t scan_ksg(int KSG, int TQ, const ScanArgs& a, size_t lds, hipStream_t st) {
+  return KSG == 1 ? scan_tq<BF, 1, KTOP>(TQ, a, lds, st) : scan_tq<BF, 2, KTOP>(TQ, a, lds, st);
 }
 
 }  // namespace
 
-size_t traj_lds_bytes(bool bf, int TQ, int NBA, int ksg, int max_depth, int KTOP) {
-  const size_t np = bf ? 1 : 3;
-  const size_t qg = 16 * TQ, mw = 16 * NBA;
-  const size_t qrow = 32 * ksg + 8;
-  size_t lds = np * qg * qrow * 2;
-  lds += kWaves * static_cast<size_t>(max_depth) * mw * 4 + 3 * qg * 4;
-  lds = (lds + 7) / 8 * 8;
-  const size_t tail = kWaves * qg * static_cast<size_t>(KTOP) * 8;
-  const size_t bits = kMaxL * 16 * 8;
-  return lds + (tail > bits ? tail : bits);
+size_t traj_qrows_bytes(int L, int E, fm_dtype dt, int b_pad) {
+  const Geo g = geometry(E);
+  const int np = dt == FM_BF16 ? 1 : 3;
+  const int nlg = (L + g.lpg - 1) / g.lpg;
+  // + slack: a stage's loads round the last group slab up to whole 4 KB
+  return static_cast<size_t>(nlg) * b_pad * np * qrow_bytes(g.ksg) + 16384;
 }
 
 hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int32_t* depth, int32_t max_depth,
@@ -626,61 +810,90 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
                                    const Workspace& ws, hipStream_t st) {
   const bool bf = s.map_dtype == FM_BF16;
   const int esz = bf ? 2 : 4;
-  TrajArgs a{};
-  // slot geometry: E | 32 (E >= 8) packs 32/E layers per 32 slots, otherwise
-  // each layer is padded to a multiple of 32 slots
-  if (s.E >= 8 && 32 % s.E == 0) {
-    a.spl = s.E;
-    a.lpg = 32 / s.E;
-    a.ksg = 1;
-  } else {
-    a.spl = (s.E + 31) / 32 * 32;
-    a.lpg = 1;
-    a.ksg = a.spl / 32;
-  }
+  const Geo geo = geometry(s.E);
   const int KTOP = k == 1 ? 1 : (k <= 4 ? 4 : 8);
-  const int tq_max = KTOP == 1 ? 16 : (KTOP == 4 ? 8 : 4);
+  const int tq_max = tq_limit(bf, geo.ksg, KTOP);
+  constexpr size_t kLds = 160 * 1024;
 
   for (int b0 = 0; b0 < B; b0 += kChunkB) {
     const int Bc = (B - b0) < kChunkB ? (B - b0) : kChunkB;
     int TQ = 1;
     while (16 * TQ < Bc && TQ < tq_max) TQ *= 2;
+    if (dbg_scores != nullptr) TQ = 1;   // the dense-output variant exists for one shape only
+    // smaller query groups when the staged planes of one would not fit the ring
+    while (TQ > 1 && scan_lds(bf, TQ, TQ <= 4 ? 2 : 1, geo.ksg, KTOP, max_depth) > kLds) TQ /= 2;
+    const int QG = 16 * TQ;
+    const int n_qg = (Bc + QG - 1) / QG;
+    const int b_pad = n_qg * QG;
+    const int nlg = (max_depth + geo.lpg - 1) / geo.lpg;
+
+    PrepArgs pa{};
+    pa.q = static_cast<const char*>(q) + static_cast<int64_t>(b0) * s.L * s.E * esz;
+    pa.depth = depth + b0;
+    pa.B = Bc;
+    pa.L = s.L;
+    pa.E = s.E;
+    pa.dmax = max_depth;
+    pa.geo = geo;
+    pa.nlg = nlg;
+    pa.b_pad = b_pad;
+    pa.qg = QG;
+    pa.ws = ws;
+    pa.flags = s.flags;
+    const dim3 pgrid(b_pad / 16, nlg + 4);
+    if (bf) hipLaunchKernelGGL(k_traj_prep<true>, pgrid, dim3(kThreads), 0, st, pa);
+    else hipLaunchKernelGGL(k_traj_prep<false>, pgrid, dim3(kThreads), 0, st, pa);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+
+    // Two 16-map blocks per wave unless the query group is large.
     const int NBA = TQ <= 4 ? 2 : 1;
-    const int n_qg = (Bc + 16 * TQ - 1) / (16 * TQ);
-    const int maps_per_slice = kWaves * 16 * NBA;
-    const int slices = s.n > 0 ? (s.n + maps_per_slice - 1) / maps_per_slice : 0;
+    const size_t lds = scan_lds(bf, TQ, NBA, geo.ksg, KTOP, max_depth);
+    if (lds > kLds) return hipErrorInvalidConfiguration;
+
+    const int slice_maps = 8 * 16 * NBA;
+    const int slices = s.n > 0 ? (s.n + slice_maps - 1) / slice_maps : 0;
+    // workgroups per query group: about one workgroup per CU in total
+    int R = 256 / n_qg;
+    if (R < 1) R = 1;
+    if (R > slices) R = slices > 0 ? slices : 1;
+    if (R > kMaxPartials) R = kMaxPartials;
+
+    ScanArgs a{};
     a.planes = s.planes;
-    a.plane_elems = s.plane_elems;
-    a.q = static_cast<const char*>(q) + static_cast<int64_t>(b0) * s.L * s.E * esz;
-    a.depth = depth + b0;
+    a.plane_bytes = s.plane_elems * esz;
     a.n = s.n;
     a.L = s.L;
     a.E = s.E;
+    a.geo = geo;
     a.B = Bc;
-    a.k = k;
-    a.n_qg = n_qg;
-    a.n_units = slices * n_qg;
-    a.grid = ((a.n_units > 0 ? a.n_units : 1) + 7) / 8 * 8;
+    a.b_pad = b_pad;
     a.dmax = max_depth;
+    a.n_qg = n_qg;
+    a.R = R;
+    a.slices = slices;
+    a.grid = (n_qg * R + 7) / 8 * 8;
     a.ws = ws;
-    a.flags = s.flags;
-    a.idx_out = idx_out != nullptr ? idx_out + static_cast<int64_t>(b0) * k : nullptr;
-    a.score_out = score_out != nullptr ? score_out + static_cast<int64_t>(b0) * k : nullptr;
     a.dbg = dbg_scores != nullptr ? dbg_scores + static_cast<int64_t>(b0) * s.n : nullptr;
-
-    const size_t lds = traj_lds_bytes(bf, TQ, NBA, a.ksg, max_depth, KTOP);
-    if (lds > 160 * 1024) return hipErrorInvalidConfiguration;
-    hipError_t err;
-    if (bf) {
-      err = KTOP == 1 ? launch_ksg<true, 1>(a.ksg, TQ, NBA, a, lds, st)
-          : KTOP == 4 ? launch_ksg<true, 4>(a.ksg, TQ, NBA, a, lds, st)
-                      : launch_ksg<true, 8>(a.ksg, TQ, NBA, a, lds, st);
+    if (dbg_scores != nullptr) {
+      // same arithmetic as the match kernels, plus the dense score stores
+      if (bf) err = geo.ksg == 1 ? scan_launch<true, 1, 2, 1, 1, true>(a, lds, st) : scan_launch<true, 1, 2, 2, 1, true>(a, lds, st);
+      else err = geo.ksg == 1 ? scan_launch<false, 1, 2, 1, 1, true>(a, lds, st) : scan_launch<false, 1, 2, 2, 1, true>(a, lds, st);
+    } else if (bf) {
+      err = KTOP == 1 ? scan_ksg<true, 1>(geo.ksg, TQ, a, lds, st)
+          : KTOP == 4 ? scan_ksg<true, 4>(geo.ksg, TQ, a, lds, st)
+                      : scan_ksg<true, 8>(geo.ksg, TQ, a, lds, st);
     } else {
-      err = KTOP == 1 ? launch_ksg<false, 1>(a.ksg, TQ, NBA, a, lds, st)
-          : KTOP == 4 ? launch_ksg<false, 4>(a.ksg, TQ, NBA, a, lds, st)
-                      : launch_ksg<false, 8>(a.ksg, TQ, NBA, a, lds, st);
+      err = KTOP == 1 ? scan_ksg<false, 1>(geo.ksg, TQ, a, lds, st)
+          : KTOP == 4 ? scan_ksg<false, 4>(geo.ksg, TQ, a, lds, st)
+                      : scan_ksg<false, 8>(geo.ksg, TQ, a, lds, st);
     }
     if (err != hipSuccess) return err;
+    if (idx_out != nullptr) {
+      err = launch_finalize(ws.partial, ws.perm, Bc, R, k, KTOP, idx_out + static_cast<int64_t>(b0) * k,
+                            score_out + static_cast<int64_t>(b0) * k, st);
+      if (err != hipSuccess) return err;
+    }
   }
   return hipSuccess;
 }
