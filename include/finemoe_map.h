@@ -95,14 +95,17 @@ typedef struct {
 } fm_select_params;
 
 /* Bytes of the layer-major map planes alone: L planes of cap rows of E
- * elements, each plane padded to 256 bytes.  For cap = 32768 maps of 24 x 60
- * float32 (Section 6.8's largest store, Qwen1.5-MoE shape) this is
- * 188,743,680 bytes. */
+ * elements rounded up to a multiple of 4 (the padding is stored as zeros),
+ * each plane padded to 256 bytes.  For cap = 32768 maps of 24 x 60 float32
+ * (Section 6.8's largest store, Qwen1.5-MoE shape) this is 188,743,680
+ * bytes. */
 size_t fm_map_bytes(int32_t cap, int32_t L, int32_t E, fm_dtype map_dtype);
 
-/* Bytes of the whole device buffer a store needs: map planes, embeddings
- * (cap x d_emb bf16), their float32 norms and 256 bytes of device flags,
- * each part 256-byte aligned.  Returns 0 for invalid sizes. */
+/* Bytes of the whole device buffer a store needs: map planes, the prefix
+ * inverse norms 1/|x[y][0:l+1]| of every map at every depth (L x cap float32,
+ * cap rounded up to 64, computed at insert time in float64), embeddings
+ * (cap x d_emb bf16), their float32 norms and 256 bytes of device flags, each
+ * part 256-byte aligned.  Returns 0 for invalid sizes. */
 size_t fm_store_bytes(int32_t cap, int32_t L, int32_t E, int32_t d_emb, fm_dtype map_dtype);
 
 /* Bytes of match workspace for a store of L layers of E experts (map_dtype)
@@ -130,8 +133,8 @@ fm_status fm_store_build(fm_store** out, const fm_store_desc* desc);
 /* Append n iterations (Step 5 of Section 3.2: new expert maps enter the
  * store).  maps: device [n][L][E] of map_dtype, map-major; embs: device
  * [n][d_emb] bf16, required when d_emb > 0 and ignored otherwise.  The maps
- * are transposed into the layer-major planes and the embedding norms are
- * computed.  slots_out: device [n] int32 receiving the store index of each
+ * are transposed into the layer-major planes, and their prefix norms and the
+ * embedding norms are computed.  slots_out: device [n] int32 receiving the store index of each
  * inserted iteration, or NULL.  FM_ERR_FULL if size + n > cap (nothing is
  * inserted).  n == 0 is a no-op. */
 fm_status fm_store_insert(fm_store* store, const void* maps, const void* embs, int32_t n,

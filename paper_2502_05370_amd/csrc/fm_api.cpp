@@ -41,22 +41,24 @@ bool valid_dtype(int t) { return t == FM_F32 || t == FM_BF16; }
 constexpr size_t kMaxGroupBytes = 0xF0000000u;
 
 struct Layout {
-  size_t plane_bytes, maps, embs, norms, flags, total;
+  size_t plane_bytes, maps, rnorm, embs, norms, flags, total;
   int64_t plane_elems;
 };
 
-// Buffer layout: [L map planes][embeddings][norms][flags], 256-byte aligned parts.
+// Buffer layout: [L map planes][L prefix inverse-norm planes][embeddings]
+// [embedding norms][flags], 256-byte aligned parts.
 bool make_layout(int32_t cap, int32_t L, int32_t E, int32_t d_emb, fm_dtype t, Layout* out) {
   if (cap < 1 || L < 1 || E < 1 || d_emb < 0 || !valid_dtype(t)) return false;
   Layout ly;
   const size_t es = elem_size(t);
-  ly.plane_bytes = fm::align_up(static_cast<size_t>(cap) * E * es, fm::kAlign);
+  ly.plane_bytes = fm::align_up(static_cast<size_t>(cap) * fm::row_elems(E) * es, fm::kAlign);
   ly.plane_elems = static_cast<int64_t>(ly.plane_bytes / es);
   ly.maps = ly.plane_bytes * L;
+  ly.rnorm = fm::align_up(static_cast<size_t>(fm::rnorm_stride(cap)) * L * 4, fm::kAlign);
   ly.embs = fm::align_up(static_cast<size_t>(cap) * d_emb * 2, fm::kAlign);
   ly.norms = d_emb > 0 ? fm::align_up(static_cast<size_t>(cap) * 4, fm::kAlign) : 0;
   ly.flags = fm::kAlign;
-  ly.total = ly.maps + ly.embs + ly.norms + ly.flags;
+  ly.total = ly.maps + ly.rnorm + ly.embs + ly.norms + ly.flags;
   *out = ly;
   return true;
 }
@@ -180,7 +182,7 @@ fm_status fm_store_build(fm_store** out, const fm_store_desc* d) {
   if (d->L > fm::kMaxL) return fail(FM_ERR_UNSUPPORTED, "L=%d exceeds %d layers", d->L, fm::kMaxL);
   if (d->d_emb % 128 != 0)
     return fail(FM_ERR_UNSUPPORTED, "d_emb=%d is not a multiple of 128", d->d_emb);
-  if (static_cast<int64_t>(d->cap) * d->E > (static_cast<int64_t>(1) << 31) - 1)
+  if (static_cast<int64_t>(d->cap) * fm::row_elems(d->E) > (static_cast<int64_t>(1) << 31) - 1)
     return fail(FM_ERR_UNSUPPORTED, "cap*E exceeds 2^31-1");
   Layout ly;
   make_layout(d->cap, d->L, d->E, d->d_emb, d->map_dtype, &ly);
@@ -203,12 +205,16 @@ fm_status fm_store_build(fm_store** out, const fm_store_desc* d) {
   char* base = static_cast<char*>(d->buffer);
   s->v.planes = base;
   s->v.plane_elems = ly.plane_elems;
-  s->v.embs = d->d_emb > 0 ? reinterpret_cast<uint16_t*>(base + ly.maps) : nullptr;
-  s->v.emb_norm = d->d_emb > 0 ? reinterpret_cast<float*>(base + ly.maps + ly.embs) : nullptr;
-  s->v.flags = reinterpret_cast<uint32_t*>(base + ly.maps + ly.embs + ly.norms);
+  s->v.rnorm = reinterpret_cast<float*>(base + ly.maps);
+  s->v.rn_stride = fm::rnorm_stride(d->cap);
+  char* after = base + ly.maps + ly.rnorm;
+  s->v.embs = d->d_emb > 0 ? reinterpret_cast<uint16_t*>(after) : nullptr;
+  s->v.emb_norm = d->d_emb > 0 ? reinterpret_cast<float*>(after + ly.embs) : nullptr;
+  s->v.flags = reinterpret_cast<uint32_t*>(after + ly.embs + ly.norms);
   s->v.cap = d->cap;
   s->v.L = d->L;
   s->v.E = d->E;
+  s->v.row = fm::row_elems(d->E);
   s->v.d_emb = d->d_emb;
   s->v.n = 0;
   s->v.map_dtype = d->map_dtype;

@@ -19,14 +19,23 @@ constexpr size_t kAlign = 256;
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Device view of a store: layer-major map planes, embeddings and norms.
+// Row stride of the map planes: E rounded up to a multiple of 4 elements (the
+// padding is stored as zeros).
+inline int32_t row_elems(int32_t E) { return (E + 3) / 4 * 4; }
+// Stride of the prefix inverse-norm planes: cap rounded up to 64 maps.
+inline int64_t rnorm_stride(int32_t cap) { return (static_cast<int64_t>(cap) + 63) / 64 * 64; }
+
+// Device view of a store: layer-major map planes, prefix inverse norms,
+// embeddings and their norms.
 struct StoreView {
-  void* planes;          // [L][cap][E] elements of map dtype; plane stride plane_elems
-  int64_t plane_elems;   // elements per plane (cap * E, padded to 256 bytes)
+  void* planes;          // [L][cap][row] elements of map dtype; plane stride plane_elems
+  int64_t plane_elems;   // elements per plane (cap * row, padded to 256 bytes)
+  float* rnorm;          // [L][rn_stride]: 1/|x[y][0:l+1]| (0 for a zero prefix, NaN for NaN)
+  int64_t rn_stride;
   uint16_t* embs;        // [cap][d_emb] bf16
   float* emb_norm;       // [cap]
   uint32_t* flags;       // sticky FM_FLAG_* bits
-  int32_t cap, L, E, d_emb, n;
+  int32_t cap, L, E, row, d_emb, n;
   fm_dtype map_dtype;
 };
 

@@ -20,7 +20,7 @@ namespace {
 struct SelArgs {
   const void* planes;
   int64_t plane_elems;
-  int32_t n, L, E;
+  int32_t n, L, E, row;
   fm_dtype dtype;
   const int32_t* idx;
   const float* score;
@@ -36,7 +36,7 @@ struct SelArgs {
 };
 
 __device__ __forceinline__ double stored_prob(const SelArgs& a, int y, int l, int j) {
-  const int64_t off = static_cast<int64_t>(l) * a.plane_elems + static_cast<int64_t>(y) * a.E + j;
+  const int64_t off = static_cast<int64_t>(l) * a.plane_elems + static_cast<int64_t>(y) * a.row + j;
   if (a.dtype == FM_F32) return static_cast<double>(static_cast<const float*>(a.planes)[off]);
   return static_cast<double>(bf16_to_f32(static_cast<const uint16_t*>(a.planes)[off]));
 }
@@ -154,6 +154,7 @@ hipError_t launch_select(const StoreView& s, const int32_t* idx, const float* sc
   a.n = s.n;
   a.L = s.L;
   a.E = s.E;
+  a.row = s.row;
   a.dtype = s.map_dtype;
   a.idx = idx;
   a.score = score;

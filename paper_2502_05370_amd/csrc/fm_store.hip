@@ -1,7 +1,8 @@
 // Store residency: new iterations enter the Expert Map Store (Step 5 of
 // Section 3.2).  Maps arrive map-major [n][L][E] and are transposed into
-// layer-major planes [L][cap][E], so a scan over the first p layers reads p
-// contiguous planes.  Embeddings are copied row by row and their norms are
+// layer-major planes [L][cap][row] (row = E rounded up to 4, zero padded), so
+// a scan over the first p layers reads p contiguous planes; the prefix
+// inverse norms of every map at every depth are computed once here.  Embeddings are copied row by row and their norms are
 // computed once here (float64 sum of squares, rounded to float32), so the
 // semantic scan (Eq. 4) never recomputes them.
 #include "fm_device.h"
@@ -9,21 +10,45 @@
 
 namespace fm {
 
+// One wavefront per new map: each layer row is copied into its plane (with
+// zeros in the row padding), and the running float64 sum of squares over
+// layers 0..l gives the prefix inverse norm 1/|x[y][0:l+1]| that the
+// trajectory scan (Eq. 5) divides by at depth l+1.
 template <typename T>
 __global__ void __launch_bounds__(256) k_insert_maps(const T* __restrict__ src, T* __restrict__ planes,
-                                                     int64_t plane_elems, int32_t first_slot, int32_t n_new,
-                                                     int32_t L, int32_t E, int32_t* __restrict__ slots_out) {
-  // One thread per element of the map-major input (coalesced reads).
-  const int64_t total = static_cast<int64_t>(n_new) * L * E;
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
-  for (int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; t < total; t += stride) {
-    const int64_t row = t / E;            // (i, l)
-    const int32_t e = static_cast<int32_t>(t - row * E);
-    const int32_t i = static_cast<int32_t>(row / L);
-    const int32_t l = static_cast<int32_t>(row - static_cast<int64_t>(i) * L);
-    planes[l * plane_elems + static_cast<int64_t>(first_slot + i) * E + e] = src[t];
-    if (slots_out != nullptr && l == 0 && e == 0) slots_out[i] = first_slot + i;
+                                                     int64_t plane_elems, float* __restrict__ rnorm,
+                                                     int64_t rn_stride, int32_t first_slot, int32_t n_new,
+                                                     int32_t L, int32_t E, int32_t row,
+                                                     int32_t* __restrict__ slots_out) {
+  const int lane = threadIdx.x % kWave;
+  const int i = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+  if (i >= n_new) return;
+  const int64_t y = static_cast<int64_t>(first_slot) + i;
+  double cum = 0.0;
+  for (int l = 0; l < L; ++l) {
+    double sq = 0.0;
+    for (int e = lane; e < row; e += kWave) {
+      T v = T(0);
+      if (e < E) v = src[(static_cast<int64_t>(i) * L + l) * E + e];
+      planes[l * plane_elems + y * row + e] = v;
+      double f;
+      if constexpr (sizeof(T) == 2) f = static_cast<double>(bf16_to_f32(v));
+      else f = static_cast<double>(v);
+      sq += f * f;
+    }
+    // fixed-order tree reduction across the wave
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) sq += __shfl_xor(sq, m, kWave);
+    cum += sq;
+    if (lane == 0) {
+      float r;
+      if (cum != cum) r = __uint_as_float(0x7fc00000u);
+      else if (cum == 0.0) r = 0.0f;
+      else r = static_cast<float>(1.0 / sqrt(cum));
+      rnorm[l * rn_stride + y] = r;
+    }
   }
+  if (slots_out != nullptr && lane == 0) slots_out[i] = static_cast<int32_t>(y);
 }
 
 // One wavefront per embedding row: copy it and compute its norm.
@@ -51,21 +76,20 @@ __global__ void __launch_bounds__(256) k_insert_embs(const uint16_t* __restrict_
 hipError_t launch_insert(const StoreView& s, const void* maps, const void* embs, int32_t n_new,
                          int32_t* slots_out, hipStream_t st) {
   if (n_new <= 0) return hipSuccess;
-  const int64_t total = static_cast<int64_t>(n_new) * s.L * s.E;
-  int64_t blocks64 = (total + 255) / 256;
-  const int blocks = static_cast<int>(blocks64 > 65536 ? 65536 : blocks64);
+  const int rows_per_block = 256 / kWave;
+  const dim3 grid((n_new + rows_per_block - 1) / rows_per_block);
   if (s.map_dtype == FM_F32) {
-    hipLaunchKernelGGL(k_insert_maps<float>, dim3(blocks), dim3(256), 0, st, static_cast<const float*>(maps),
-                       static_cast<float*>(s.planes), s.plane_elems, s.n, n_new, s.L, s.E, slots_out);
+    hipLaunchKernelGGL(k_insert_maps<float>, grid, dim3(256), 0, st, static_cast<const float*>(maps),
+                       static_cast<float*>(s.planes), s.plane_elems, s.rnorm, s.rn_stride, s.n, n_new, s.L, s.E,
+                       s.row, slots_out);
   } else {
-    hipLaunchKernelGGL(k_insert_maps<uint16_t>, dim3(blocks), dim3(256), 0, st,
-                       static_cast<const uint16_t*>(maps), static_cast<uint16_t*>(s.planes), s.plane_elems, s.n,
-                       n_new, s.L, s.E, slots_out);
+    hipLaunchKernelGGL(k_insert_maps<uint16_t>, grid, dim3(256), 0, st, static_cast<const uint16_t*>(maps),
+                       static_cast<uint16_t*>(s.planes), s.plane_elems, s.rnorm, s.rn_stride, s.n, n_new, s.L,
+                       s.E, s.row, slots_out);
   }
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   if (s.d_emb > 0) {
-    const int rows_per_block = 256 / kWave;
     hipLaunchKernelGGL(k_insert_embs, dim3((n_new + rows_per_block - 1) / rows_per_block), dim3(256), 0, st,
                        static_cast<const uint16_t*>(embs), s.embs, s.emb_norm, s.n, n_new, s.d_emb);
     err = hipGetLastError();

@@ -83,7 +83,9 @@ struct PrepArgs {
 struct ScanArgs {
   const void* planes;
   int64_t plane_bytes;
-  int32_t n, L, E;
+  const float* rnorm;   // [L][rn_stride] prefix inverse norms
+  int64_t rn_stride;
+  int32_t n, L, E, row;
   Geo geo;
   int32_t B, b_pad, dmax;
   int32_t n_qg;       // query groups
@@ -324,21 +326,22 @@ __global__ void __launch_bounds__(256) k_traj_prep(PrepArgs a) {
 
 // ----------------------------------------------------------------------------- scan
 
-// 8 waves; wave w owns NBA blocks of 16 maps of every slice.  Stage j of a
-// workgroup = (slice s_begin + j / NLG, layer group j % NLG).  Map operands of
-// stage j+3 are loaded into registers while stage j computes; the query
-// planes of stage j+3 are copied into LDS ring slot (j+3) % 4 by direct
-// global->LDS loads.  Every wave issues the same number of loads per stage
-// (stand-in addresses keep the count fixed), so "stage j has landed" is
-// vmcnt <= 3 * (loads per stage).
+// 8 waves; wave w owns NBA blocks of 16 maps of every slice (W * 16 * NBA
+// maps).  Stage j of a workgroup = (slice s_begin + j / NLG, layer group
+// j % NLG).  The map rows of stage j+2 are loaded into registers with raw
+// buffer loads, and the query planes of stage j+2 into LDS ring slot
+// (j+2) % 4 with direct global->LDS loads, right after stage j computes.
+// Every wave issues the same loads per stage (out-of-range offsets keep the
+// count fixed), so "stage j has landed" is vmcnt <= loads of one stage.  The
+// slot written after stage j was last read in stage j-2, which every wave
+// finished before the barrier of stage j, so one barrier per stage suffices.
 template <bool BF, int TQ, int NBA, int KSG, int KTOP, bool DBG>
 __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
-  using T = typename std::conditional<BF, uint16_t, float>::type;
   using Raw = typename std::conditional<BF, u16x8, floatx8>::type;
   constexpr int W = 8;                        // waves per workgroup
-  constexpr int D = 3;                        // stages in flight
-  constexpr int NS = D + 1;                   // LDS ring slots
-  constexpr int esz = sizeof(T);
+  constexpr int D = 2;                        // stages in flight
+  constexpr int NS = D + 2;                   // LDS ring slots
+  constexpr int esz = BF ? 2 : 4;
   constexpr int QG = 16 * TQ;                 // queries per group
   constexpr int MW = 16 * NBA;                // maps per wave and slice
   constexpr int NP = BF ? 1 : 3;              // bf16 parts per operand
@@ -346,15 +349,13 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
   constexpr int RB = 64 * KSG + 16;           // staged query plane row bytes
   constexpr int NI_Q = (NP * QG * RB + W * 1024 - 1) / (W * 1024);  // 1 KB query loads per wave and stage
   constexpr int Q_STAGE = W * NI_Q * 1024;
-  constexpr int LA = BF ? 1 : 2;              // 16-byte map loads per (block, k-step)
-  constexpr int NI_A = NBA * KSG * LA;        // map load instructions per wave and stage
+  constexpr int NI_A = NBA * KSG * 2;         // map loads per wave and stage (two halves per unit)
   constexpr int NI = NI_A + NI_Q;
   static_assert((D - 1) * NI < 64, "vmcnt field is 6 bits");
 
   extern __shared__ __align__(16) unsigned char smem[];
   unsigned char* ring = smem;                                              // [NS][Q_STAGE]
-  float* cum = reinterpret_cast<float*>(smem + NS * Q_STAGE);             // [W][dmax][MW]
-  int32_t* gperm = reinterpret_cast<int32_t*>(cum + W * a.dmax * MW);      // [QG]
+  int32_t* gperm = reinterpret_cast<int32_t*>(smem + NS * Q_STAGE);        // [QG]
   int32_t* gdep = gperm + QG;                                              // [QG]
   float* grq = reinterpret_cast<float*>(gdep + QG);                        // [QG]
   uint64_t* mbuf = reinterpret_cast<uint64_t*>(smem);                      // after the loop: [W][QG][KTOP]
@@ -394,31 +395,28 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
   for (int t = 0; t < TQ; ++t) best[t].clear();
 
   if (active && nstages > 0) {
-    // lane constants: slot run 32*ks + 8*g of the lane's map row
-    int r_li[KSG], r_e0[KSG], r_nv[KSG];
+    // lane constants: the 8-slot unit 32*ks + 8*g of the lane's map row is
+    // experts e0 .. e0+7 of layer li of the layer group
+    uint32_t lane_off[KSG];
+    int r_nv[KSG];
 #pragma unroll
     for (int ks = 0; ks < KSG; ++ks) {
       const int s0 = 32 * ks + 8 * g;
       const int li = s0 / a.geo.spl;
       const int e0 = s0 - li * a.geo.spl;
-      const int nv = a.E - e0;
-      r_li[ks] = li;
-      r_e0[ks] = e0;
-      r_nv[ks] = nv < 0 ? 0 : (nv > 8 ? 8 : nv);
+      const int nv = a.row - e0;
+      r_nv[ks] = nv < 0 ? 0 : nv;
+      lane_off[ks] = static_cast<uint32_t>(li) * static_cast<uint32_t>(a.plane_bytes) + static_cast<uint32_t>(e0 * esz);
     }
-    // Map rows are read with raw buffer loads over the planes of one layer
-    // group.  Rows past the store, padding units, the upper half of a unit
-    // holding at most 4 experts and layers at or past L use offsets beyond
-    // the descriptor's range and read as zeros without touching memory.
     const char* planes = static_cast<const char*>(a.planes);
-    uint32_t lane_off[KSG];
-#pragma unroll
-    for (int ks = 0; ks < KSG; ++ks)
-      lane_off[ks] = static_cast<uint32_t>(r_li[ks]) * static_cast<uint32_t>(a.plane_bytes) +
-                     static_cast<uint32_t>(r_e0[ks] * esz);
-    const uint32_t row_bytes = static_cast<uint32_t>(a.E * esz);
+    const uint32_t row_bytes = static_cast<uint32_t>(a.row * esz);
     const char* qrows = static_cast<const char*>(a.ws.qrows);
 
+    // Map rows are read with raw buffer loads over the planes of one layer
+    // group.  Rows past the store, padding units, the upper half of a unit
+    // holding 4 experts and layers at or past L use offsets beyond the
+    // descriptor's range and read as zeros without touching memory (the row
+    // padding itself is stored as zeros).
     auto load_a = [&](int j, Raw (&dst)[NBA][KSG]) {
       const bool real = j < nstages;
       const int si = real ? s_begin + j / NLG : s_begin;
@@ -461,71 +459,44 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
     };
 
     floatx4 acc[NBA][TQ];
-    float cumsq[NBA];
 #pragma unroll
-    for (int nb = 0; nb < NBA; ++nb) {
-      cumsq[nb] = 0.0f;
+    for (int nb = 0; nb < NBA; ++nb)
 #pragma unroll
       for (int t = 0; t < TQ; ++t) acc[nb][t] = floatx4{0.f, 0.f, 0.f, 0.f};
-    }
 
-    Raw ar0[NBA][KSG], ar1[NBA][KSG], ar2[NBA][KSG];
+    Raw ar0[NBA][KSG], ar1[NBA][KSG];
     load_a(0, ar0);
     load_q(0);
     load_a(1, ar1);
     load_q(1);
-    load_a(2, ar2);
-    load_q(2);
 
-    auto stage = [&](int j, Raw (&cur)[NBA][KSG]) {
+    auto stage = [&](int j, const Raw (&cur)[NBA][KSG]) {
       const int si = s_begin + j / NLG;
       const int lg = j % NLG;
       const int y_wave = si * (W * MW) + w * MW;
       const unsigned char* sq = ring + (j % NS) * Q_STAGE;
 
-      // query planes of stage j are in LDS once every wave's loads of it
-      // landed (only stages j+1 and j+2 may still be in flight)
+      // stage j's map rows and every wave's query loads of it have landed
+      // once at most the next stage's loads are in flight
       wait_vmcnt<(D - 1) * NI>();
       raw_barrier();
 
-      // Per k-step: the map operand (already zero outside the store and past
-      // L; a unit ending inside a 4-element half is masked here), its squared
-      // norms and bf16 parts, then the MFMAs.  Tiles are sorted by depth
-      // (deepest first); a chunk of TC tiles runs while its first tile is
-      // active, and inactive tiles inside a chunk only add zeros (their staged
-      // rows are zero).
+      // Per k-step: bf16 parts of the map operand, then the MFMAs.  Tiles
+      // are sorted by depth (deepest first); a chunk of TC tiles runs while
+      // its first tile is active (the first chunk always is), and inactive
+      // tiles inside a chunk only add zeros (their staged rows are zero).
       const int l_first = lg * a.geo.lpg;
-      const bool ragged = (a.E & 3) != 0;
-      float lsq[NBA];
-#pragma unroll
-      for (int nb = 0; nb < NBA; ++nb) lsq[nb] = 0.0f;
 #pragma unroll
       for (int ks = 0; ks < KSG; ++ks) {
         u16x8 ap[NP][NBA];
 #pragma unroll
         for (int nb = 0; nb < NBA; ++nb) {
-          Raw v = cur[nb][ks];
-          if (ragged) {
-#pragma unroll
-            for (int jj = 0; jj < 8; ++jj)
-              if (jj >= r_nv[ks]) v[jj] = 0;
-          }
-          if constexpr (BF) {
-#pragma unroll
-            for (int jj = 0; jj < 8; ++jj) {
-              const float f = bf16_to_f32(v[jj]);
-              lsq[nb] = fmaf(f, f, lsq[nb]);
-            }
-            ap[0][nb] = v;
-          } else {
-#pragma unroll
-            for (int jj = 0; jj < 8; ++jj) lsq[nb] = fmaf(v[jj], v[jj], lsq[nb]);
-            split3(v, ap[0][nb], ap[1][nb], ap[2][nb]);
-          }
+          if constexpr (BF) ap[0][nb] = cur[nb][ks];
+          else split3(cur[nb][ks], ap[0][nb], ap[1][nb], ap[2][nb]);
         }
 #pragma unroll
         for (int tc = 0; tc < TQ; tc += TC) {
-          if (tmd[tc] <= l_first) break;
+          if (tc > 0 && tmd[tc] <= l_first) break;
           u16x8 bq[NP][TC];
 #pragma unroll
           for (int tt = 0; tt < TC; ++tt) {
@@ -553,96 +524,51 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
         }
       }
 
-      // per-layer sums: with LPG == 1 all four lane groups hold one layer;
-      // with LPG > 1 layer li occupies lane groups [li*E/8, (li+1)*E/8)
-#pragma unroll
-      for (int nb = 0; nb < NBA; ++nb) {
-        if (a.geo.lpg == 1 || a.E == 32) {
-          lsq[nb] += __shfl_xor(lsq[nb], 16, kWave);
-          lsq[nb] += __shfl_xor(lsq[nb], 32, kWave);
-        } else if (a.E == 16) {
-          lsq[nb] += __shfl_xor(lsq[nb], 16, kWave);
-        }
-      }
-      for (int li = 0; li < a.geo.lpg; ++li) {
-        const int l = lg * a.geo.lpg + li;
-        const int src = c + 16 * (a.geo.lpg == 1 ? 0 : (li * a.E) / 8);
-#pragma unroll
-        for (int nb = 0; nb < NBA; ++nb) {
-          const float v = __shfl(lsq[nb], src, kWave);
-          cumsq[nb] += v;
-          if (g == 0 && l < a.dmax) cum[(w * a.dmax + l) * MW + 16 * nb + c] = cumsq[nb];
-        }
-      }
-
       if (lg == NLG - 1) {
-        // end of a slice: 1/|x[y][0:p]| at every depth of this wave's maps
-        // (the table is per wave), cosine, optional dense output, top-K
-        const int D_g = tmd[0];
-        wait_lgkm0();
-        for (int i = lane; i < D_g * MW; i += kWave) {
-          const float v = cum[w * a.dmax * MW + i];
-          cum[w * a.dmax * MW + i] = v > 0.0f ? 1.0f / sqrtf(v) : (v != v ? v : 0.0f);
-        }
-        wait_lgkm0();
+        // End of a slice: cosine = dot * 1/|q[0:p]| * 1/|x[y][0:p]| with the
+        // store's prefix inverse norm at the query's depth p; lane (g, c)
+        // holds maps 16nb + 4g + i (i = 0..3) of query column c of each tile.
 #pragma unroll
         for (int t = 0; t < TQ; ++t) {
           const int r = 16 * t + c;
           const int p = gdep[r];
-          if (p == 0) continue;
           const float rq = grq[r];
 #pragma unroll
           for (int nb = 0; nb < NBA; ++nb) {
+            const int y0 = y_wave + 16 * nb + 4 * g;
+            const float* rsp = (p > 0 && y0 < a.n) ? a.rnorm + static_cast<int64_t>(p - 1) * a.rn_stride + y0 : a.rnorm;
+            const floatx4 rs = *reinterpret_cast<const floatx4*>(rsp);
+            if (p == 0) continue;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-              const int jm = 16 * nb + 4 * g + i;
-              const int y = y_wave + jm;
+              const int y = y0 + i;
               if (y >= a.n) continue;
-              const float rs = cum[(w * a.dmax + (p - 1)) * MW + jm];
-              const float s = acc[nb][t][i] * rq * rs;
+              const float s = acc[nb][t][i] * rq * rs[i];
               if constexpr (DBG) a.dbg[static_cast<int64_t>(gperm[r]) * a.n + y] = s;
               best[t].push(make_key(s, y));
             }
           }
         }
 #pragma unroll
-        for (int nb = 0; nb < NBA; ++nb) {
-          cumsq[nb] = 0.0f;
+        for (int nb = 0; nb < NBA; ++nb)
 #pragma unroll
           for (int t = 0; t < TQ; ++t) acc[nb][t] = floatx4{0.f, 0.f, 0.f, 0.f};
-        }
       }
-      wait_lgkm0();
-      raw_barrier();   // every wave is done with ring slot j % NS
     };
 
-    // three-stage register rotation: stage j computes from ar[j % 3] and
-    // then reloads it with stage j + 3
+    // two-stage register rotation: stage j computes from ar[j % 2] and then
+    // reloads it with stage j + 2
     int j = 0;
-    for (; j + 3 <= nstages; j += 3) {
+    for (; j + 2 <= nstages; j += 2) {
       stage(j, ar0);
-      load_a(j + 3, ar0);
-      load_q(j + 3);
+      load_a(j + 2, ar0);
+      load_q(j + 2);
       stage(j + 1, ar1);
-      load_a(j + 4, ar1);
-      load_q(j + 4);
-      stage(j + 2, ar2);
-      load_a(j + 5, ar2);
-      load_q(j + 5);
-    }
-    if (j < nstages) {
-      stage(j, ar0);
-      load_a(j + 3, ar0);
-      load_q(j + 3);
-      ++j;
-    }
-    if (j < nstages) {
-      stage(j, ar1);
       load_a(j + 3, ar1);
       load_q(j + 3);
-      ++j;
     }
-    wait_vmcnt<0>();   // drain the trailing stand-in loads
+    if (j < nstages) stage(j, ar0);
+    wait_vmcnt<0>();   // drain the trailing loads
     __syncthreads();
   }
 
@@ -739,18 +665,16 @@ Geo geometry(int E) {
   return g;
 }
 
-// LDS of the scan: 4 ring slots of query planes (8 waves x NI_Q x 1 KB each),
-// the per-wave prefix-norm tables and the group's sorted query info; the
-// top-K merge buffer reuses the ring.
-size_t scan_lds(bool bf, int TQ, int NBA, int KSG, int KTOP, int dmax) {
+// LDS of the scan: 4 ring slots of query planes (8 waves x NI_Q x 1 KB each)
+// and the group's sorted query info; the top-K merge buffer reuses the ring.
+size_t scan_lds(bool bf, int TQ, int KSG, int KTOP) {
   const int NP = bf ? 1 : 3;
-  const int QG = 16 * TQ, MW = 16 * NBA;
-  const int RB = qrow_bytes(KSG);
-  const int ni_q = (NP * QG * RB + 8 * 1024 - 1) / (8 * 1024);
+  const int QG = 16 * TQ;
+  const int ni_q = (NP * QG * qrow_bytes(KSG) + 8 * 1024 - 1) / (8 * 1024);
   size_t ring = static_cast<size_t>(4) * 8 * ni_q * 1024;
   const size_t merge = static_cast<size_t>(8) * QG * KTOP * 8;
   if (merge > ring) ring = merge;
-  return ring + static_cast<size_t>(8) * dmax * MW * 4 + 3 * QG * 4 + 64;
+  return ring + static_cast<size_t>(3) * QG * 4;
 }
 
 template <bool BF, int TQ, int NBA, int KSG, int KTOP, bool DBG = false>
@@ -821,7 +745,7 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
     while (16 * TQ < Bc && TQ < tq_max) TQ *= 2;
     if (dbg_scores != nullptr) TQ = 1;   // the dense-output variant exists for one shape only
     // smaller query groups when the staged planes of one would not fit the ring
-    while (TQ > 1 && scan_lds(bf, TQ, TQ <= 4 ? 2 : 1, geo.ksg, KTOP, max_depth) > kLds) TQ /= 2;
+    while (TQ > 1 && scan_lds(bf, TQ, geo.ksg, KTOP) > kLds) TQ /= 2;
     const int QG = 16 * TQ;
     const int n_qg = (Bc + QG - 1) / QG;
     const int b_pad = n_qg * QG;
@@ -848,7 +772,7 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
 
     // Two 16-map blocks per wave unless the query group is large.
     const int NBA = TQ <= 4 ? 2 : 1;
-    const size_t lds = scan_lds(bf, TQ, NBA, geo.ksg, KTOP, max_depth);
+    const size_t lds = scan_lds(bf, TQ, geo.ksg, KTOP);
     if (lds > kLds) return hipErrorInvalidConfiguration;
 
     const int slice_maps = 8 * 16 * NBA;
@@ -862,6 +786,9 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
     ScanArgs a{};
     a.planes = s.planes;
     a.plane_bytes = s.plane_elems * esz;
+    a.rnorm = s.rnorm;
+    a.rn_stride = s.rn_stride;
+    a.row = s.row;
     a.n = s.n;
     a.L = s.L;
     a.E = s.E;
