@@ -72,7 +72,7 @@ def load() -> C.CDLL:
         return _LIB
     if not os.path.exists(LIB_PATH):
         raise ImportError(
-            f"{LIB_PATH} is missing: build it with `python -m paper_2502_05370_amd.build` "
+            f"{LIB_PATH} is missing: build it with `python paper_2502_05370_amd/build.py` "
             "(hipcc for gfx950); there is no CPU fallback")
     lib = C.CDLL(LIB_PATH)
     for name, (res, args) in SIGNATURES.items():

@@ -1,6 +1,8 @@
 """Build libfinemoe_map.so for gfx950 with hipcc (in-tree, no JIT cache).
 
-    python -m paper_2502_05370_amd.build        # or build.build()
+    python paper_2502_05370_amd/build.py        # or build.build()
+
+(run by path: importing the package itself needs the library built here).
 
 Every call recompiles every source.  Objects go to ``_build/`` next to this
 file; the shared library lands in the package directory.
