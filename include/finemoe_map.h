@@ -94,11 +94,13 @@ typedef struct {
     fm_blend blend;
 } fm_select_params;
 
-/* Bytes of the layer-major map planes alone: L planes of cap rows of E
- * elements rounded up to a multiple of 4 (the padding is stored as zeros),
- * each plane padded to 256 bytes.  For cap = 32768 maps of 24 x 60 float32
- * (Section 6.8's largest store, Qwen1.5-MoE shape) this is 188,743,680
- * bytes. */
+/* Bytes of the layer-major map planes alone: L planes of cap (rounded up to
+ * 16) rows of E elements rounded up to a multiple of 4 (the padding is stored
+ * as zeros), each plane padded to 256 bytes.  Inside a plane the maps are
+ * stored in tiles of 16: for every quad of 4 consecutive experts, the tile's
+ * 16 rows of that quad are contiguous.  For cap = 32768 maps of 24 x 60
+ * float32 (Section 6.8's largest store, Qwen1.5-MoE shape) this is
+ * 188,743,680 bytes. */
 size_t fm_map_bytes(int32_t cap, int32_t L, int32_t E, fm_dtype map_dtype);
 
 /* Bytes of the whole device buffer a store needs: map planes, the prefix

@@ -51,7 +51,7 @@ bool make_layout(int32_t cap, int32_t L, int32_t E, int32_t d_emb, fm_dtype t, L
   if (cap < 1 || L < 1 || E < 1 || d_emb < 0 || !valid_dtype(t)) return false;
   Layout ly;
   const size_t es = elem_size(t);
-  ly.plane_bytes = fm::align_up(static_cast<size_t>(cap) * fm::row_elems(E) * es, fm::kAlign);
+  ly.plane_bytes = fm::align_up(static_cast<size_t>(fm::round16(cap)) * fm::row_elems(E) * es, fm::kAlign);
   ly.plane_elems = static_cast<int64_t>(ly.plane_bytes / es);
   ly.maps = ly.plane_bytes * L;
   ly.rnorm = fm::align_up(static_cast<size_t>(fm::rnorm_stride(cap)) * L * 4, fm::kAlign);
@@ -182,7 +182,7 @@ fm_status fm_store_build(fm_store** out, const fm_store_desc* d) {
   if (d->L > fm::kMaxL) return fail(FM_ERR_UNSUPPORTED, "L=%d exceeds %d layers", d->L, fm::kMaxL);
   if (d->d_emb % 128 != 0)
     return fail(FM_ERR_UNSUPPORTED, "d_emb=%d is not a multiple of 128", d->d_emb);
-  if (static_cast<int64_t>(d->cap) * fm::row_elems(d->E) > (static_cast<int64_t>(1) << 31) - 1)
+  if (fm::round16(d->cap) * fm::row_elems(d->E) > (static_cast<int64_t>(1) << 31) - 1)
     return fail(FM_ERR_UNSUPPORTED, "cap*E exceeds 2^31-1");
   Layout ly;
   make_layout(d->cap, d->L, d->E, d->d_emb, d->map_dtype, &ly);

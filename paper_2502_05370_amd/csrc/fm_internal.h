@@ -19,17 +19,24 @@ constexpr size_t kAlign = 256;
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Row stride of the map planes: E rounded up to a multiple of 4 elements (the
-// padding is stored as zeros).
+// Map planes are tiled: plane l holds the maps in tiles of 16 consecutive maps;
+// inside a tile, each quad of 4 consecutive experts (e = 4q .. 4q+3) stores
+// the 16 maps' 4 values contiguously, so one wave reading 4 quads of a tile
+// reads one contiguous block.  row = E rounded up to a multiple of 4 (the
+// padding is stored as zeros), so a tile holds 16 * row elements.
 inline int32_t row_elems(int32_t E) { return (E + 3) / 4 * 4; }
+inline int64_t round16(int64_t cap) { return (cap + 15) / 16 * 16; }
+__host__ __device__ __forceinline__ int64_t tile_offset(int64_t y, int32_t e, int32_t row) {
+  return (y / 16) * 16 * row + (e / 4) * 64 + (y % 16) * 4 + (e % 4);
+}
 // Stride of the prefix inverse-norm planes: cap rounded up to 64 maps.
 inline int64_t rnorm_stride(int32_t cap) { return (static_cast<int64_t>(cap) + 63) / 64 * 64; }
 
 // Device view of a store: layer-major map planes, prefix inverse norms,
 // embeddings and their norms.
 struct StoreView {
-  void* planes;          // [L][cap][row] elements of map dtype; plane stride plane_elems
-  int64_t plane_elems;   // elements per plane (cap * row, padded to 256 bytes)
+  void* planes;          // [L] tiled planes (tile_offset) of map dtype; plane stride plane_elems
+  int64_t plane_elems;   // elements per plane (round16(cap) * row, padded to 256 bytes)
   float* rnorm;          // [L][rn_stride]: 1/|x[y][0:l+1]| (0 for a zero prefix, NaN for NaN)
   int64_t rn_stride;
   uint16_t* embs;        // [cap][d_emb] bf16

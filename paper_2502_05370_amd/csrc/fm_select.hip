@@ -36,7 +36,7 @@ struct SelArgs {
 };
 
 __device__ __forceinline__ double stored_prob(const SelArgs& a, int y, int l, int j) {
-  const int64_t off = static_cast<int64_t>(l) * a.plane_elems + static_cast<int64_t>(y) * a.row + j;
+  const int64_t off = static_cast<int64_t>(l) * a.plane_elems + tile_offset(y, j, a.row);
   if (a.dtype == FM_F32) return static_cast<double>(static_cast<const float*>(a.planes)[off]);
   return static_cast<double>(bf16_to_f32(static_cast<const uint16_t*>(a.planes)[off]));
 }

@@ -1,8 +1,9 @@
 // Store residency: new iterations enter the Expert Map Store (Step 5 of
 // Section 3.2).  Maps arrive map-major [n][L][E] and are transposed into
-// layer-major planes [L][cap][row] (row = E rounded up to 4, zero padded), so
-// a scan over the first p layers reads p contiguous planes; the prefix
-// inverse norms of every map at every depth are computed once here.  Embeddings are copied row by row and their norms are
+// layer-major planes of 16-map tiles (row = E rounded up to 4, zero padded;
+// see tile_offset), so a scan over the first p layers reads p contiguous
+// planes; the prefix inverse norms of every map at every depth are computed
+// once here.  Embeddings are copied row by row and their norms are
 // computed once here (float64 sum of squares, rounded to float32), so the
 // semantic scan (Eq. 4) never recomputes them.
 #include "fm_device.h"
@@ -30,7 +31,7 @@ __global__ void __launch_bounds__(256) k_insert_maps(const T* __restrict__ src, 
     for (int e = lane; e < row; e += kWave) {
       T v = T(0);
       if (e < E) v = src[(static_cast<int64_t>(i) * L + l) * E + e];
-      planes[l * plane_elems + y * row + e] = v;
+      planes[l * plane_elems + tile_offset(y, e, row)] = v;
       double f;
       if constexpr (sizeof(T) == 2) f = static_cast<double>(bf16_to_f32(v));
       else f = static_cast<double>(v);

@@ -241,33 +241,28 @@ __global__ void __launch_bounds__(256) k_traj_prep(PrepArgs a) {
       u16x8 h = u16x8{}, m = u16x8{}, l = u16x8{};
       const int b = s_b[r];
       if (b >= 0 && unit < 4 * a.geo.ksg) {
-        const int s0 = 8 * unit;
-        const int li = s0 / a.geo.spl;
-        const int e0 = s0 - li * a.geo.spl;
-        const int layer = lg * a.geo.lpg + li;
-        if (layer < s_d[r] && e0 < a.E) {
-          const T* src = q + (static_cast<int64_t>(b) * a.L + layer) * a.E + e0;
-          const int nv = a.E - e0 < 8 ? a.E - e0 : 8;
-          if constexpr (BF) {
-            if (nv == 8 && a.E % 4 == 0) {
-              const u16x4 lo = *reinterpret_cast<const u16x4*>(src);
-              const u16x4 hi = *reinterpret_cast<const u16x4*>(src + 4);
-              h = u16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-            } else {
-              for (int k = 0; k < nv; ++k) h[k] = src[k];
+        // k positions 8*unit .. 8*unit+7 hold the slot runs
+        // 32ks + 4g .. +3 and 32ks + 16 + 4g .. +3 (unit = 4ks + g), the
+        // order in which the scan loads the map quads
+        const int ks = unit / 4;
+        const int gg = unit - 4 * ks;
+        floatx8 v = floatx8{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const int s0 = 32 * ks + 16 * half + 4 * gg;
+          const int li = s0 / a.geo.spl;
+          const int e0 = s0 - li * a.geo.spl;
+          const int layer = lg * a.geo.lpg + li;
+          if (layer < s_d[r] && e0 < a.E) {
+            const T* src = q + (static_cast<int64_t>(b) * a.L + layer) * a.E + e0;
+            const int nv = a.E - e0 < 4 ? a.E - e0 : 4;
+            for (int k = 0; k < nv; ++k) {
+              if constexpr (BF) h[4 * half + k] = src[k];
+              else v[4 * half + k] = src[k];
             }
-          } else {
-            floatx8 v = floatx8{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-            if (nv == 8 && a.E % 4 == 0) {
-              const floatx4 lo = *reinterpret_cast<const floatx4*>(src);
-              const floatx4 hi = *reinterpret_cast<const floatx4*>(src + 4);
-              v = floatx8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-            } else {
-              for (int k = 0; k < nv; ++k) v[k] = src[k];
-            }
-            split3(v, h, m, l);
           }
         }
+        if constexpr (!BF) split3(v, h, m, l);
       }
       char* dst = slab + static_cast<int64_t>(row_in_grp) * rb + 16 * unit;
       *reinterpret_cast<u16x8*>(dst) = h;
@@ -395,28 +390,33 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
   for (int t = 0; t < TQ; ++t) best[t].clear();
 
   if (active && nstages > 0) {
-    // lane constants: the 8-slot unit 32*ks + 8*g of the lane's map row is
-    // experts e0 .. e0+7 of layer li of the layer group
-    uint32_t lane_off[KSG];
-    int r_nv[KSG];
+    // Lane constants.  Register element j of lane (g, c) in k-step ks holds
+    // slot 32ks + 4g + j (j < 4) or 32ks + 16 + 4g + j - 4 (j >= 4) of map
+    // row c of the block; each run of 4 slots is one quad of a layer of the
+    // group, so the two loads of a lane read one quad each and the 64 lanes
+    // of a load read 4 consecutive quads of a tile.
+    uint32_t lane_off[KSG][2];
+    bool quad_ok[KSG][2];
 #pragma unroll
     for (int ks = 0; ks < KSG; ++ks) {
-      const int s0 = 32 * ks + 8 * g;
-      const int li = s0 / a.geo.spl;
-      const int e0 = s0 - li * a.geo.spl;
-      const int nv = a.row - e0;
-      r_nv[ks] = nv < 0 ? 0 : nv;
-      lane_off[ks] = static_cast<uint32_t>(li) * static_cast<uint32_t>(a.plane_bytes) + static_cast<uint32_t>(e0 * esz);
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int s0 = 32 * ks + 16 * half + 4 * g;
+        const int li = s0 / a.geo.spl;
+        const int e0 = s0 - li * a.geo.spl;
+        quad_ok[ks][half] = e0 < a.row;
+        lane_off[ks][half] = static_cast<uint32_t>(li) * static_cast<uint32_t>(a.plane_bytes) +
+                             static_cast<uint32_t>(((e0 / 4) * 64 + c * 4) * esz);
+      }
     }
     const char* planes = static_cast<const char*>(a.planes);
-    const uint32_t row_bytes = static_cast<uint32_t>(a.row * esz);
+    const uint32_t tile_bytes = static_cast<uint32_t>(16 * a.row * esz);
     const char* qrows = static_cast<const char*>(a.ws.qrows);
 
-    // Map rows are read with raw buffer loads over the planes of one layer
-    // group.  Rows past the store, padding units, the upper half of a unit
-    // holding 4 experts and layers at or past L use offsets beyond the
-    // descriptor's range and read as zeros without touching memory (the row
-    // padding itself is stored as zeros).
+    // Map quads are read with raw buffer loads over the planes of one layer
+    // group.  Rows past the store, padding quads and layers at or past L use
+    // offsets beyond the descriptor's range and read as zeros without
+    // touching memory (the row padding itself is stored as zeros).
     auto load_a = [&](int j, Raw (&dst)[NBA][KSG]) {
       const bool real = j < nstages;
       const int si = real ? s_begin + j / NLG : s_begin;
@@ -428,13 +428,13 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
           static_cast<int>(static_cast<uint32_t>(nl) * static_cast<uint32_t>(a.plane_bytes)), kBufWord3);
 #pragma unroll
       for (int nb = 0; nb < NBA; ++nb) {
-        const int y = si * (W * MW) + w * MW + 16 * nb + c;
-        const bool row_ok = real && y < a.n;
-        const uint32_t row_off = static_cast<uint32_t>(y) * row_bytes;
+        const int y_blk = si * (W * MW) + w * MW + 16 * nb;
+        const bool row_ok = real && y_blk + c < a.n;
+        const uint32_t blk = static_cast<uint32_t>(y_blk / 16) * tile_bytes;
 #pragma unroll
         for (int ks = 0; ks < KSG; ++ks) {
-          const uint32_t lo = row_ok && r_nv[ks] > 0 ? lane_off[ks] + row_off : kOutside;
-          const uint32_t hi = r_nv[ks] > 4 ? lo + 4 * esz : kOutside;
+          const uint32_t lo = row_ok && quad_ok[ks][0] ? lane_off[ks][0] + blk : kOutside;
+          const uint32_t hi = row_ok && quad_ok[ks][1] ? lane_off[ks][1] + blk : kOutside;
           if constexpr (BF) {
             const uint32x2 vl = __builtin_amdgcn_raw_buffer_load_b64(rs, static_cast<int>(lo), 0, 0);
             const uint32x2 vh = __builtin_amdgcn_raw_buffer_load_b64(rs, static_cast<int>(hi), 0, 0);

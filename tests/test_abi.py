@@ -41,10 +41,10 @@ def test_store_footprint_matches_section_6_8():
         assert got == g["fp32_map_store_bytes_at_capacity_max"][name]
         assert lib.fm_store_bytes(cap, m["L"], m["E"], 0, L.FM_F32) < g["store_bytes_limit"]
     assert lib.fm_map_bytes(1000, 32, 8, L.FM_BF16) == 32 * 16128
-    # rows of E = 37 experts are padded to 40 elements
-    assert lib.fm_map_bytes(1000, 2, 37, L.FM_F32) == 2 * 160000
+    # rows of E = 37 experts are padded to 40 elements, cap to 1008 maps
+    assert lib.fm_map_bytes(1000, 2, 37, L.FM_F32) == 2 * 161280
     # prefix inverse norms: L planes of cap rounded up to 64 float32
-    assert lib.fm_store_bytes(1000, 2, 37, 0, L.FM_F32) == 2 * 160000 + 8192 + 256
+    assert lib.fm_store_bytes(1000, 2, 37, 0, L.FM_F32) == 2 * 161280 + 8192 + 256
     assert lib.fm_map_bytes(0, 32, 8, L.FM_F32) == 0
     assert lib.fm_store_bytes(10, 4, 4, 128, 7) == 0
 
