@@ -90,7 +90,7 @@ struct ScanArgs {
   int32_t B, b_pad, dmax;
   int32_t n_qg;       // query groups
   int32_t R;          // workgroups per query group
-  int32_t slices;     // map slices of 64*NBA maps
+  int32_t n_blocks;   // 16-map blocks of the store (ceil(n / 16))
   int32_t grid;
   Workspace ws;
   float* dbg;         // optional dense scores [B][n]
@@ -321,32 +321,31 @@ __global__ void __launch_bounds__(256) k_traj_prep(PrepArgs a) {
 
 // ----------------------------------------------------------------------------- scan
 
-// 8 waves; wave w owns NBA blocks of 16 maps of every slice (W * 16 * NBA
-// maps).  Stage j of a workgroup = (slice s_begin + j / NLG, layer group
-// j % NLG).  The map rows of stage j+2 are loaded into registers with raw
-// buffer loads, and the query planes of stage j+2 into LDS ring slot
-// (j+2) % 4 with direct global->LDS loads, right after stage j computes.
-// Every wave issues the same loads per stage (out-of-range offsets keep the
-// count fixed), so "stage j has landed" is vmcnt <= loads of one stage.  The
-// slot written after stage j was last read in stage j-2, which every wave
-// finished before the barrier of stage j, so one barrier per stage suffices.
+// 8 waves; wave w owns NBA blocks of 16 maps of every slice (W * NBA blocks
+// of the workgroup's range).  Stage j = (slice j / NLG, layer group j % NLG).
+// During stage j every wave loads its share of the query planes of stage j+2
+// into LDS ring slot (j+2) % 3 (direct global->LDS loads) and, once stage
+// j's map rows are split into bf16 parts, the map rows of stage j+2 into the
+// freed registers (raw buffer loads), so both overlap the MFMAs.  Every wave
+// issues the same loads per stage (out-of-range offsets keep the count fixed),
+// so "stage j has landed" is vmcnt <= the loads of one stage.  Slot (j+2) % 3
+// was last read in stage j-1, which every wave finished before the barrier of
+// stage j, so one barrier per stage suffices.
 template <bool BF, int TQ, int NBA, int KSG, int KTOP, bool DBG>
 __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
   using Raw = typename std::conditional<BF, u16x8, floatx8>::type;
   constexpr int W = 8;                        // waves per workgroup
-  constexpr int D = 2;                        // stages in flight
-  constexpr int NS = D + 2;                   // LDS ring slots
+  constexpr int NS = 3;                       // query-plane ring slots (two stages in flight)
   constexpr int esz = BF ? 2 : 4;
   constexpr int QG = 16 * TQ;                 // queries per group
   constexpr int MW = 16 * NBA;                // maps per wave and slice
   constexpr int NP = BF ? 1 : 3;              // bf16 parts per operand
-  constexpr int TC = TQ < 4 ? TQ : 4;         // query tiles per MFMA chunk
   constexpr int RB = 64 * KSG + 16;           // staged query plane row bytes
   constexpr int NI_Q = (NP * QG * RB + W * 1024 - 1) / (W * 1024);  // 1 KB query loads per wave and stage
   constexpr int Q_STAGE = W * NI_Q * 1024;
   constexpr int NI_A = NBA * KSG * 2;         // map loads per wave and stage (two halves per unit)
   constexpr int NI = NI_A + NI_Q;
-  static_assert((D - 1) * NI < 64, "vmcnt field is 6 bits");
+  static_assert(NI < 64, "vmcnt field is 6 bits");
 
   extern __shared__ __align__(16) unsigned char smem[];
   unsigned char* ring = smem;                                              // [NS][Q_STAGE]
@@ -368,8 +367,11 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
   const bool active = u < a.n_qg * a.R;
   const int qgrp = active ? u % a.n_qg : 0;
   const int rr = active ? u / a.n_qg : 0;
-  const int s_begin = active ? static_cast<int>((static_cast<int64_t>(rr) * a.slices) / a.R) : 0;
-  const int s_end = active ? static_cast<int>((static_cast<int64_t>(rr + 1) * a.slices) / a.R) : 0;
+  // this workgroup's maps: 16-map blocks [b_begin, b_end), an even share of
+  // the store, taken as slices of W * NBA blocks (the last one partial)
+  const int b_begin = active ? static_cast<int>((static_cast<int64_t>(rr) * a.n_blocks) / a.R) : 0;
+  const int b_end = active ? static_cast<int>((static_cast<int64_t>(rr + 1) * a.n_blocks) / a.R) : 0;
+  const int n_slices = (b_end - b_begin + W * NBA - 1) / (W * NBA);
   const int g0 = qgrp * QG;
 
   for (int r = tid; r < QG; r += W * kWave) {
@@ -383,7 +385,7 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
 #pragma unroll
   for (int t = 0; t < TQ; ++t) tmd[t] = gdep[16 * t];
   const int NLG = (tmd[0] + a.geo.lpg - 1) / a.geo.lpg;
-  const int nstages = (s_end - s_begin) * NLG;
+  const int nstages = n_slices * NLG;
 
   TopK<KTOP> best[TQ];
 #pragma unroll
@@ -419,7 +421,7 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
     // touching memory (the row padding itself is stored as zeros).
     auto load_a = [&](int j, Raw (&dst)[NBA][KSG]) {
       const bool real = j < nstages;
-      const int si = real ? s_begin + j / NLG : s_begin;
+      const int si = real ? j / NLG : 0;
       const int lg = real ? j % NLG : 0;
       const int l0 = lg * a.geo.lpg;
       const int nl = a.L - l0 < a.geo.lpg ? a.L - l0 : a.geo.lpg;
@@ -428,13 +430,14 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
           static_cast<int>(static_cast<uint32_t>(nl) * static_cast<uint32_t>(a.plane_bytes)), kBufWord3);
 #pragma unroll
       for (int nb = 0; nb < NBA; ++nb) {
-        const int y_blk = si * (W * MW) + w * MW + 16 * nb;
-        const bool row_ok = real && y_blk + c < a.n;
-        const uint32_t blk = static_cast<uint32_t>(y_blk / 16) * tile_bytes;
+        const int blk = b_begin + si * (W * NBA) + w * NBA + nb;
+        const int y_blk = 16 * blk;
+        const bool row_ok = real && blk < b_end && y_blk + c < a.n;
+        const uint32_t blk_off = static_cast<uint32_t>(blk) * tile_bytes;
 #pragma unroll
         for (int ks = 0; ks < KSG; ++ks) {
-          const uint32_t lo = row_ok && quad_ok[ks][0] ? lane_off[ks][0] + blk : kOutside;
-          const uint32_t hi = row_ok && quad_ok[ks][1] ? lane_off[ks][1] + blk : kOutside;
+          const uint32_t lo = row_ok && quad_ok[ks][0] ? lane_off[ks][0] + blk_off : kOutside;
+          const uint32_t hi = row_ok && quad_ok[ks][1] ? lane_off[ks][1] + blk_off : kOutside;
           if constexpr (BF) {
             const uint32x2 vl = __builtin_amdgcn_raw_buffer_load_b64(rs, static_cast<int>(lo), 0, 0);
             const uint32x2 vh = __builtin_amdgcn_raw_buffer_load_b64(rs, static_cast<int>(hi), 0, 0);
@@ -464,62 +467,137 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
 #pragma unroll
       for (int t = 0; t < TQ; ++t) acc[nb][t] = floatx4{0.f, 0.f, 0.f, 0.f};
 
+    // issue order: Q0 A0 Q1 A1, then during stage j: Q(j+2) A(j+2)
     Raw ar0[NBA][KSG], ar1[NBA][KSG];
-    load_a(0, ar0);
     load_q(0);
-    load_a(1, ar1);
+    load_a(0, ar0);
     load_q(1);
+    load_a(1, ar1);
 
-    auto stage = [&](int j, const Raw (&cur)[NBA][KSG]) {
-      const int si = s_begin + j / NLG;
+    // MFMAs of one k-step for the first NT (active) query tiles, term-major so
+    // that consecutive MFMAs update different accumulators.
+    auto mfma_tiles = [&](auto nt_const, int ks, const unsigned char* sq, const u16x8 (&ap)[NP][NBA][KSG]) {
+      constexpr int NT = decltype(nt_const)::value;
+      u16x8 bq[NP][NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int pl = 0; pl < NP; ++pl)
+          bq[pl][t] = *reinterpret_cast<const u16x8*>(sq + (pl * QG + 16 * t + c) * RB + (32 * ks + 8 * g) * 2);
+      if constexpr (BF) {
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+          for (int nb = 0; nb < NBA; ++nb) acc[nb][t] = mfma_bf16(ap[0][nb][ks], bq[0][t], acc[nb][t]);
+      } else {
+        // the six cross terms, small ones first, grouped by query part so
+        // that each part's fragments die early
+        constexpr int TA[6] = {0, 1, 0, 2, 1, 0};
+        constexpr int TB[6] = {2, 1, 1, 0, 0, 0};
+#pragma unroll
+        for (int term = 0; term < 6; ++term)
+#pragma unroll
+          for (int t = 0; t < NT; ++t)
+#pragma unroll
+            for (int nb = 0; nb < NBA; ++nb)
+              acc[nb][t] = mfma_bf16(ap[TA[term]][nb][ks], bq[TB[term]][t], acc[nb][t]);
+      }
+    };
+
+    // bf16 parts of the map operand of one stage.  k-step 0 is converted at
+    // the end of the previous stage, once this wave's loads of the stage have
+    // landed; further k-steps during the stage, between MFMAs.  The ring
+    // registers pass through an empty asm placed after the wait, so no use of
+    // them is scheduled above it (the compiler would then wait for every
+    // outstanding load itself, emptying the prefetch).
+    u16x8 ap[NP][NBA][KSG];
+    Raw held[NBA][KSG];
+    auto convert_ks = [&](int ks) {
+#pragma unroll
+      for (int nb = 0; nb < NBA; ++nb) {
+        if constexpr (BF) ap[0][nb][ks] = held[nb][ks];
+        else split3(held[nb][ks], ap[0][nb][ks], ap[1][nb][ks], ap[2][nb][ks]);
+      }
+    };
+    auto convert = [&](Raw (&ring_regs)[NBA][KSG]) {
+      wait_vmcnt<NI>();
+#pragma unroll
+      for (int nb = 0; nb < NBA; ++nb)
+#pragma unroll
+        for (int ks = 0; ks < KSG; ++ks) {
+          held[nb][ks] = ring_regs[nb][ks];
+          asm volatile("" : "+v"(held[nb][ks]));
+        }
+      convert_ks(0);
+    };
+
+    // Stage j: the map operand was converted at the end of stage j-1 (by a
+    // wave that may then wait at the barrier while the other wave of its SIMD
+    // finishes its MFMAs); after the barrier every wave's query planes of
+    // stage j are in LDS.
+    auto stage = [&](int j, Raw (&ring_regs)[NBA][KSG], Raw (&next_regs)[NBA][KSG]) {
+      const int si = j / NLG;
       const int lg = j % NLG;
-      const int y_wave = si * (W * MW) + w * MW;
+      const int blk_wave = b_begin + si * (W * NBA) + w * NBA;
       const unsigned char* sq = ring + (j % NS) * Q_STAGE;
 
-      // stage j's map rows and every wave's query loads of it have landed
-      // once at most the next stage's loads are in flight
-      wait_vmcnt<(D - 1) * NI>();
       raw_barrier();
+      // The query planes of stage j+2 go to slot (j+2) % 3 = (j-1) % 3,
+      // which every wave finished reading before this barrier; the map rows
+      // of stage j+2 go to the registers of stage j once all of its k-steps
+      // are converted.
+      load_q(j + 2);
 
-      // Per k-step: bf16 parts of the map operand, then the MFMAs.  Tiles
-      // are sorted by depth (deepest first); a chunk of TC tiles runs while
-      // its first tile is active (the first chunk always is), and inactive
-      // tiles inside a chunk only add zeros (their staged rows are zero).
+      // Query tiles are sorted by depth (deepest first): the first na tiles
+      // are those whose deepest query still has layers in this group (the
+      // first tile always does); shallower queries inside an active tile
+      // only add zeros (their staged rows are zero).
       const int l_first = lg * a.geo.lpg;
+      int na = 1;
+#pragma unroll
+      for (int t = 1; t < TQ; ++t) na += tmd[t] > l_first ? 1 : 0;
 #pragma unroll
       for (int ks = 0; ks < KSG; ++ks) {
-        u16x8 ap[NP][NBA];
+        if (ks > 0) convert_ks(ks);
+        if (ks == KSG - 1) load_a(j + 2, ring_regs);
+        if constexpr (TQ == 1) {
+          mfma_tiles(std::integral_constant<int, 1>{}, ks, sq, ap);
+        } else if constexpr (TQ == 2) {
+          if (na == 1) mfma_tiles(std::integral_constant<int, 1>{}, ks, sq, ap);
+          else mfma_tiles(std::integral_constant<int, 2>{}, ks, sq, ap);
+        } else if constexpr (TQ == 4) {
+          if (na == 1) mfma_tiles(std::integral_constant<int, 1>{}, ks, sq, ap);
+          else if (na == 2) mfma_tiles(std::integral_constant<int, 2>{}, ks, sq, ap);
+          else if (na == 3) mfma_tiles(std::integral_constant<int, 3>{}, ks, sq, ap);
+          else mfma_tiles(std::integral_constant<int, 4>{}, ks, sq, ap);
+        } else {
+          // larger groups: chunks of 4 tiles, each run while its first tile
+          // is active
 #pragma unroll
-        for (int nb = 0; nb < NBA; ++nb) {
-          if constexpr (BF) ap[0][nb] = cur[nb][ks];
-          else split3(cur[nb][ks], ap[0][nb], ap[1][nb], ap[2][nb]);
-        }
+          for (int tc = 0; tc < TQ; tc += 4) {
+            if (tc > 0 && tc >= na) break;
+            u16x8 bq[NP][4];
 #pragma unroll
-        for (int tc = 0; tc < TQ; tc += TC) {
-          if (tc > 0 && tmd[tc] <= l_first) break;
-          u16x8 bq[NP][TC];
+            for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
-          for (int tt = 0; tt < TC; ++tt) {
+              for (int pl = 0; pl < NP; ++pl)
+                bq[pl][tt] = *reinterpret_cast<const u16x8*>(sq + (pl * QG + 16 * (tc + tt) + c) * RB + (32 * ks + 8 * g) * 2);
+            if constexpr (BF) {
 #pragma unroll
-            for (int pl = 0; pl < NP; ++pl)
-              bq[pl][tt] = *reinterpret_cast<const u16x8*>(sq + (pl * QG + 16 * (tc + tt) + c) * RB + (32 * ks + 8 * g) * 2);
-          }
-          if constexpr (BF) {
+              for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
-            for (int tt = 0; tt < TC; ++tt)
+                for (int nb = 0; nb < NBA; ++nb) acc[nb][tc + tt] = mfma_bf16(ap[0][nb][ks], bq[0][tt], acc[nb][tc + tt]);
+            } else {
+              constexpr int TA[6] = {0, 1, 0, 2, 1, 0};
+              constexpr int TB[6] = {2, 1, 1, 0, 0, 0};
 #pragma unroll
-              for (int nb = 0; nb < NBA; ++nb) acc[nb][tc + tt] = mfma_bf16(ap[0][nb], bq[0][tt], acc[nb][tc + tt]);
-          } else {
-            // the six cross terms, smallest first
-            constexpr int TA[6] = {2, 1, 0, 1, 0, 0};
-            constexpr int TB[6] = {0, 1, 2, 0, 1, 0};
+              for (int term = 0; term < 6; ++term)
 #pragma unroll
-            for (int term = 0; term < 6; ++term)
+                for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
-              for (int tt = 0; tt < TC; ++tt)
-#pragma unroll
-                for (int nb = 0; nb < NBA; ++nb)
-                  acc[nb][tc + tt] = mfma_bf16(ap[TA[term]][nb], bq[TB[term]][tt], acc[nb][tc + tt]);
+                  for (int nb = 0; nb < NBA; ++nb)
+                    acc[nb][tc + tt] = mfma_bf16(ap[TA[term]][nb][ks], bq[TB[term]][tt], acc[nb][tc + tt]);
+            }
           }
         }
       }
@@ -535,10 +613,12 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
           const float rq = grq[r];
 #pragma unroll
           for (int nb = 0; nb < NBA; ++nb) {
-            const int y0 = y_wave + 16 * nb + 4 * g;
-            const float* rsp = (p > 0 && y0 < a.n) ? a.rnorm + static_cast<int64_t>(p - 1) * a.rn_stride + y0 : a.rnorm;
+            // blocks past b_end belong to the next workgroup
+            const bool blk_ok = blk_wave + nb < b_end;
+            const int y0 = 16 * (blk_wave + nb) + 4 * g;
+            const float* rsp = (p > 0 && blk_ok && y0 < a.n) ? a.rnorm + static_cast<int64_t>(p - 1) * a.rn_stride + y0 : a.rnorm;
             const floatx4 rs = *reinterpret_cast<const floatx4*>(rsp);
-            if (p == 0) continue;
+            if (p == 0 || !blk_ok) continue;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const int y = y0 + i;
@@ -554,20 +634,20 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
 #pragma unroll
           for (int t = 0; t < TQ; ++t) acc[nb][t] = floatx4{0.f, 0.f, 0.f, 0.f};
       }
+      // map operand of stage j+1 (loads issued during stage j-1)
+      convert(next_regs);
     };
 
-    // two-stage register rotation: stage j computes from ar[j % 2] and then
-    // reloads it with stage j + 2
+    // Two-stage register rotation: stage j computes from the parts of
+    // ar[j % 2], reloads it with the map rows of stage j + 2, and converts
+    // ar[(j + 1) % 2] for stage j + 1.
+    convert(ar0);
     int j = 0;
     for (; j + 2 <= nstages; j += 2) {
-      stage(j, ar0);
-      load_a(j + 2, ar0);
-      load_q(j + 2);
-      stage(j + 1, ar1);
-      load_a(j + 3, ar1);
-      load_q(j + 3);
+      stage(j, ar0, ar1);
+      stage(j + 1, ar1, ar0);
     }
-    if (j < nstages) stage(j, ar0);
+    if (j < nstages) stage(j, ar0, ar1);
     wait_vmcnt<0>();   // drain the trailing loads
     __syncthreads();
   }
@@ -665,13 +745,13 @@ Geo geometry(int E) {
   return g;
 }
 
-// LDS of the scan: 4 ring slots of query planes (8 waves x NI_Q x 1 KB each)
+// LDS of the scan: 3 ring slots of query planes (8 waves x NI_Q x 1 KB each)
 // and the group's sorted query info; the top-K merge buffer reuses the ring.
 size_t scan_lds(bool bf, int TQ, int KSG, int KTOP) {
   const int NP = bf ? 1 : 3;
   const int QG = 16 * TQ;
   const int ni_q = (NP * QG * qrow_bytes(KSG) + 8 * 1024 - 1) / (8 * 1024);
-  size_t ring = static_cast<size_t>(4) * 8 * ni_q * 1024;
+  size_t ring = static_cast<size_t>(3) * 8 * ni_q * 1024;
   const size_t merge = static_cast<size_t>(8) * QG * KTOP * 8;
   if (merge > ring) ring = merge;
   return ring + static_cast<size_t>(3) * QG * 4;
@@ -692,7 +772,7 @@ hipError_t scan_launch(const ScanArgs& a, size_t lds, hipStream_t st) {
 // Largest query-tile count per workgroup whose registers fit without spills
 // (512 threads leave 256 registers per lane).
 constexpr int tq_limit(bool bf, int ksg, int ktop) {
-  return ktop == 1 ? ((bf || ksg == 1) ? 16 : 8) : ktop == 4 ? ((bf || ksg == 1) ? 8 : 2) : ((bf || ksg == 1) ? 4 : 2);
+  return ktop == 1 ? (bf ? 16 : 8) : ktop == 4 ? ((bf || ksg == 1) ? 8 : 2) : ((bf || ksg == 1) ? 4 : 2);
 }
 
 // NBA (16-map blocks per wave) follows from TQ: 2 up to 4 query tiles, else 1.
@@ -775,12 +855,12 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
     const size_t lds = scan_lds(bf, TQ, geo.ksg, KTOP);
     if (lds > kLds) return hipErrorInvalidConfiguration;
 
-    const int slice_maps = 8 * 16 * NBA;
-    const int slices = s.n > 0 ? (s.n + slice_maps - 1) / slice_maps : 0;
-    // workgroups per query group: about one workgroup per CU in total
+    const int n_blocks = (s.n + 15) / 16;
+    // workgroups per query group: about one workgroup per CU in total, each
+    // with an even share of the blocks (at least one)
     int R = 256 / n_qg;
     if (R < 1) R = 1;
-    if (R > slices) R = slices > 0 ? slices : 1;
+    if (R > n_blocks) R = n_blocks > 0 ? n_blocks : 1;
     if (R > kMaxPartials) R = kMaxPartials;
 
     ScanArgs a{};
@@ -798,7 +878,7 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
     a.dmax = max_depth;
     a.n_qg = n_qg;
     a.R = R;
-    a.slices = slices;
+    a.n_blocks = n_blocks;
     a.grid = (n_qg * R + 7) / 8 * 8;
     a.ws = ws;
     a.dbg = dbg_scores != nullptr ? dbg_scores + static_cast<int64_t>(b0) * s.n : nullptr;
