@@ -111,15 +111,16 @@ size_t fm_map_bytes(int32_t cap, int32_t L, int32_t E, fm_dtype map_dtype);
 size_t fm_store_bytes(int32_t cap, int32_t L, int32_t E, int32_t d_emb, fm_dtype map_dtype);
 
 /* Bytes of match workspace for a store of L layers of E experts (map_dtype)
- * and batches of up to B_max queries keeping up to k_max matches each (device
- * memory, 256-byte aligned, owned by the caller).  It holds the staged,
- * depth-sorted query rows, the per-workgroup partial top-k lists, and the
- * top-k slots and completion counter of the semantic scan.  It must be
- * zero-filled once before its first use; every completed match call leaves
- * the slots and the counter zero again.  Calls that share a workspace must be
- * ordered (same stream, or synchronised); concurrent calls on one workspace
- * race.  Returns 0 for invalid arguments. */
-size_t fm_workspace_bytes(int32_t L, int32_t E, fm_dtype map_dtype, int32_t B_max, int32_t k_max);
+ * and d_emb embedding dimensions (0 or a multiple of 128), serving batches of
+ * up to B_max queries keeping up to k_max matches each (device memory,
+ * 256-byte aligned, owned by the caller).  It holds the staged queries of one
+ * launch (depth-sorted trajectory planes, or tiled semantic embeddings), the
+ * query norms and the per-workgroup partial top-k lists.  Every match call
+ * rewrites what it reads, so the contents need no initialisation.  Calls that
+ * share a workspace must be ordered (same stream, or synchronised); concurrent
+ * calls on one workspace race.  Returns 0 for invalid arguments. */
+size_t fm_workspace_bytes(int32_t L, int32_t E, int32_t d_emb, fm_dtype map_dtype, int32_t B_max,
+                          int32_t k_max);
 
 /* Create a host handle over a caller-owned device buffer (Expert Map Store,
  * Section 4.4).  The store starts empty.  The buffer contents are not read;
@@ -134,7 +135,8 @@ fm_status fm_store_build(fm_store** out, const fm_store_desc* desc);
 
 /* Append n iterations (Step 5 of Section 3.2: new expert maps enter the
  * store).  maps: device [n][L][E] of map_dtype, map-major; embs: device
- * [n][d_emb] bf16, required when d_emb > 0 and ignored otherwise.  The maps
+ * [n][d_emb] bf16, 16-byte aligned, required when d_emb > 0 and ignored
+ * otherwise.  The maps
  * are transposed into the layer-major planes, and their prefix norms and the
  * embedding norms are computed.  slots_out: device [n] int32 receiving the store index of each
  * inserted iteration, or NULL.  FM_ERR_FULL if size + n > cap (nothing is
@@ -154,12 +156,12 @@ fm_status fm_store_check(fm_store* store, void* stream, uint32_t* flags_out);
 fm_status fm_store_destroy(fm_store* store);
 
 /* Semantic search, Eq. 4: for each query embedding q[b] (device [B][d_emb]
- * bf16) the k stored iterations with the highest cosine
+ * bf16, 16-byte aligned) the k stored iterations with the highest cosine
  * q[b].x[y] / (|q[b]| |x[y]|) over y < size, accumulated in float32.  A zero
  * norm gives score 0.  Outputs: idx_out device [B][k] int32, score_out device
  * [B][k] float32, in ranking order.  1 <= k <= 8, 1 <= B <= 65536.
- * FM_ERR_INVALID if the store has no embeddings or the workspace is too
- * small. */
+ * FM_ERR_INVALID if the store has no embeddings, q is misaligned or the
+ * workspace is too small. */
 fm_status fm_match_semantic(const fm_store* store, const void* q, int32_t B, int32_t k,
                             int32_t* idx_out, float* score_out,
                             void* workspace, size_t workspace_bytes, void* stream);

@@ -59,21 +59,21 @@ def store_bytes(cap: int, L: int, E: int, d_emb: int = 0, map_dtype: str = "f32"
     return int(_lib.load().fm_store_bytes(cap, L, E, d_emb, _DTYPES[map_dtype]))
 
 
-def workspace_bytes(L: int, E: int, map_dtype: str = "f32", B_max: int = 1024, k_max: int = 8) -> int:
-    return int(_lib.load().fm_workspace_bytes(L, E, _DTYPES[map_dtype], B_max, k_max))
+def workspace_bytes(L: int, E: int, d_emb: int = 0, map_dtype: str = "f32", B_max: int = 1024,
+                    k_max: int = 8) -> int:
+    return int(_lib.load().fm_workspace_bytes(L, E, d_emb, _DTYPES[map_dtype], B_max, k_max))
 
 
 class Workspace:
-    """Device scratch for match calls: zero-filled here, and every completed
-    call leaves it zero-filled.  Calls sharing one workspace must be ordered."""
+    """Device scratch for match calls (every call rewrites what it reads).
+    Calls sharing one workspace must be ordered."""
 
     def __init__(self, store: "Store", B_max: int = 1024, k_max: int = 8, device=None):
-        self.nbytes = workspace_bytes(store.L, store.E, store.map_dtype, B_max, k_max)
+        self.nbytes = workspace_bytes(store.L, store.E, store.d_emb, store.map_dtype, B_max, k_max)
         if self.nbytes == 0:
             raise ValueError(f"invalid workspace request B_max={B_max} k_max={k_max}")
         device = store.device if device is None else device
         self.buf = _aligned_bytes(self.nbytes, device)
-        self.buf.zero_()
 
     @property
     def ptr(self):

@@ -41,7 +41,7 @@ class SelectParams(C.Structure):
 SIGNATURES = {
     "fm_map_bytes": (_sz, [_i32, _i32, _i32, C.c_int]),
     "fm_store_bytes": (_sz, [_i32, _i32, _i32, _i32, C.c_int]),
-    "fm_workspace_bytes": (_sz, [_i32, _i32, C.c_int, _i32, _i32]),
+    "fm_workspace_bytes": (_sz, [_i32, _i32, _i32, C.c_int, _i32, _i32]),
     "fm_store_build": (C.c_int, [C.POINTER(_vp), C.POINTER(StoreDesc)]),
     "fm_store_insert": (C.c_int, [_vp, _vp, _vp, _i32, _vp, _vp]),
     "fm_store_size": (C.c_int, [_vp, C.POINTER(_i32)]),

@@ -55,7 +55,7 @@ bool make_layout(int32_t cap, int32_t L, int32_t E, int32_t d_emb, fm_dtype t, L
   ly.plane_elems = static_cast<int64_t>(ly.plane_bytes / es);
   ly.maps = ly.plane_bytes * L;
   ly.rnorm = fm::align_up(static_cast<size_t>(fm::rnorm_stride(cap)) * L * 4, fm::kAlign);
-  ly.embs = fm::align_up(static_cast<size_t>(cap) * d_emb * 2, fm::kAlign);
+  ly.embs = fm::align_up(static_cast<size_t>(fm::round16(cap)) * d_emb * 2, fm::kAlign);
   ly.norms = d_emb > 0 ? fm::align_up(static_cast<size_t>(cap) * 4, fm::kAlign) : 0;
   ly.flags = fm::kAlign;
   ly.total = ly.maps + ly.rnorm + ly.embs + ly.norms + ly.flags;
@@ -76,37 +76,32 @@ fm_status check_workspace(const fm_store* s, void* ws, size_t bytes) {
   if (ws == nullptr) return fail(FM_ERR_INVALID, "workspace is NULL");
   if (reinterpret_cast<uintptr_t>(ws) % fm::kAlign != 0)
     return fail(FM_ERR_INVALID, "workspace must be %zu-byte aligned", fm::kAlign);
-  const size_t need = fm::workspace_bytes_needed(s->v.L, s->v.E, s->v.map_dtype);
+  const size_t need = fm::workspace_bytes_needed(s->v.L, s->v.E, s->v.d_emb, s->v.map_dtype);
   if (bytes < need) return fail(FM_ERR_INVALID, "workspace of %zu bytes is smaller than the %zu bytes required", bytes, need);
   return FM_OK;
 }
 
-fm::Workspace carve(const fm_store* s, void* ws) { return fm::carve_workspace(ws, s->v.L, s->v.E, s->v.map_dtype); }
+fm::Workspace carve(const fm_store*, void* ws) { return fm::carve_workspace(ws); }
 
 }  // namespace
 
 namespace fm {
 
-// Workspace layout: [keys][counter][partial][perm][sdep][rq][qrows], each
-// part 256-byte aligned.
-size_t workspace_bytes_needed(int32_t L, int32_t E, fm_dtype map_dtype) {
-  size_t b = align_up(sizeof(uint64_t) * kChunkB * kMaxK, kAlign) + kAlign;
-  b += align_up(sizeof(uint64_t) * kChunkB * kMaxPartials * kMaxK, kAlign);
+// Workspace layout: [partial][perm][sdep][rq][qrows], each part 256-byte
+// aligned.  qrows holds the staged queries of one launch: the trajectory
+// planes, or the tiled semantic queries (1024 x d_emb bf16).
+size_t workspace_bytes_needed(int32_t L, int32_t E, int32_t d_emb, fm_dtype map_dtype) {
+  size_t b = align_up(sizeof(uint64_t) * kChunkB * kMaxPartials * kMaxK, kAlign);
   b += 3 * align_up(sizeof(int32_t) * kChunkB, kAlign);
-  b += align_up(traj_qrows_bytes(L, E, map_dtype, kChunkB), kAlign);
+  const size_t traj = traj_qrows_bytes(L, E, map_dtype, kChunkB);
+  const size_t sem = static_cast<size_t>(kChunkB) * d_emb * 2;
+  b += align_up(traj > sem ? traj : sem, kAlign);
   return b;
 }
 
-Workspace carve_workspace(void* base, int32_t L, int32_t E, fm_dtype map_dtype) {
-  (void)L;
-  (void)E;
-  (void)map_dtype;
+Workspace carve_workspace(void* base) {
   char* p = static_cast<char*>(base);
   Workspace w;
-  w.keys = reinterpret_cast<uint64_t*>(p);
-  p += align_up(sizeof(uint64_t) * kChunkB * kMaxK, kAlign);
-  w.counter = reinterpret_cast<uint32_t*>(p);
-  p += kAlign;
   w.partial = reinterpret_cast<uint64_t*>(p);
   p += align_up(sizeof(uint64_t) * kChunkB * kMaxPartials * kMaxK, kAlign);
   w.perm = reinterpret_cast<int32_t*>(p);
@@ -167,10 +162,11 @@ size_t fm_store_bytes(int32_t cap, int32_t L, int32_t E, int32_t d_emb, fm_dtype
   return ly.total;
 }
 
-size_t fm_workspace_bytes(int32_t L, int32_t E, fm_dtype map_dtype, int32_t B_max, int32_t k_max) {
+size_t fm_workspace_bytes(int32_t L, int32_t E, int32_t d_emb, fm_dtype map_dtype, int32_t B_max, int32_t k_max) {
   if (L < 1 || L > fm::kMaxL || E < 1 || E > fm::kMaxE || !valid_dtype(map_dtype)) return 0;
+  if (d_emb < 0 || d_emb % 128 != 0) return 0;
   if (B_max < 1 || k_max < 1 || k_max > fm::kMaxK) return 0;
-  return fm::workspace_bytes_needed(L, E, map_dtype);
+  return fm::workspace_bytes_needed(L, E, d_emb, map_dtype);
 }
 
 fm_status fm_store_build(fm_store** out, const fm_store_desc* d) {
@@ -236,6 +232,8 @@ fm_status fm_store_insert(fm_store* s, const void* maps, const void* embs, int32
   if (n == 0) return ok();
   if (maps == nullptr) return fail(FM_ERR_INVALID, "maps is NULL");
   if (s->v.d_emb > 0 && embs == nullptr) return fail(FM_ERR_INVALID, "store has d_emb=%d but embs is NULL", s->v.d_emb);
+  if (s->v.d_emb > 0 && reinterpret_cast<uintptr_t>(embs) % 16 != 0)
+    return fail(FM_ERR_INVALID, "embs must be 16-byte aligned");
   if (static_cast<int64_t>(s->v.n) + n > s->v.cap)
     return fail(FM_ERR_FULL, "inserting %d into a store holding %d of %d", n, s->v.n, s->v.cap);
   DeviceGuard dg(s->device);
@@ -289,6 +287,7 @@ fm_status fm_match_semantic(const fm_store* s, const void* q, int32_t B, int32_t
                             float* score_out, void* ws, size_t ws_bytes, void* stream) {
   if (fm_status st = check_match_common(s, B, k, idx_out, score_out, ws, ws_bytes)) return st;
   if (q == nullptr) return fail(FM_ERR_INVALID, "q is NULL");
+  if (reinterpret_cast<uintptr_t>(q) % 16 != 0) return fail(FM_ERR_INVALID, "q must be 16-byte aligned");
   if (s->v.d_emb == 0) return fail(FM_ERR_INVALID, "store has no embeddings (d_emb = 0)");
   DeviceGuard dg(s->device);
   if (!dg.ok) return fail(FM_ERR_HIP, "cannot select the store's device %d", s->device);

@@ -10,7 +10,50 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
 
+typedef uint32_t uint32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t uint32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void* lds_vp;
+typedef __attribute__((address_space(1))) void* gbl_vp;
+
 constexpr int kWave = 64;
+
+// Fourth word of a raw buffer descriptor (32-bit data format, no swizzle), and
+// a byte offset beyond every descriptor's range: loads there return zeros
+// without touching memory.
+constexpr int kBufWord3 = 0x00020000;
+constexpr uint32_t kOutside = 0xFFFFF000u;
+
+// Raw s_waitcnt bounding only the vector-memory counter (gfx9 encoding:
+// vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt field is 6 bits");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
+  asm volatile("" ::: "memory");
+}
+__device__ __forceinline__ void wait_lgkm0() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xF | (0x7 << 4) | (0x0 << 8) | (0x3 << 14));
+  asm volatile("" ::: "memory");
+}
+// Workgroup barrier without the implicit release/acquire fence (which would
+// wait for every outstanding global->LDS load); callers wait explicitly.
+__device__ __forceinline__ void raw_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// 16 bytes per lane from src into LDS at lds_base + 16 * lane.
+__device__ __forceinline__ void dma16(const void* src, void* lds_base) {
+  __builtin_amdgcn_global_load_lds((gbl_vp)(const_cast<void*>(src)), (lds_vp)(lds_base), 16, 0, 0);
+}
+
+__device__ __forceinline__ floatx4 mfma_bf16(const u16x8& a, const u16x8& b, floatx4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                 0, 0, 0);
+}
 
 // Score used inside the scans for a NaN cosine: below every real cosine
 // (which lies in [-1, 1] up to rounding) and above the empty sentinel.
@@ -79,24 +122,5 @@ struct TopK {
   }
 };
 
-// Insert a descending list of candidate keys into a global top-k list
-// (k slots, descending, 0 = empty) shared by all workgroups.  Each slot only
-// grows; a displaced key moves on to the next slot.  The final contents are
-// the k largest keys ever offered, whatever the arrival order.
-template <int KTOP>
-__device__ __forceinline__ void global_topk_insert(uint64_t* slots, int k, const uint64_t (&cand)[KTOP]) {
-#pragma unroll
-  for (int c = 0; c < KTOP; ++c) {
-    if (c >= k) return;
-    uint64_t carry = cand[c];
-    if (carry == 0) return;
-    const uint64_t last = __hip_atomic_load(slots + (k - 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (carry <= last) return;  // the list is descending: later candidates are smaller still
-    for (int j = 0; j < k && carry != 0; ++j) {
-      const uint64_t old = __hip_atomic_fetch_max(slots + j, carry, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      carry = old < carry ? old : carry;
-    }
-  }
-}
 
 }  // namespace fm

@@ -29,6 +29,13 @@ inline int64_t round16(int64_t cap) { return (cap + 15) / 16 * 16; }
 __host__ __device__ __forceinline__ int64_t tile_offset(int64_t y, int32_t e, int32_t row) {
   return (y / 16) * 16 * row + (e / 4) * 64 + (y % 16) * 4 + (e % 4);
 }
+// Embeddings (and staged semantic queries) are tiled as MFMA operands: for a
+// block of 16 rows and a k-step of 32 dimensions, a contiguous 1 KB tile holds
+// at 16-byte slot 16g + c the dimensions 32s + 8g .. +7 of row c (the operand
+// of lane 16g + c of v_mfma_f32_16x16x32_bf16).  d is a multiple of 128.
+__host__ __device__ __forceinline__ int64_t emb_offset(int64_t y, int32_t e, int32_t d) {
+  return ((y / 16) * (d / 32) + e / 32) * 512 + (16 * ((e % 32) / 8) + y % 16) * 8 + (e % 8);
+}
 // Stride of the prefix inverse-norm planes: cap rounded up to 64 maps.
 inline int64_t rnorm_stride(int32_t cap) { return (static_cast<int64_t>(cap) + 63) / 64 * 64; }
 
@@ -39,28 +46,27 @@ struct StoreView {
   int64_t plane_elems;   // elements per plane (round16(cap) * row, padded to 256 bytes)
   float* rnorm;          // [L][rn_stride]: 1/|x[y][0:l+1]| (0 for a zero prefix, NaN for NaN)
   int64_t rn_stride;
-  uint16_t* embs;        // [cap][d_emb] bf16
+  uint16_t* embs;        // round16(cap) x d_emb bf16, tiled (emb_offset)
   float* emb_norm;       // [cap]
   uint32_t* flags;       // sticky FM_FLAG_* bits
   int32_t cap, L, E, row, d_emb, n;
   fm_dtype map_dtype;
 };
 
-// Match workspace: the global top-k lists of one launch and its completion
-// counter.  Zero between calls: the last workgroup of every launch clears
-// what the launch used.
+// Match workspace of one launch (every part is fully rewritten by the
+// launch that reads it, so it needs no initialisation).
 struct Workspace {
-  uint64_t* keys;     // [kChunkB][kMaxK] packed (score, index) keys, 0 = empty
-  uint32_t* counter;  // workgroups finished in the current launch
   uint64_t* partial;  // [kChunkB][kMaxPartials][kMaxK] per-workgroup top-k keys
   int32_t* perm;      // [kChunkB] query index at each depth-sorted position (-1: padding)
   int32_t* sdep;      // [kChunkB] clamped depth at each position (0: padding)
   float* rq;          // [kChunkB] 1/|query prefix| at each position
   void* qrows;        // staged query rows of every layer group (trajectory)
 };
-size_t workspace_bytes_needed(int32_t L, int32_t E, fm_dtype map_dtype);
-Workspace carve_workspace(void* base, int32_t L, int32_t E, fm_dtype map_dtype);
+size_t workspace_bytes_needed(int32_t L, int32_t E, int32_t d_emb, fm_dtype map_dtype);
+Workspace carve_workspace(void* base);
 size_t traj_qrows_bytes(int L, int E, fm_dtype dt, int b_pad);
+hipError_t launch_finalize(const uint64_t* partial, const int32_t* perm, int32_t B, int32_t R, int32_t k, int KTOP,
+                           int32_t* idx_out, float* score_out, hipStream_t st);
 
 // Launchers (return hipSuccess or the first HIP error).
 hipError_t launch_insert(const StoreView& s, const void* maps, const void* embs, int32_t n_new,

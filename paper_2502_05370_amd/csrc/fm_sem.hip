@@ -2,19 +2,24 @@
 //
 // The score of query embedding q[b] against stored embedding x[y] is
 // q[b].x[y] / (|q[b]| |x[y]|).  For a batch this is a dense B x n
-// contraction over the hidden size, so it runs on bf16 MFMA
-// (v_mfma_f32_16x16x32_bf16: exact bf16 products, float32 accumulation):
+// contraction over the hidden size on bf16 MFMA
+// (v_mfma_f32_16x16x32_bf16: exact bf16 products, float32 accumulation).
+// Stored embeddings are kept as 1 KB MFMA operand tiles (emb_offset), so every
+// operand load is one contiguous 1 KB read.  A batch of up to 1024 queries is
+// served by three launches:
 //
-//   k_sem_scan  each workgroup owns a 128-map x (16*TQ)-query output tile
-//               and walks the hidden dimension in chunks of 64, staging both
-//               operands in LDS.  Four waves split the tile 2 x 2 (or 4 x 1
-//               for a single query tile).  The epilogue scales by the stored
-//               norms, keeps a per-lane top-K, merges it across the
-//               workgroup and inserts it into the global top-k list; the last
-//               workgroup to finish writes idx/score and clears the list.
-//               Query norms are summed in float64 from the staged chunks.  The
-//               B x n score matrix is never written (except into the optional
-//               debug output).
+//  k_sem_prep   copies the queries into the same tile layout (zero rows pad
+//               the last 16-query tile) and writes 1/|q| (float64 sum).
+//  k_sem_scan   workgroup = a group of 16*TQ queries x an even share of the
+//               store's 16-map blocks, walked as slices of 8 waves x NBA
+//               blocks.  A stage is KS k-steps of one slice: the map tiles of
+//               stage j+2 load into registers (raw buffer loads) and the query
+//               tiles of stage j+2 into an LDS ring slot (direct global->LDS
+//               loads) while stage j computes.  At the end of a slice the
+//               epilogue scales by the stored norms and keeps a per-lane
+//               top-K; the workgroup's merged list is stored as its partial
+//               list per query.
+//  k_finalize   (shared with the trajectory search) merges the partial lists.
 #include "fm_device.h"
 #include "fm_internal.h"
 
@@ -22,290 +27,399 @@ namespace fm {
 
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / kWave;
-constexpr int kTileMaps = 128;   // stored maps per workgroup tile
-constexpr int kChunk = 64;       // hidden elements per LDS stage
-constexpr int kRow = kChunk + 8; // LDS row stride (elements): 144 bytes, conflict-free 16-byte reads
+struct SemPrepArgs {
+  const uint16_t* q;   // [B][d] bf16
+  int32_t B, d, b_pad;
+  uint16_t* qst;       // tiled [b_pad][d]
+  float* rq;           // [b_pad]
+};
 
 struct SemArgs {
-  const uint16_t* x;      // [cap][d]
-  const float* xnorm;     // [cap]
-  const uint16_t* q;      // [B][d]
-  int32_t n, d, B, k;
-  int32_t n_qg, n_units, grid;
+  const uint16_t* x;     // tiled embeddings
+  int64_t x_bytes;       // bytes of the embedding region
+  const float* xnorm;    // [cap] |x|
+  int32_t n, d, B;
+  int32_t n_qg;          // query groups
+  int32_t R;             // workgroups per query group
+  int32_t n_blocks;      // 16-map blocks of the store
+  int32_t grid;
   Workspace ws;
-  int32_t* idx_out;
-  float* score_out;
-  float* dbg;
+  float* dbg;            // optional dense scores [B][n]
 };
 
 }  // namespace
 
-template <int TQ, int WN, int KTOP>
-__global__ void __launch_bounds__(256) k_sem_scan(SemArgs a) {
-  constexpr int QT = 16 * TQ;              // queries per workgroup tile
-  constexpr int WM = kWaves / WN;          // wave rows (maps)
-  constexpr int MBW = kTileMaps / WM / 16; // 16-map blocks per wave
-  constexpr int NBW = TQ / WN;             // 16-query blocks per wave
-  constexpr int XU = kTileMaps * kChunk / 8 / kThreads;  // 16-byte units per thread (maps)
-  constexpr int QU = (QT * kChunk / 8 + kThreads - 1) / kThreads;
-  static_assert(NBW >= 1, "query tiles per wave");
+// One wave per query position: the row is copied 8 dimensions (16 bytes) at a
+// time into its tile slots; positions past B get zero rows.
+__global__ void __launch_bounds__(256) k_sem_prep(SemPrepArgs a) {
+  const int lane = threadIdx.x % kWave;
+  const int pos = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+  if (pos >= a.b_pad) return;
+  double acc = 0.0;
+  for (int j0 = 8 * lane; j0 < a.d; j0 += 8 * kWave) {
+    u16x8 h = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+    if (pos < a.B) {
+      h = *reinterpret_cast<const u16x8*>(a.q + static_cast<int64_t>(pos) * a.d + j0);
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const double v = static_cast<double>(bf16_to_f32(h[t]));
+        acc += v * v;
+      }
+    }
+    *reinterpret_cast<u16x8*>(a.qst + emb_offset(pos, j0, a.d)) = h;
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, kWave);
+  if (lane == 0) {
+    float r;
+    if (acc != acc) r = __uint_as_float(0x7fc00000u);
+    else if (acc == 0.0) r = 0.0f;
+    else r = static_cast<float>(1.0 / sqrt(acc));
+    a.rq[pos] = pos < a.B ? r : 0.0f;
+  }
+}
 
-  __shared__ __align__(16) uint16_t xs[kTileMaps * kRow];
-  __shared__ __align__(16) uint16_t qs[QT * kRow];
-  __shared__ uint64_t mbuf[WM][QT][KTOP];
-  __shared__ float grq[QT];
-  __shared__ int32_t s_last;
+// 8 waves; wave w owns NBA blocks of 16 maps of every slice.  Stage j =
+// (slice j / NKC, k-steps KS * (j % NKC) ..).  During stage j every wave loads
+// its share of the query tiles of stage j+2 into LDS slot (j+2) % 3 and, after
+// its MFMAs, the map tiles of stage j+2 into the registers stage j used.  Every
+// wave issues the same loads per stage (out-of-range offsets and a repeated
+// query tile keep the count fixed), so "stage j+1 has landed" is vmcnt <= the
+// loads of one stage at the end of stage j.  Slot (j+2) % 3 was last read in
+// stage j-1, which every wave finished before the barrier of stage j.
+template <int TQ, int KTOP, bool DBG>
+__global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
+  constexpr int W = 8;                        // waves per workgroup
+  constexpr int NBA = 2;                      // 16-map blocks per wave and slice
+  constexpr int KS = 2;                       // k-steps (32 dimensions each) per stage
+  constexpr int NS = 3;                       // query ring slots
+  constexpr int QG = 16 * TQ;                 // queries per group
+  constexpr int NQ = TQ * KS;                 // 1 KB query tiles per stage
+  constexpr int NI_Q = (NQ + W - 1) / W;      // query tile loads per wave and stage
+  constexpr int Q_STAGE = NQ * 1024;
+  constexpr int NI_A = NBA * KS + NBA;        // map tile and map norm loads per wave and stage
+  constexpr int NI = NI_A + NI_Q;
+  static_assert(NI < 64, "vmcnt field is 6 bits");
+
+  extern __shared__ __align__(16) unsigned char smem[];
+  unsigned char* ring = smem;                                      // [NS][Q_STAGE]
+  float* grq = reinterpret_cast<float*>(smem + NS * Q_STAGE);      // [QG]
+  uint64_t* mbuf = reinterpret_cast<uint64_t*>(smem);              // after the loop: [W][QG][KTOP]
 
   const int tid = threadIdx.x;
   const int w = tid / kWave;
   const int lane = tid % kWave;
   const int g = lane / 16;
   const int c = lane % 16;
-  const int wm = w / WN;
-  const int wn = w % WN;
 
+  // workgroup -> (query group, block range); the n_qg workgroups sharing a
+  // block range are consecutive, hence on one XCD, and read the same map
+  // tiles at about the same time (the later reads hit that XCD's L2)
   const int bid = blockIdx.x;
   const int u = (bid % 8) * (a.grid / 8) + bid / 8;
-  const bool active = u < a.n_units;
-  const int tile = active ? u / a.n_qg : 0;
+  const bool active = u < a.n_qg * a.R;
   const int qgrp = active ? u % a.n_qg : 0;
-  const int y0 = tile * kTileMaps;
-  const int b0 = qgrp * QT;
+  const int rr = active ? u / a.n_qg : 0;
+  const int b_begin = active ? static_cast<int>((static_cast<int64_t>(rr) * a.n_blocks) / a.R) : 0;
+  const int b_end = active ? static_cast<int>((static_cast<int64_t>(rr + 1) * a.n_blocks) / a.R) : 0;
+  const int n_slices = (b_end - b_begin + W * NBA - 1) / (W * NBA);
+  const int g0 = qgrp * QG;
+  const int ksteps = a.d / 32;
+  const int NKC = ksteps / KS;
+  const int nstages = n_slices * NKC;
 
-  for (int r = tid; r < QT; r += kThreads) grq[r] = 0.0f;
+  for (int r = tid; r < QG; r += W * kWave) grq[r] = a.ws.rq[g0 + r];
+  __syncthreads();
 
-  TopK<KTOP> best[NBW];
+  TopK<KTOP> best[TQ];
 #pragma unroll
-  for (int nb = 0; nb < NBW; ++nb) best[nb].clear();
+  for (int t = 0; t < TQ; ++t) best[t].clear();
 
-  if (active) {
-    floatx4 acc[MBW][NBW];
-#pragma unroll
-    for (int mb = 0; mb < MBW; ++mb)
-#pragma unroll
-      for (int nb = 0; nb < NBW; ++nb) acc[mb][nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+  if (active && nstages > 0) {
+    const char* xb = reinterpret_cast<const char*>(a.x);
+    const char* qst = static_cast<const char*>(a.ws.qrows);
+    const int64_t blk_bytes = static_cast<int64_t>(ksteps) * 1024;   // one 16-row block, all k-steps
 
-    // Register prefetch of one chunk of both operands.
-    u16x8 xr[XU];
-    u16x8 qr[QU];
-    double qn2[QU];
+    // Map tiles: descriptor based at the slice's first block; rows past the
+    // store and blocks past the range read as zeros.  The first stage of a
+    // slice also loads the slice's map norms (lane group g: maps 4g .. 4g+3
+    // of each block); the other stages issue the same loads out of range.
+    const __amdgpu_buffer_rsrc_t rs_norm = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(a.xnorm), static_cast<short>(0), static_cast<int>(static_cast<uint32_t>(a.n) * 4u), kBufWord3);
+    auto load_a = [&](int j, u16x8 (&dst)[NBA][KS], floatx4 (&dxn)[NBA]) {
+      const bool real = j < nstages;
+      const int si = real ? j / NKC : 0;
+      const int kc = real ? j % NKC : 0;
+      const int blk0 = b_begin + si * (W * NBA);
+      const int64_t base = static_cast<int64_t>(blk0) * blk_bytes;
+      int64_t rem = a.x_bytes - base;
+      if (rem > static_cast<int64_t>(kOutside)) rem = kOutside;
+      if (rem < 0) rem = 0;
+      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<char*>(xb + base), static_cast<short>(0), static_cast<int>(static_cast<uint32_t>(rem)), kBufWord3);
 #pragma unroll
-    for (int i = 0; i < QU; ++i) qn2[i] = 0.0;
-    auto load_chunk = [&](int kc) {
+      for (int nb = 0; nb < NBA; ++nb) {
+        const int blk = blk0 + w * NBA + nb;
+        const bool ok = real && blk < b_end && 16 * blk + c < a.n;
+        const uint32_t base_off = static_cast<uint32_t>(((w * NBA + nb) * ksteps + kc * KS) * 1024 + lane * 16);
 #pragma unroll
-      for (int i = 0; i < XU; ++i) {
-        int unit = tid + i * kThreads;
-        int row = unit / (kChunk / 8);
-        int part = unit % (kChunk / 8);
-        int y = y0 + row;
-        u16x8 v = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-        if (y < a.n) v = *reinterpret_cast<const u16x8*>(a.x + static_cast<int64_t>(y) * a.d + kc + part * 8);
-        xr[i] = v;
-      }
-#pragma unroll
-      for (int i = 0; i < QU; ++i) {
-        int unit = tid + i * kThreads;
-        int row = unit / (kChunk / 8);
-        int part = unit % (kChunk / 8);
-        int b = b0 + row;
-        u16x8 v = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-        if (row < QT && b < a.B) v = *reinterpret_cast<const u16x8*>(a.q + static_cast<int64_t>(b) * a.d + kc + part * 8);
-        qr[i] = v;
+        for (int ks = 0; ks < KS; ++ks) {
+          const uint32_t off = ok ? base_off + static_cast<uint32_t>(ks * 1024) : kOutside;
+          dst[nb][ks] = __builtin_bit_cast(u16x8, __builtin_amdgcn_raw_buffer_load_b128(rs, static_cast<int>(off), 0, 0));
+        }
+        const uint32_t noff = (real && kc == 0 && blk < b_end) ? static_cast<uint32_t>((16 * blk + 4 * g) * 4) : kOutside;
+        dxn[nb] = __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(rs_norm, static_cast<int>(noff), 0, 0));
       }
     };
-    auto store_chunk = [&]() {
+    // Query tiles of stage j: tile (t, ks) is 1 KB at slot offset (t*KS+ks) KB;
+    // wave w loads tiles w, w+8, ... (wrapping: a repeated tile rewrites
+    // identical bytes).
+    auto load_q = [&](int j) {
+      const bool real = j < nstages;
+      const int kc = real ? j % NKC : 0;
+      unsigned char* st = ring + (j % NS) * Q_STAGE;
 #pragma unroll
-      for (int i = 0; i < XU; ++i) {
-        int unit = tid + i * kThreads;
-        int row = unit / (kChunk / 8);
-        int part = unit % (kChunk / 8);
-        *reinterpret_cast<u16x8*>(xs + row * kRow + part * 8) = xr[i];
+      for (int i = 0; i < NI_Q; ++i) {
+        const int tile = (w + W * i) % NQ;
+        const int t = tile / KS;
+        const int ks = tile - t * KS;
+        const char* src = qst + ((static_cast<int64_t>(g0 / 16 + t) * ksteps + kc * KS + ks) * 1024) + lane * 16;
+        dma16(src, st + tile * 1024);
       }
+    };
+
+    floatx4 acc[NBA][TQ];
 #pragma unroll
-      for (int i = 0; i < QU; ++i) {
-        int unit = tid + i * kThreads;
-        int row = unit / (kChunk / 8);
-        int part = unit % (kChunk / 8);
-        if (row < QT) *reinterpret_cast<u16x8*>(qs + row * kRow + part * 8) = qr[i];
+    for (int nb = 0; nb < NBA; ++nb)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const double f = static_cast<double>(bf16_to_f32(qr[i][j]));
-          qn2[i] += f * f;
+      for (int t = 0; t < TQ; ++t) acc[nb][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    // issue order: Q0 A0 Q1 A1, then during stage j: Q(j+2) A(j+2)
+    u16x8 ar0[NBA][KS], ar1[NBA][KS];
+    floatx4 xr0[NBA], xr1[NBA];
+    load_q(0);
+    load_a(0, ar0, xr0);
+    load_q(1);
+    load_a(1, ar1, xr1);
+
+    // The map registers of a stage pass through an empty asm placed after
+    // the wait for them, so no use of them is scheduled above it (the
+    // compiler would then wait for every outstanding load itself, emptying
+    // the prefetch).
+    u16x8 cur[NBA][KS];
+    floatx4 xn_slice[NBA];
+    auto take = [&](int j, u16x8 (&ring_regs)[NBA][KS], floatx4 (&ring_xn)[NBA]) {
+      wait_vmcnt<NI>();
+#pragma unroll
+      for (int nb = 0; nb < NBA; ++nb) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          cur[nb][ks] = ring_regs[nb][ks];
+          asm volatile("" : "+v"(cur[nb][ks]));
+        }
+        if (j % NKC == 0) {
+          xn_slice[nb] = ring_xn[nb];
+          asm volatile("" : "+v"(xn_slice[nb]));
         }
       }
     };
 
-    load_chunk(0);
-    for (int kc = 0; kc < a.d; kc += kChunk) {
-      store_chunk();
-      __syncthreads();
-      if (kc + kChunk < a.d) load_chunk(kc + kChunk);
-#pragma unroll
-      for (int kk = 0; kk < kChunk / 32; ++kk) {
-        u16x8 af[MBW];
-#pragma unroll
-        for (int mb = 0; mb < MBW; ++mb)
-          af[mb] = *reinterpret_cast<const u16x8*>(xs + ((wm * MBW + mb) * 16 + c) * kRow + 32 * kk + 8 * g);
-#pragma unroll
-        for (int nb = 0; nb < NBW; ++nb) {
-          u16x8 bf = *reinterpret_cast<const u16x8*>(qs + ((wn * NBW + nb) * 16 + c) * kRow + 32 * kk + 8 * g);
-#pragma unroll
-          for (int mb = 0; mb < MBW; ++mb)
-            acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8, af[mb]), __builtin_bit_cast(bf16x8, bf), acc[mb][nb], 0, 0, 0);
-        }
-      }
-      __syncthreads();
-    }
+    auto stage = [&](int j, u16x8 (&ring_regs)[NBA][KS], floatx4 (&ring_xn)[NBA], u16x8 (&next_regs)[NBA][KS],
+                     floatx4 (&next_xn)[NBA]) {
+      const int si = j / NKC;
+      const int kc = j % NKC;
+      const int blk_wave = b_begin + si * (W * NBA) + w * NBA;
+      const unsigned char* sq = ring + (j % NS) * Q_STAGE;
 
-    // query norms: the 8 parts of a row sit in 8 consecutive lanes (fixed order)
+      raw_barrier();
+      load_q(j + 2);
 #pragma unroll
-    for (int i = 0; i < QU; ++i) {
-      double v = qn2[i];
-      v += __shfl_xor(v, 1, kWave);
-      v += __shfl_xor(v, 2, kWave);
-      v += __shfl_xor(v, 4, kWave);
-      const int unit = tid + i * kThreads;
-      const int row = unit / (kChunk / 8);
-      if (row < QT && unit % (kChunk / 8) == 0) {
-        float r;
-        if (v != v) r = __uint_as_float(0x7fc00000u);
-        else if (v == 0.0) r = 0.0f;
-        else r = static_cast<float>(1.0 / sqrt(v));
-        grq[row] = r;
+      for (int ks = 0; ks < KS; ++ks) {
+        u16x8 bq[TQ];
+#pragma unroll
+        for (int t = 0; t < TQ; ++t) bq[t] = *reinterpret_cast<const u16x8*>(sq + (t * KS + ks) * 1024 + lane * 16);
+#pragma unroll
+        for (int t = 0; t < TQ; ++t)
+#pragma unroll
+          for (int nb = 0; nb < NBA; ++nb) acc[nb][t] = mfma_bf16(cur[nb][ks], bq[t], acc[nb][t]);
       }
+      load_a(j + 2, ring_regs, ring_xn);
+
+      if (kc == NKC - 1) {
+        // End of a slice: cosine = dot * 1/|q| * 1/|x|; lane (g, c) holds maps
+        // 16nb + 4g + i (i = 0..3) of query column c of each tile.
+#pragma unroll
+        for (int nb = 0; nb < NBA; ++nb) {
+          const bool blk_ok = blk_wave + nb < b_end;
+          const int y0 = 16 * (blk_wave + nb) + 4 * g;
+          const floatx4 xn = xn_slice[nb];
+          if (!blk_ok) continue;
+#pragma unroll
+          for (int t = 0; t < TQ; ++t) {
+            const int r = 16 * t + c;
+            const int b = g0 + r;
+            if (b >= a.B) continue;
+            const float rq = grq[r];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int y = y0 + i;
+              if (y >= a.n) continue;
+              const float rx = xn[i] > 0.0f ? 1.0f / xn[i] : (xn[i] != xn[i] ? xn[i] : 0.0f);
+              const float s = acc[nb][t][i] * rq * rx;
+              if constexpr (DBG) a.dbg[static_cast<int64_t>(b) * a.n + y] = s;
+              best[t].push(make_key(s, y));
+            }
+          }
+        }
+#pragma unroll
+        for (int nb = 0; nb < NBA; ++nb)
+#pragma unroll
+          for (int t = 0; t < TQ; ++t) acc[nb][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+      }
+      take(j + 1, next_regs, next_xn);
+    };
+
+    take(0, ar0, xr0);
+    int j = 0;
+    for (; j + 2 <= nstages; j += 2) {
+      stage(j, ar0, xr0, ar1, xr1);
+      stage(j + 1, ar1, xr1, ar0, xr0);
     }
+    if (j < nstages) stage(j, ar0, xr0, ar1, xr1);
+    wait_vmcnt<0>();   // drain the trailing loads
     __syncthreads();
-
-    // Epilogue: lane (g, c) holds maps 4g+i of each 16-map block for query c of each query block.
-#pragma unroll
-    for (int nb = 0; nb < NBW; ++nb) {
-      const int r = (wn * NBW + nb) * 16 + c;
-      const int b = b0 + r;
-      if (b >= a.B) continue;
-      const float rq = grq[r];
-#pragma unroll
-      for (int mb = 0; mb < MBW; ++mb) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int y = y0 + (wm * MBW + mb) * 16 + 4 * g + i;
-          if (y >= a.n) continue;
-          const float xn = a.xnorm[y];
-          const float rx = xn > 0.0f ? 1.0f / xn : (xn != xn ? xn : 0.0f);
-          const float s = acc[mb][nb][i] * rq * rx;
-          if (a.dbg != nullptr) a.dbg[static_cast<int64_t>(b) * a.n + y] = s;
-          best[nb].push(make_key(s, y));
-        }
-      }
-    }
   }
 
+  // merge the per-lane lists across the 4 lane groups, then across waves
 #pragma unroll
-  for (int nb = 0; nb < NBW; ++nb) {
+  for (int t = 0; t < TQ; ++t) {
 #pragma unroll
     for (int m = 16; m <= 32; m <<= 1) {
       uint64_t o[KTOP];
 #pragma unroll
-      for (int j = 0; j < KTOP; ++j) o[j] = shfl_xor_u64(best[nb].v[j], m);
-      best[nb].merge(o);
+      for (int jj = 0; jj < KTOP; ++jj) o[jj] = shfl_xor_u64(best[t].v[jj], m);
+      best[t].merge(o);
     }
-    if (g == 0) {
+  }
+  __syncthreads();
+  if (g == 0) {
 #pragma unroll
-      for (int j = 0; j < KTOP; ++j) mbuf[wm][(wn * NBW + nb) * 16 + c][j] = best[nb].v[j];
-    }
-  }
-  __syncthreads();
-  for (int r = tid; r < QT; r += kThreads) {
-    if (!active || b0 + r >= a.B) continue;
-    TopK<KTOP> m;
-    m.clear();
+    for (int t = 0; t < TQ; ++t) {
 #pragma unroll
-    for (int ww = 0; ww < WM; ++ww) m.merge(&mbuf[ww][r][0]);
-    global_topk_insert<KTOP>(a.ws.keys + static_cast<int64_t>(b0 + r) * kMaxK, a.k, m.v);
-  }
-
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) {
-    uint32_t ticket = __hip_atomic_fetch_add(a.ws.counter, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    s_last = (ticket == static_cast<uint32_t>(a.grid - 1)) ? 1 : 0;
-  }
-  __syncthreads();
-  if (s_last) {
-    __threadfence();
-    for (int i = tid; i < a.B * a.k; i += kThreads) {
-      const int b = i / a.k;
-      const int j = i - b * a.k;
-      uint64_t* slot = a.ws.keys + static_cast<int64_t>(b) * kMaxK + j;
-      const uint64_t key = __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (a.idx_out != nullptr) {
-        a.idx_out[i] = key_index(key);
-        a.score_out[i] = key_score(key);
-      }
-      __hip_atomic_store(slot, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      for (int jj = 0; jj < KTOP; ++jj) mbuf[(w * QG + 16 * t + c) * KTOP + jj] = best[t].v[jj];
     }
-    if (tid == 0) __hip_atomic_store(a.ws.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  if (active) {
+    for (int r = tid; r < QG; r += W * kWave) {
+      TopK<KTOP> m;
+      m.clear();
+#pragma unroll
+      for (int ww = 0; ww < W; ++ww) m.merge(mbuf + (ww * QG + r) * KTOP);
+      uint64_t* out = a.ws.partial + (static_cast<int64_t>(g0 + r) * a.R + rr) * KTOP;
+#pragma unroll
+      for (int jj = 0; jj < KTOP; ++jj) out[jj] = m.v[jj];
+    }
   }
 }
 
-template <int TQ, int WN, int KTOP>
-static hipError_t sem_launch(const SemArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL((k_sem_scan<TQ, WN, KTOP>), dim3(a.grid), dim3(kThreads), 0, st, a);
+namespace {
+
+// Largest query-tile count per workgroup for each list size (registers).
+constexpr int sem_tq_limit(int ktop) { return ktop == 8 ? 4 : 8; }
+
+// LDS: three query ring slots and the query norms; the merge buffer reuses
+// the ring.
+size_t sem_lds(int TQ, int KTOP) {
+  size_t ring = static_cast<size_t>(3) * TQ * 2 * 1024;
+  const size_t merge = static_cast<size_t>(8) * 16 * TQ * KTOP * 8;
+  if (merge > ring) ring = merge;
+  return ring + static_cast<size_t>(16) * TQ * 4;
+}
+
+template <int TQ, int KTOP, bool DBG = false>
+hipError_t sem_launch(const SemArgs& a, hipStream_t st) {
+  const size_t lds = sem_lds(TQ, KTOP);
+  auto kern = k_sem_scan<TQ, KTOP, DBG>;
+  if (lds > 64 * 1024) {
+    const hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+    if (err != hipSuccess) return err;
+  }
+  hipLaunchKernelGGL(kern, dim3(a.grid), dim3(512), lds, st, a);
   return hipGetLastError();
 }
+
+template <int KTOP>
+hipError_t sem_tq(int TQ, const SemArgs& a, hipStream_t st) {
+  switch (TQ) {
+    case 1: return sem_launch<1, KTOP>(a, st);
+    case 2: return sem_launch<2, KTOP>(a, st);
+    case 4: return sem_launch<4, KTOP>(a, st);
+    case 8:
+      if constexpr (sem_tq_limit(KTOP) >= 8) return sem_launch<8, KTOP>(a, st);
+      break;
+    default: break;
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
 
 hipError_t launch_match_semantic(const StoreView& s, const void* q, int32_t B, int32_t k, int32_t* idx_out,
                                  float* score_out, float* dbg_scores, const Workspace& ws, hipStream_t st) {
   const int KTOP = k == 1 ? 1 : (k <= 4 ? 4 : 8);
-  const int tq_max = KTOP == 1 ? 16 : (KTOP == 4 ? 8 : 4);
+  const int tq_max = dbg_scores != nullptr ? 1 : sem_tq_limit(KTOP);
+  const int n_blocks = (s.n + 15) / 16;
   for (int b0 = 0; b0 < B; b0 += kChunkB) {
     const int Bc = (B - b0) < kChunkB ? (B - b0) : kChunkB;
-    const uint16_t* qc = static_cast<const uint16_t*>(q) + static_cast<int64_t>(b0) * s.d_emb;
-    hipError_t err = hipSuccess;
     int TQ = 1;
     while (16 * TQ < Bc && TQ < tq_max) TQ *= 2;
-    const int n_qg = (Bc + 16 * TQ - 1) / (16 * TQ);
-    const int tiles = s.n > 0 ? (s.n + kTileMaps - 1) / kTileMaps : 0;
+    const int QG = 16 * TQ;
+    const int n_qg = (Bc + QG - 1) / QG;
+    const int b_pad = n_qg * QG;
+
+    SemPrepArgs pa;
+    pa.q = static_cast<const uint16_t*>(q) + static_cast<int64_t>(b0) * s.d_emb;
+    pa.B = Bc;
+    pa.d = s.d_emb;
+    pa.b_pad = b_pad;
+    pa.qst = static_cast<uint16_t*>(ws.qrows);
+    pa.rq = ws.rq;
+    hipLaunchKernelGGL(k_sem_prep, dim3((b_pad + 3) / 4), dim3(256), 0, st, pa);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+
+    // workgroups per query group: about one workgroup per CU in total, each
+    // with an even share of the blocks (at least one)
+    int R = 256 / n_qg;
+    if (R < 1) R = 1;
+    if (R > n_blocks) R = n_blocks > 0 ? n_blocks : 1;
+    if (R > kMaxPartials) R = kMaxPartials;
+
     SemArgs a;
     a.x = s.embs;
+    a.x_bytes = round16(s.cap) * static_cast<int64_t>(s.d_emb) * 2;
     a.xnorm = s.emb_norm;
-    a.q = qc;
     a.n = s.n;
     a.d = s.d_emb;
     a.B = Bc;
-    a.k = k;
     a.n_qg = n_qg;
-    a.n_units = tiles * n_qg;
-    a.grid = ((a.n_units > 0 ? a.n_units : 1) + 7) / 8 * 8;
+    a.R = R;
+    a.n_blocks = n_blocks;
+    a.grid = (n_qg * R + 7) / 8 * 8;
     a.ws = ws;
-    a.idx_out = idx_out != nullptr ? idx_out + static_cast<int64_t>(b0) * k : nullptr;
-    a.score_out = score_out != nullptr ? score_out + static_cast<int64_t>(b0) * k : nullptr;
     a.dbg = dbg_scores != nullptr ? dbg_scores + static_cast<int64_t>(b0) * s.n : nullptr;
-    if (KTOP == 1) {
-      switch (TQ) {
-        case 1: err = sem_launch<1, 1, 1>(a, st); break;
-        case 2: err = sem_launch<2, 2, 1>(a, st); break;
-        case 4: err = sem_launch<4, 2, 1>(a, st); break;
-        case 8: err = sem_launch<8, 2, 1>(a, st); break;
-        default: err = sem_launch<16, 2, 1>(a, st); break;
-      }
-    } else if (KTOP == 4) {
-      switch (TQ) {
-        case 1: err = sem_launch<1, 1, 4>(a, st); break;
-        case 2: err = sem_launch<2, 2, 4>(a, st); break;
-        case 4: err = sem_launch<4, 2, 4>(a, st); break;
-        default: err = sem_launch<8, 2, 4>(a, st); break;
-      }
-    } else {
-      switch (TQ) {
-        case 1: err = sem_launch<1, 1, 8>(a, st); break;
-        case 2: err = sem_launch<2, 2, 8>(a, st); break;
-        default: err = sem_launch<4, 2, 8>(a, st); break;
-      }
-    }
+    if (dbg_scores != nullptr) err = sem_launch<1, 1, true>(a, st);
+    else if (KTOP == 1) err = sem_tq<1>(TQ, a, st);
+    else if (KTOP == 4) err = sem_tq<4>(TQ, a, st);
+    else err = sem_tq<8>(TQ, a, st);
     if (err != hipSuccess) return err;
+    if (idx_out != nullptr) {
+      err = launch_finalize(ws.partial, nullptr, Bc, R, k, KTOP, idx_out + static_cast<int64_t>(b0) * k,
+                            score_out + static_cast<int64_t>(b0) * k, st);
+      if (err != hipSuccess) return err;
+    }
   }
   return hipSuccess;
 }

@@ -52,7 +52,9 @@ __global__ void __launch_bounds__(256) k_insert_maps(const T* __restrict__ src, 
   if (slots_out != nullptr && lane == 0) slots_out[i] = static_cast<int32_t>(y);
 }
 
-// One wavefront per embedding row: copy it and compute its norm.
+// One wavefront per embedding row: copy it into the tiled layout
+// (emb_offset, 8 consecutive dimensions per 16-byte store) and compute its
+// norm.
 __global__ void __launch_bounds__(256) k_insert_embs(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst,
                                                      float* __restrict__ norms, int32_t first_slot, int32_t n_new,
                                                      int32_t d) {
@@ -60,13 +62,16 @@ __global__ void __launch_bounds__(256) k_insert_embs(const uint16_t* __restrict_
   const int row = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
   if (row >= n_new) return;
   const uint16_t* s = src + static_cast<int64_t>(row) * d;
-  uint16_t* o = dst + static_cast<int64_t>(first_slot + row) * d;
+  const int64_t y = static_cast<int64_t>(first_slot) + row;
   double acc = 0.0;
-  for (int j = lane; j < d; j += kWave) {
-    uint16_t h = s[j];
-    o[j] = h;
-    double v = static_cast<double>(bf16_to_f32(h));
-    acc += v * v;
+  for (int j0 = 8 * lane; j0 < d; j0 += 8 * kWave) {
+    const u16x8 h = *reinterpret_cast<const u16x8*>(s + j0);
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const double v = static_cast<double>(bf16_to_f32(h[t]));
+      acc += v * v;
+    }
+    *reinterpret_cast<u16x8*>(dst + emb_offset(y, j0, d)) = h;
   }
   // Fixed-order tree reduction across the wave.
 #pragma unroll

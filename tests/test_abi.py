@@ -51,13 +51,16 @@ def test_store_footprint_matches_section_6_8():
 
 def test_workspace_size():
     L, lib = _lib()
-    big = lib.fm_workspace_bytes(24, 60, L.FM_F32, 1024, 8)
+    big = lib.fm_workspace_bytes(24, 60, 0, L.FM_F32, 1024, 8)
     assert big > 1024 * 8 * 8
-    assert lib.fm_workspace_bytes(24, 60, L.FM_BF16, 1024, 8) < big
-    assert lib.fm_workspace_bytes(24, 60, L.FM_F32, 0, 1) == 0
-    assert lib.fm_workspace_bytes(24, 60, L.FM_F32, 16, 9) == 0
-    assert lib.fm_workspace_bytes(65, 60, L.FM_F32, 16, 1) == 0
-    assert lib.fm_workspace_bytes(24, 65, L.FM_F32, 16, 1) == 0
+    assert lib.fm_workspace_bytes(24, 60, 0, L.FM_BF16, 1024, 8) < big
+    assert lib.fm_workspace_bytes(24, 60, 0, L.FM_F32, 0, 1) == 0
+    assert lib.fm_workspace_bytes(24, 60, 0, L.FM_F32, 16, 9) == 0
+    assert lib.fm_workspace_bytes(65, 60, 0, L.FM_F32, 16, 1) == 0
+    assert lib.fm_workspace_bytes(24, 65, 0, L.FM_F32, 16, 1) == 0
+    # semantic staging: 1024 tiled queries of d_emb bf16
+    assert lib.fm_workspace_bytes(32, 8, 4096, L.FM_F32, 1024, 8) >= 1024 * 4096 * 2
+    assert lib.fm_workspace_bytes(32, 8, 100, L.FM_F32, 1024, 8) == 0
 
 
 def _build(lib, L, cap=16, Lr=4, E=8, d=0, dtype=0, buf=0x1000, nbytes=1 << 20):
