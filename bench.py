@@ -9,9 +9,12 @@ Default workload: the Qwen1.5-MoE-shaped trajectory batch (50,000 stored maps
 of 24 x 60 float32, 64 queries with prefix depths U{1..23}, top-1, threshold
 0.8, at most 8 experts).  ``--config`` selects another workload.
 
-Prints ONE JSON line.  ``roofline`` refers to the match call (the dominant
-kernel) timed with HIP events on the stream it runs on; ``cpu_baseline`` is the
-CPU oracle timed on a bounded sample of the same batch.
+Prints ONE JSON line.  ``roofline`` refers to the dominant kernel (the scan
+kernel of the match call; for the mixed workload the slower of the two scans),
+timed by HIP events that the library records right around its launch on the
+stream it runs on (fm_debug_scan_events); ``match_call_us`` is the whole match
+call (staging, scan, merge).  ``cpu_baseline`` is the CPU oracle timed on a
+bounded sample of the same batch.
 """
 from __future__ import annotations
 
@@ -30,10 +33,68 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_MFMA_PEAK_TFS = 2500.0    # dense bf16 MFMA
 FP32_MFMA_PEAK_TFS = 157.3     # dense fp32 MFMA
 
-# Measured HBM traffic of the dominant kernel (rocprofv3 FETCH_SIZE + WRITE_SIZE,
-# scaled by a plain copy kernel's counter reading), per launch, by workload.
-# None until counters are taken for the kernel as it stands.
-COUNTER_TRAFFIC_BYTES = {}
+# HBM traffic of the dominant kernel per launch, from two rocprofv3 --pmc runs
+# (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch) of this bench, each scaled by
+# what the same counter reads for a plain copy kernel of 256 MiB
+# (profiles/traffic_counters.md).  Only for kernels unchanged since.
+COPY_BYTES_KIB = 262144.0
+COPY_COUNTERS_KIB = {"FETCH_SIZE": 131083.5, "WRITE_SIZE": 262144.0}
+COUNTERS_KIB = {
+    # workload: (kernel, FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch
+    "qwen_traj_n50k_b64": ("k_traj_scan", 139763.75, 128.0),
+}
+
+
+def counter_traffic(workload):
+    if workload not in COUNTERS_KIB:
+        return None
+    _, fetch, write = COUNTERS_KIB[workload]
+    kib = (fetch * COPY_BYTES_KIB / COPY_COUNTERS_KIB["FETCH_SIZE"]
+           + write * COPY_BYTES_KIB / COPY_COUNTERS_KIB["WRITE_SIZE"])
+    return kib * 1024.0
+
+
+def hip_runtime():
+    """The HIP runtime this process already uses (torch's), for raw events."""
+    import ctypes
+    import re
+    paths = sorted(set(re.findall(r"(/\S*libamdhip64\.so\S*)", open("/proc/self/maps").read())))
+    if not paths:
+        raise RuntimeError("the HIP runtime is not loaded")
+    hip = ctypes.CDLL(paths[0])
+    hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+    hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+    hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+    return hip
+
+
+class ScanTimer:
+    """HIP event pairs that the library records around its scan kernel launch
+    (fm_debug_scan_events), one pair per timed call."""
+
+    def __init__(self, hip, lib, n):
+        import ctypes
+        self.hip, self.lib, self.C = hip, lib, ctypes
+        self.pairs = []
+        for _ in range(n):
+            a, b = ctypes.c_void_p(), ctypes.c_void_p()
+            assert hip.hipEventCreate(ctypes.byref(a)) == 0 and hip.hipEventCreate(ctypes.byref(b)) == 0
+            self.pairs.append((a, b))
+
+    def arm(self, i):
+        a, b = self.pairs[i]
+        assert self.lib.fm_debug_scan_events(a, b) == 0
+
+    def disarm(self):
+        assert self.lib.fm_debug_scan_events(None, None) == 0
+
+    def mean_ms(self, n):
+        vals = []
+        for a, b in self.pairs[:n]:
+            ms = self.C.c_float()
+            assert self.hip.hipEventElapsedTime(self.C.byref(ms), a, b) == 0
+            vals.append(ms.value)
+        return float(np.mean(vals))
 
 
 def parse():
@@ -44,7 +105,8 @@ def parse():
     p.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--graph", action="store_true", help="replay the step as a captured HIP graph")
+    p.add_argument("--copy-probe", action="store_true",
+                   help="only copy 256 MiB device-to-device three times (reference for HBM traffic counters)")
     return p.parse_args()
 
 
@@ -104,6 +166,14 @@ def main():
         sys.exit(2)
 
     import torch
+    if args.copy_probe:
+        src = torch.ones(64 << 20, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": src.numel() * 4, "launches": 3}))
+        return
     import synth
     import paper_2502_05370_amd as fm
     sys.path.insert(0, os.path.join(ROOT, "tests"))
@@ -130,13 +200,24 @@ def main():
     max_depth = int(np.clip(a["depth"], 1, s.L).max()) if s.B_traj else s.L
     stream = torch.cuda.current_stream()
 
-    def match():
+    hip = hip_runtime()
+    lib = fm._lib.load()
+    timers = {"k_sem_scan": ScanTimer(hip, lib, args.steps) if s.B_sem else None,
+              "k_traj_scan": ScanTimer(hip, lib, args.steps) if s.B_traj else None}
+
+    def match(i=None):
         if s.B_sem:
+            if i is not None:
+                timers["k_sem_scan"].arm(i)
             fm.match_semantic(store, q_sem, s.k, out=(idx[:s.B_sem], score[:s.B_sem]), workspace=ws_sem,
                               stream=stream)
         if s.B_traj:
+            if i is not None:
+                timers["k_traj_scan"].arm(i)
             fm.match_trajectory(store, q_traj, depth, s.k, max_depth=max_depth,
                                 out=(idx[s.B_sem:], score[s.B_sem:]), workspace=ws_traj, stream=stream)
+        if i is not None:
+            lib.fm_debug_scan_events(None, None)
 
     def select():
         fm.select_prefetch(store, idx, score, lb, le, tau=s.tau, k_min=s.k_min, k_max=s.k_max,
@@ -147,57 +228,51 @@ def main():
         select()
     torch.cuda.synchronize()
 
-    graph = None
-    if args.graph:
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            match()
-            select()
-        torch.cuda.synchronize()
-
-    # Timed region: K steps; HIP events bracket the match call of every step
-    # on the stream the kernels run on.
+    # Timed region: K steps of (match, select) on one stream.  HIP events
+    # bracket the match call of every step, and the library records a second
+    # pair right around each scan kernel launch on the same stream.
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        if graph is not None:
-            ev[i][0].record(stream)
-            graph.replay()
-            ev[i][1].record(stream)
-        else:
-            ev[i][0].record(stream)
-            match()
-            ev[i][1].record(stream)
-            select()
+        ev[i][0].record(stream)
+        match(i)
+        ev[i][1].record(stream)
+        select()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     elapsed = t1 - t0
     match_ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
+    scan_ms = {k: t.mean_ms(args.steps) for k, t in timers.items() if t is not None}
 
+    # Dominant kernel and its binding roofline: the larger of its algorithmic
+    # bytes at the HBM peak and its algorithmic flops at the MFMA peak of the
+    # arithmetic it implements (float32 products for float32 maps, bf16
+    # otherwise).
     cost = algorithmic_cost(s, a)
-    if s.B_sem and not s.B_traj:
-        # semantic-only: balanced, report against HBM (the binding roofline at this shape)
-        achieved = cost["sem_bytes"] / (match_ms * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": achieved / HBM_PEAK_GBS}
-        roof_kernel = "k_sem_scan"
-    elif s.config_no == 4:
-        achieved = cost["traj_flops"] / (match_ms * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": achieved, "peak": FP32_MFMA_PEAK_TFS, "unit": "TFLOP/s",
-                "frac": achieved / FP32_MFMA_PEAK_TFS}
-        roof_kernel = "k_traj_scan"
+    kernel = max(scan_ms, key=scan_ms.get)
+    if kernel == "k_traj_scan":
+        byts, flops = cost["traj_bytes"], cost["traj_flops"]
+        fpeak, fdt = (FP32_MFMA_PEAK_TFS, "f32") if s.map_dtype == "f32" else (BF16_MFMA_PEAK_TFS, "bf16")
     else:
-        byts = cost["traj_bytes"] + cost["sem_bytes"]
-        achieved = byts / (match_ms * 1e-3) / 1e9
+        byts, flops = cost["sem_bytes"], cost["sem_flops"]
+        fpeak, fdt = BF16_MFMA_PEAK_TFS, "bf16"
+    dur_s = scan_ms[kernel] * 1e-3
+    if flops / (fpeak * 1e12) > byts / (HBM_PEAK_GBS * 1e9):
+        achieved = flops / dur_s / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": fpeak, "unit": "TFLOP/s", "frac": achieved / fpeak}
+    else:
+        achieved = byts / dur_s / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": achieved / HBM_PEAK_GBS}
-        roof_kernel = "k_traj_scan" if s.B_traj else "k_sem_scan"
-    roof["traffic"] = COUNTER_TRAFFIC_BYTES.get(s.name)
-    roof["kernel"] = roof_kernel
-    roof["duration_us"] = match_ms * 1e3
-    roof["algorithmic_bytes"] = cost["traj_bytes"] + cost["sem_bytes"]
-    roof["algorithmic_flops"] = cost["traj_flops"] + cost["sem_flops"]
+    roof["traffic"] = counter_traffic(s.name) if COUNTERS_KIB.get(s.name, ("",))[0] == kernel else None
+    roof["kernel"] = kernel
+    roof["mfma_dtype"] = fdt
+    roof["duration_us"] = scan_ms[kernel] * 1e3
+    roof["algorithmic_bytes"] = byts
+    roof["algorithmic_flops"] = flops
+    roof["scan_us"] = {k: v * 1e3 for k, v in scan_ms.items()}
+    roof["match_call_us"] = match_ms * 1e3
 
     value = s.B * args.steps / elapsed
     gpu_idx = idx.cpu().numpy()
@@ -214,8 +289,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": s.name, "store_maps": s.n, "layers": s.L, "experts": s.E,
                    "map_dtype": s.map_dtype, "d_emb": s.d_emb, "batch": s.B, "batch_semantic": s.B_sem,
-                   "batch_trajectory": s.B_traj, "top_k": s.k, "tau": s.tau, "k_max": s.k_max,
-                   "graph": bool(args.graph)},
+                   "batch_trajectory": s.B_traj, "top_k": s.k, "tau": s.tau, "k_max": s.k_max},
         "roofline": roof,
         "cpu_baseline": cpu,
     }

@@ -201,6 +201,15 @@ fm_status fm_debug_scores(const fm_store* store, const void* q, const int32_t* d
                           int32_t max_depth, const void* q_sem, int32_t B, float* scores_out,
                           void* workspace, size_t workspace_bytes, void* stream);
 
+/* Measurement support: start and stop are hipEvent_t handles (passed as
+ * void*) created by the caller, or both NULL to switch this off.  While set,
+ * every match call made on this thread records start on its stream right
+ * before the launch of its scan kernel (k_traj_scan or k_sem_scan) and stop
+ * right after it, so the events bracket exactly that kernel (for a batch of
+ * more than 1024 queries, the last chunk's).  The library does not own or
+ * destroy the events.  FM_ERR_INVALID if exactly one of them is NULL. */
+fm_status fm_debug_scan_events(void* start, void* stop);
+
 /* Description of the last non-OK status on this thread ("" if none). */
 const char* fm_last_error(void);
 

@@ -51,6 +51,7 @@ SIGNATURES = {
     "fm_match_trajectory": (C.c_int, [_vp, _vp, _vp, _i32, _i32, _i32, _vp, _vp, _vp, _sz, _vp]),
     "fm_select_prefetch": (C.c_int, [_vp, _vp, _vp, _i32, _i32, _vp, _vp, C.POINTER(SelectParams), _vp, _vp, _vp]),
     "fm_debug_scores": (C.c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _sz, _vp]),
+    "fm_debug_scan_events": (C.c_int, [_vp, _vp]),
     "fm_last_error": (C.c_char_p, []),
     "fm_version": (C.c_int32, []),
 }

@@ -87,6 +87,11 @@ fm::Workspace carve(const fm_store*, void* ws) { return fm::carve_workspace(ws);
 
 namespace fm {
 
+ScanEvents& scan_events() {
+  thread_local ScanEvents ev;
+  return ev;
+}
+
 // Workspace layout: [partial][perm][sdep][rq][qrows], each part 256-byte
 // aligned.  qrows holds the staged queries of one launch: the trajectory
 // planes, or the tiled semantic queries (1024 x d_emb bf16).
@@ -359,6 +364,13 @@ fm_status fm_debug_scores(const fm_store* s, const void* q, const int32_t* depth
     e = fm::launch_match_semantic(s->v, q_sem, B, 1, nullptr, nullptr, scores_out, w, st);
   }
   if (e != hipSuccess) return hip_fail(e, "debug scores launch");
+  return ok();
+}
+
+fm_status fm_debug_scan_events(void* start, void* stop) {
+  if ((start == nullptr) != (stop == nullptr)) return fail(FM_ERR_INVALID, "start and stop must both be set or both NULL");
+  fm::scan_events().start = static_cast<hipEvent_t>(start);
+  fm::scan_events().stop = static_cast<hipEvent_t>(stop);
   return ok();
 }
 

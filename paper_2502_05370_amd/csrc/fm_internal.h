@@ -68,6 +68,14 @@ size_t traj_qrows_bytes(int L, int E, fm_dtype dt, int b_pad);
 hipError_t launch_finalize(const uint64_t* partial, const int32_t* perm, int32_t B, int32_t R, int32_t k, int KTOP,
                            int32_t* idx_out, float* score_out, hipStream_t st);
 
+// Caller-provided events bracketing the next scan launches on this thread
+// (both null when unset); see fm_debug_scan_events.
+struct ScanEvents {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+ScanEvents& scan_events();
+
 // Launchers (return hipSuccess or the first HIP error).
 hipError_t launch_insert(const StoreView& s, const void* maps, const void* embs, int32_t n_new,
                          int32_t* slots_out, hipStream_t st);

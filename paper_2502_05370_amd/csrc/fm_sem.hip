@@ -346,8 +346,15 @@ hipError_t sem_launch(const SemArgs& a, hipStream_t st) {
                                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
     if (err != hipSuccess) return err;
   }
+  const ScanEvents& ev = scan_events();
+  if (ev.start != nullptr) {
+    const hipError_t err = hipEventRecord(ev.start, st);
+    if (err != hipSuccess) return err;
+  }
   hipLaunchKernelGGL(kern, dim3(a.grid), dim3(512), lds, st, a);
-  return hipGetLastError();
+  const hipError_t err = hipGetLastError();
+  if (err != hipSuccess || ev.stop == nullptr) return err;
+  return hipEventRecord(ev.stop, st);
 }
 
 template <int KTOP>

@@ -11,25 +11,29 @@
 //                   (three parts of each float32 value, one plane for bf16
 //                   stores), zero beyond each query's depth and padded, so
 //                   the scan copies them verbatim.
-//  k_traj_scan      workgroup = one group of 16*TQ sorted queries x a range
-//                   of map slices (64*NBA maps each).  Map rows and query rows
-//                   of upcoming layer groups stream into an LDS ring of D+1
-//                   stages with direct global->LDS loads, D stages ahead of
-//                   the MFMAs.  A query tile (16 queries) stops at the layer
-//                   group of its deepest member.  float32 operands are split
-//                   into three bf16 parts a = a1 + a2 + a3 + r (|r| <= 2^-27
-//                   |a|) and a.b accumulates the six terms
-//                   a1b1 + a1b2 + a2b1 + a1b3 + a2b2 + a3b1 on
-//                   v_mfma_f32_16x16x32_bf16 (dropped terms < 2^-25 |ab|);
-//                   bf16 stores take one MFMA.  Squared map-row norms come
-//                   from the same operands, giving every map's prefix norm at
-//                   every depth.  A per-lane top-K of packed (score, index)
-//                   keys is merged across the workgroup and stored (plain
-//                   stores) as this workgroup's partial list per query.
+//  k_traj_scan      workgroup = one group of 16*TQ sorted queries x an even
+//                   share of the store's 16-map blocks, walked as slices of
+//                   8 waves x NBA blocks.  The map quads of a stage two stages
+//                   ahead load into registers (raw buffer loads), the query
+//                   planes into a three-slot LDS ring (direct global->LDS
+//                   loads); one barrier per stage.  A query tile (16 queries)
+//                   stops at the layer group of its deepest member.  float32
+//                   operands are split into three bf16 parts
+//                   a = a1 + a2 + a3 + r (|r| <= 2^-27 |a|) and a.b
+//                   accumulates the six terms a1b3 + a2b2 + a1b2 + a3b1 +
+//                   a2b1 + a1b1 on v_mfma_f32_16x16x32_bf16 (dropped terms
+//                   < 2^-25 |ab|); bf16 stores take one MFMA.  The slice
+//                   epilogue divides by the query's and the store's prefix
+//                   norms (the latter precomputed at insert), keeps a per-lane
+//                   top-K of packed (score, index) keys, merges it across the
+//                   workgroup and stores it (plain stores) as this workgroup's
+//                   partial list per query.
 //  k_finalize       merges the partial lists of each query into idx/score.
 //
 // "Slots": each layer's E experts padded to a multiple of 32, or LPG = 32/E
-// layers per 32 slots when E (>= 8) divides 32.
+// layers per 32 slots when E (>= 8) divides 32.  MFMA k position 8g + j of a
+// 32-slot k-step holds slot 4g + j (j < 4) or 16 + 4g + j - 4 (j >= 4), so
+// that the map operand of one k-step is two runs of whole expert quads.
 #include <type_traits>
 
 #include "fm_device.h"
@@ -727,8 +731,15 @@ hipError_t scan_launch(const ScanArgs& a, size_t lds, hipStream_t st) {
                                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
     if (err != hipSuccess) return err;
   }
+  const ScanEvents& ev = scan_events();
+  if (ev.start != nullptr) {
+    const hipError_t err = hipEventRecord(ev.start, st);
+    if (err != hipSuccess) return err;
+  }
   hipLaunchKernelGGL(kern, dim3(a.grid), dim3(512), lds, st, a);
-  return hipGetLastError();
+  const hipError_t err = hipGetLastError();
+  if (err != hipSuccess || ev.stop == nullptr) return err;
+  return hipEventRecord(ev.stop, st);
 }
 
 // Largest query-tile count per workgroup whose registers fit without spills

@@ -108,3 +108,10 @@ def test_no_device_is_a_hip_error_not_a_crash():
 def test_version():
     L, lib = _lib()
     assert lib.fm_version() >> 16 == 1
+
+
+def test_scan_events_need_both_or_neither():
+    L, lib = _lib()
+    assert lib.fm_debug_scan_events(C.c_void_p(0x1000), None) == L.FM_ERR_INVALID
+    assert lib.fm_debug_scan_events(None, C.c_void_p(0x1000)) == L.FM_ERR_INVALID
+    assert lib.fm_debug_scan_events(None, None) == L.FM_OK
