@@ -53,6 +53,7 @@ __device__ __forceinline__ bool ahead(double pi, int i, double pj, int j) {
 
 __global__ void __launch_bounds__(256) k_select(SelArgs a) {
   __shared__ double sorted[4][kMaxE];
+  __shared__ double vals[4][kMaxE];
   const int lane = threadIdx.x % kWave;
   const int wv = threadIdx.x / kWave;
   const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + wv;
@@ -116,25 +117,41 @@ __global__ void __launch_bounds__(256) k_select(SelArgs a) {
     tau = static_cast<double>(a.tau);
   }
 
-  // 3. rank
+  // 3. rank: every lane counts the experts ahead of its own, reading all
+  // values from LDS (broadcast reads, independent of each other)
+  if (lane < a.E) vals[wv][lane] = p;
+  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_wave_barrier();
   int rank = 0;
+#pragma unroll 8
   for (int i = 0; i < a.E; ++i) {
-    const double pi = __shfl(p, i, kWave);
+    const double pi = vals[wv][i];
     if (i != lane && ahead(pi, i, p, lane)) ++rank;
   }
   if (lane < a.E) sorted[wv][rank] = p;
   __builtin_amdgcn_s_waitcnt(0);
   __builtin_amdgcn_wave_barrier();
 
-  // 4. sequential float64 prefix sum in rank order
+  // 4. sequential float64 prefix sum in rank order: k* is the first count
+  // whose running sum reaches tau (E if none); values are read 8 at a time
+  // ahead of the sequential adds
   int kstar = a.E;
   double run = 0.0;
-  for (int kk = 0; kk <= a.E; ++kk) {
-    if (run >= tau) {
-      kstar = kk;
-      break;
+  bool found = false;
+  for (int k0 = 0; k0 < a.E && !found; k0 += 8) {
+    double v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = k0 + u < a.E ? sorted[wv][k0 + u] : 0.0;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (found || k0 + u >= a.E) break;
+      if (run >= tau) {
+        kstar = k0 + u;
+        found = true;
+        break;
+      }
+      run = __dadd_rn(run, v[u]);
     }
-    if (kk < a.E) run = __dadd_rn(run, sorted[wv][kk]);
   }
   int kk = kstar < a.k_min ? a.k_min : kstar;
   kk = kk > a.k_max ? a.k_max : kk;

@@ -745,7 +745,7 @@ hipError_t scan_launch(const ScanArgs& a, size_t lds, hipStream_t st) {
 // Largest query-tile count per workgroup whose registers fit without spills
 // (512 threads leave 256 registers per lane).
 constexpr int tq_limit(bool bf, int ksg, int ktop) {
-  return ktop == 1 ? (bf ? 16 : 8) : ktop == 4 ? ((bf || ksg == 1) ? 8 : 2) : ((bf || ksg == 1) ? 4 : 2);
+  return ktop == 1 ? (bf ? 16 : 8) : ktop == 4 ? ((bf || ksg == 1) ? 8 : 2) : (bf ? 4 : 2);
 }
 
 // NBA (16-map blocks per wave) follows from TQ: 2 up to 4 query tiles, else 1.
