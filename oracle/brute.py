@@ -61,3 +61,44 @@ def prefetch_set(p: Sequence[float], tau: float, k_min: int, k_max: int) -> Tupl
         if best_key is None or key < best_key:
             best, best_key = S, key
     return kk, frozenset(best if best is not None else ())
+
+
+def redundancy_fsum(old_map: Sequence[Sequence[float]], old_emb, new_map: Sequence[Sequence[float]], new_emb,
+                    d: int) -> float:
+    """RDY of one (new, stored) pair (Section 4.4) from correctly rounded
+    cosines: (d/L) * cos(embeddings) + ((L-d)/L) * cos(whole maps flattened),
+    a zero-weight term left out."""
+    L = len(old_map)
+    r = 0.0
+    if d > 0:
+        r += (d / L) * cosine_fsum(list(new_emb), list(old_emb))
+    if d < L:
+        flat_new = [v for row in new_map for v in row]
+        flat_old = [v for row in old_map for v in row]
+        r += ((L - d) / L) * cosine_fsum(flat_new, flat_old)
+    return r
+
+
+def dedup_by_enumeration(rdy: Sequence[Sequence[float]], size: int, cap: int) -> List[int]:
+    """Slots of a batch by exhaustive search (Section 4.4, no NaN in rdy).
+
+    The first cap - size new iterations are appended.  Over every injective
+    assignment of the remaining ones (in batch order) to stored iterations
+    (as many as can be assigned, the rest -1), take the one whose sequence of
+    (RDY, -index) pairs is lexicographically largest: the first replacing
+    iteration gets its most redundant entry, the next the most redundant of
+    the rest, and so on."""
+    m = len(rdy)
+    free = max(0, cap - size)
+    head = [size + x for x in range(min(m, free))]
+    rest = list(range(min(m, free), m))
+    r = min(len(rest), size)
+    best, best_key = None, None
+    for perm in itertools.permutations(range(size), r):
+        key = []
+        for x, y in zip(rest, perm):
+            key += [rdy[x][y], -y]
+        if best_key is None or key > best_key:
+            best, best_key = perm, key
+    tail = list(best) if best is not None else []
+    return head + tail + [-1] * (len(rest) - len(tail))

@@ -157,6 +157,93 @@ def match_semantic(embs: np.ndarray, Qs: np.ndarray, k: int, n: int = None) -> T
     return out_i, out_s
 
 
+# ---------------------------------------------------------------- store deduplication (Section 4.4)
+
+def redundancy(old_maps: np.ndarray, old_embs, new_maps: np.ndarray, new_embs, dtype: str,
+               d: int) -> np.ndarray:
+    """Pairwise redundancy RDY[x][y] of Section 4.4 between new iterations x
+    (rows) and stored iterations y (columns):
+
+        RDY[x][y] = (d / L) * score_sem[x][y] + ((L - d) / L) * score_traj[x][y]
+
+    with score_sem the Eq. 4 cosine of the embeddings and score_traj the Eq. 5
+    cosine over all L layers (a finished iteration has its whole map), d the
+    prefetch distance (0 <= d <= L).  A term whose weight is 0 is left out, so
+    a store without embeddings is deduplicated with d = 0 and a NaN in an
+    unused score does not reach RDY.  The weighted terms are added in that
+    order, in float64.
+
+    old_maps [s][L][E], new_maps [m][L][E] of ``dtype``; old_embs [s][d_emb]
+    and new_embs [m][d_emb] bf16 bits (may be None when d == 0).
+    Returns float64 [m][s].
+    """
+    s, L, E = old_maps.shape
+    m = new_maps.shape[0]
+    if not 0 <= d <= L:
+        raise ValueError(f"prefetch distance {d} outside [0, {L}]")
+    w_sem = d / L
+    w_traj = (L - d) / L
+    out = np.zeros((m, s), dtype=np.float64)
+    for a in range(0, s, _CHUNK):
+        b = min(a + _CHUNK, s)
+        M = widen(old_maps[a:b], dtype) if w_traj > 0.0 else None
+        X = widen(old_embs[a:b], "bf16") if w_sem > 0.0 else None
+        for x in range(m):
+            r = np.zeros(b - a, dtype=np.float64)
+            if w_sem > 0.0:
+                r = r + w_sem * semantic_scores(X, widen(new_embs[x], "bf16"))
+            if w_traj > 0.0:
+                r = r + w_traj * trajectory_scores(M, widen(new_maps[x], dtype), L)
+            out[x, a:b] = r
+    return out
+
+
+def dedup_slots(rdy: np.ndarray, size: int, cap: int) -> np.ndarray:
+    """Where each new iteration x = 0..m-1 of a batch is written (Section 4.4).
+
+    While the store has room, new iterations are appended in batch order
+    (slots size, size + 1, ...).  Once it is full, each remaining x, in batch
+    order, replaces the stored iteration it is most redundant with: the
+    highest RDY[x][y] (lower y first on equal values, NaN last) among the
+    iterations stored before this batch that no earlier x has replaced.  An x
+    left without such a candidate is dropped (slot -1).
+
+    rdy [m][size] float64 (rows of appended x are not read).
+    Returns slots [m] int64.
+    """
+    rdy = np.asarray(rdy, dtype=np.float64)
+    m = rdy.shape[0]
+    free = max(0, cap - size)
+    slots = np.full(m, -1, dtype=np.int64)
+    taken = np.zeros(size, dtype=bool)
+    for x in range(m):
+        if x < free:
+            slots[x] = size + x
+            continue
+        cand = np.flatnonzero(~taken)
+        if cand.size == 0:
+            continue
+        best, _ = rank(rdy[x, cand], 1, cand)
+        slots[x] = best[0]
+        taken[best[0]] = True
+    return slots
+
+
+def insert_dedup(old_maps: np.ndarray, old_embs, cap: int, new_maps: np.ndarray, new_embs,
+                 dtype: str, d: int) -> np.ndarray:
+    """Slots of a batch of new iterations inserted into a store holding
+    ``old_*`` (size = len(old_maps)) of capacity ``cap``: RDY is computed for
+    the new iterations that find the store full, then ``dedup_slots``."""
+    size = old_maps.shape[0]
+    m = new_maps.shape[0]
+    free = max(0, cap - size)
+    rdy = np.zeros((m, size), dtype=np.float64)
+    if m > free and size > 0:
+        rdy[free:] = redundancy(old_maps, old_embs, new_maps[free:],
+                                None if new_embs is None else new_embs[free:], dtype, d)
+    return dedup_slots(rdy, size, cap)
+
+
 # ---------------------------------------------------------------- threshold and selection (Section 4.3)
 
 def threshold(mode: int, tau: float, score: float) -> float:

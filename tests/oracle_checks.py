@@ -275,10 +275,129 @@ def check_select_prefetch_layout(seed=11):
     assert mask[2, 4] == m and cnt[2, 4] == c
 
 
+# ------------------------------------------------------------------ store deduplication (Section 4.4)
+
+def _bf16(x):
+    """bf16 bit patterns of float values (round to nearest even)."""
+    u = np.asarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    return u.astype(np.uint16)
+
+
+def _store(rng, n, L, E, d_emb, dtype="f32"):
+    maps = _rand_maps(rng, n, L, E, zero_frac=0.2)
+    if dtype == "bf16":
+        maps = _bf16(maps)
+    embs = _bf16(rng.standard_normal((n, d_emb)))
+    return maps, embs
+
+
+def check_redundancy_vs_fsum(seed=12):
+    rng = np.random.default_rng(seed)
+    for dtype in ("f32", "bf16"):
+        L, E, d_emb = 4, 5, 8
+        old_maps, old_embs = _store(rng, 7, L, E, d_emb, dtype)
+        new_maps, new_embs = _store(rng, 3, L, E, d_emb, dtype)
+        for d in range(L + 1):
+            got = F.redundancy(old_maps, old_embs, new_maps, new_embs, dtype, d)
+            assert got.shape == (3, 7)
+            for x in range(3):
+                for y in range(7):
+                    ref = brute.redundancy_fsum(F.widen(old_maps[y], dtype).tolist(), F.widen(old_embs[y], "bf16"),
+                                                F.widen(new_maps[x], dtype).tolist(), F.widen(new_embs[x], "bf16"), d)
+                    assert abs(got[x, y] - ref) <= 1e-14, (dtype, d, x, y, got[x, y], ref)
+
+
+def check_redundancy_closed_forms(seed=13):
+    rng = np.random.default_rng(seed)
+    L, E, d_emb = 6, 4, 16
+    maps, embs = _store(rng, 5, L, E, d_emb)
+    for d in range(L + 1):
+        # an iteration is fully redundant with itself
+        r = F.redundancy(maps, embs, maps[2:3], embs[2:3], "f32", d)
+        assert abs(r[0, 2] - 1.0) <= 1e-15, (d, r[0, 2])
+    # disjoint expert supports and orthogonal embeddings: nothing in common
+    a = np.zeros((1, L, E), np.float32)
+    b = np.zeros((1, L, E), np.float32)
+    a[0, :, :2] = 0.5
+    b[0, :, 2:] = 0.5
+    ea = _bf16(np.eye(d_emb)[:1])
+    eb = _bf16(np.eye(d_emb)[1:2])
+    for d in range(L + 1):
+        assert F.redundancy(a, ea, b, eb, "f32", d)[0, 0] == 0.0
+    # the two halves weigh d/L and (L-d)/L: same map, orthogonal embeddings
+    for d in range(L + 1):
+        r = F.redundancy(a, ea, a, eb, "f32", d)[0, 0]
+        assert abs(r - (L - d) / L) <= 1e-15, (d, r)
+        r = F.redundancy(a, ea, b, ea, "f32", d)[0, 0]
+        assert abs(r - d / L) <= 1e-15, (d, r)
+    # a map that differs only in its last layer still counts that layer
+    c = a.copy()
+    c[0, L - 1] = b[0, L - 1]
+    r = F.redundancy(a, ea, c, ea, "f32", 0)[0, 0]
+    assert abs(r - (L - 1) / L) <= 1e-15, r
+
+
+def check_dedup_vs_enumeration(seed=14):
+    rng = np.random.default_rng(seed)
+    for _ in range(300):
+        size = int(rng.integers(0, 6))
+        cap = size + int(rng.integers(0, 3))
+        m = int(rng.integers(0, 5))
+        rdy = np.round(rng.uniform(-1, 1, (m, size)), 1)   # coarse values give ties
+        got = F.dedup_slots(rdy, size, cap)
+        ref = brute.dedup_by_enumeration(rdy.tolist(), size, cap)
+        assert list(got) == ref, (size, cap, rdy, list(got), ref)
+
+
+def check_dedup_duplicates(seed=15):
+    rng = np.random.default_rng(seed)
+    L, E, d_emb = 4, 6, 8
+    maps, embs = _store(rng, 12, L, E, d_emb)
+    pick = [5, 2, 5]
+    new_maps = np.concatenate([maps[pick], _store(rng, 1, L, E, d_emb)[0]])
+    new_embs = np.concatenate([embs[pick], _store(rng, 1, L, E, d_emb)[1]])
+    for d in (0, 1, L):
+        slots = F.insert_dedup(maps, embs, 12, new_maps, new_embs, "f32", d)
+        # exact copies replace their originals; the second copy of 5 takes its
+        # next most redundant entry, and every victim is distinct
+        assert slots[0] == 5 and slots[1] == 2, slots
+        rdy = [[brute.redundancy_fsum(F.widen(maps[y], "f32").tolist(), F.widen(embs[y], "bf16"),
+                                      F.widen(new_maps[x], "f32").tolist(), F.widen(new_embs[x], "bf16"), d)
+                for y in range(12)] for x in range(4)]
+        rest = [y for y in range(12) if y not in (5, 2)]
+        assert slots[2] == max(rest, key=lambda y: (rdy[2][y], -y)), slots
+        rest = [y for y in rest if y != slots[2]]
+        assert slots[3] == max(rest, key=lambda y: (rdy[3][y], -y)), slots
+        assert len(set(slots.tolist())) == 4
+
+
+def check_dedup_appends_first():
+    rng = np.random.default_rng(16)
+    L, E, d_emb = 3, 4, 8
+    maps, embs = _store(rng, 3, L, E, d_emb)
+    new_maps, new_embs = _store(rng, 4, L, E, d_emb)
+    # room for two: appended at 3 and 4, the other two replace stored entries
+    slots = F.insert_dedup(maps, embs, 5, new_maps, new_embs, "f32", 1)
+    assert list(slots[:2]) == [3, 4] and all(0 <= y < 3 for y in slots[2:]) and slots[2] != slots[3], slots
+    # room for all: nothing is replaced
+    assert list(F.insert_dedup(maps, embs, 10, new_maps, new_embs, "f32", 1)) == [3, 4, 5, 6]
+    # empty store smaller than the batch: the overflow is dropped
+    empty_m, empty_e = maps[:0], embs[:0]
+    assert list(F.insert_dedup(empty_m, empty_e, 2, new_maps[:3], new_embs[:3], "f32", 1)) == [0, 1, -1]
+    # full store smaller than the batch: every entry is replaced once, then drop
+    slots = F.insert_dedup(maps, embs, 3, new_maps, new_embs, "f32", 1)
+    assert sorted(slots[:3].tolist()) == [0, 1, 2] and slots[3] == -1, slots
+    # no embeddings needed when d = 0
+    slots = F.insert_dedup(maps, None, 3, new_maps[:1], None, "f32", 0)
+    assert 0 <= slots[0] < 3
+
+
 ALL_CHECKS = [
     check_cosine_vs_fsum, check_cosine_vs_torch, check_self_match, check_disjoint_support,
     check_depth_special_cases, check_unobserved_layers_ignored, check_semantic_vs_fsum,
     check_match_vs_bruteforce, check_rank_rules, check_uniform_golden, check_delta_golden,
     check_select_vs_enumeration, check_select_nesting_and_minimality, check_blend,
-    check_select_prefetch_layout,
+    check_select_prefetch_layout, check_redundancy_vs_fsum, check_redundancy_closed_forms,
+    check_dedup_vs_enumeration, check_dedup_duplicates, check_dedup_appends_first,
 ]

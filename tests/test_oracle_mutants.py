@@ -149,6 +149,48 @@ def score_as_delta(mode, tau, score):
     return _orig_threshold(mode, tau, score)
 
 
+_orig_redundancy = F.redundancy
+_orig_dedup_slots = F.dedup_slots
+
+
+def redundancy_swapped_weights(old_maps, old_embs, new_maps, new_embs, dtype, d):
+    L = old_maps.shape[1]
+    return _orig_redundancy(old_maps, old_embs, new_maps, new_embs, dtype, L - d)
+
+
+def redundancy_partial_depth(old_maps, old_embs, new_maps, new_embs, dtype, d):
+    L = old_maps.shape[1]
+    out = np.zeros((new_maps.shape[0], old_maps.shape[0]))
+    for x in range(new_maps.shape[0]):
+        r = 0.0
+        if d > 0:
+            r = r + (d / L) * F.semantic_scores(F.widen(old_embs, "bf16"), F.widen(new_embs[x], "bf16"))
+        if d < L:
+            r = r + ((L - d) / L) * F.trajectory_scores(F.widen(old_maps, dtype), F.widen(new_maps[x], dtype), L - 1)
+        out[x] = r
+    return out
+
+
+def dedup_reuses_victims(rdy, size, cap):
+    rdy = np.asarray(rdy, dtype=np.float64)
+    free = max(0, cap - size)
+    out = np.full(rdy.shape[0], -1, dtype=np.int64)
+    for x in range(rdy.shape[0]):
+        if x < free:
+            out[x] = size + x
+        elif size > 0:
+            out[x] = F.rank(rdy[x], 1)[0][0]
+    return out
+
+
+def dedup_least_redundant(rdy, size, cap):
+    return _orig_dedup_slots(-np.asarray(rdy, dtype=np.float64), size, cap)
+
+
+def dedup_never_appends(rdy, size, cap):
+    return _orig_dedup_slots(rdy, size, min(cap, size) if size > 0 else cap)
+
+
 MUTANTS = [
     ("select_row", strict_threshold_select),
     ("select_row", high_index_first_select),
@@ -165,6 +207,11 @@ MUTANTS = [
     ("blend_rows", softmax_weight_blend),
     ("threshold", unclipped_delta),
     ("threshold", score_as_delta),
+    ("redundancy", redundancy_swapped_weights),
+    ("redundancy", redundancy_partial_depth),
+    ("dedup_slots", dedup_reuses_victims),
+    ("dedup_slots", dedup_least_redundant),
+    ("dedup_slots", dedup_never_appends),
 ]
 
 
