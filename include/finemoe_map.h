@@ -144,6 +144,37 @@ fm_status fm_store_build(fm_store** out, const fm_store_desc* desc);
 fm_status fm_store_insert(fm_store* store, const void* maps, const void* embs, int32_t n,
                           int32_t* slots_out, void* stream);
 
+/* Bytes of scratch (device memory owned by the caller, 256-byte aligned)
+ * that fm_store_insert_dedup needs for batches of up to n_max new iterations
+ * on a store of capacity cap: two dense float32 matrices of n_max x cap
+ * scores plus 72 KB of index arrays.  Returns 0 unless cap >= 1 and
+ * 1 <= n_max <= 1024. */
+size_t fm_dedup_scratch_bytes(int32_t cap, int32_t n_max);
+
+/* Insert with deduplication (Section 4.4, Expert map deduplication).  maps,
+ * embs and slots_out as for fm_store_insert, 1 <= n <= 1024 (n == 0 is a
+ * no-op).  While the store has room, new iterations are appended in batch
+ * order.  The rest replace stored iterations: for each such new iteration x
+ * the redundancy score against every iteration y stored before this call is
+ *     RDY[x][y] = (d/L) score_sem[x][y] + ((L-d)/L) score_traj[x][y]
+ * with d = prefetch_distance (0..L), score_sem the Eq. 4 cosine of the
+ * embeddings and score_traj the Eq. 5 cosine over all L layers, both as the
+ * match calls compute them (float32), weighted in float64 and rounded to
+ * float32; a term with weight 0 is not computed.  In batch order, each x
+ * overwrites the y with the highest RDY (lower index on equal values, NaN
+ * last) that no earlier x of this call took; an x left without a candidate
+ * (a store of fewer than n entries) is dropped and gets slot -1.  The
+ * store size becomes min(size + n, cap).
+ * workspace: as for the match calls, sized with B_max >= n.  scratch: at least
+ * fm_dedup_scratch_bytes(cap, n) bytes, rewritten by the call.  Calls sharing
+ * a workspace or scratch must be ordered.
+ * Errors: FM_ERR_INVALID for NULL or misaligned pointers, n or d out of
+ * range, d > 0 on a store without embeddings, or a short workspace or
+ * scratch; nothing is enqueued then. */
+fm_status fm_store_insert_dedup(fm_store* store, const void* maps, const void* embs, int32_t n,
+                                int32_t prefetch_distance, int32_t* slots_out, void* workspace,
+                                size_t workspace_bytes, void* scratch, size_t scratch_bytes, void* stream);
+
 /* Current number of stored iterations (host-side count, no synchronisation). */
 fm_status fm_store_size(const fm_store* store, int32_t* n_out);
 

@@ -9,6 +9,7 @@ been built.
 
     store = Store(cap, L, E, d_emb=0, map_dtype="f32")
     store.insert(maps, embs=None)                       # maps [n][L][E] on the GPU
+    slots = store.insert_dedup(maps, embs, d)           # Section 4.4, replaces when full
     idx, score = match_trajectory(store, q, depth, k=1) # Eq. 5
     idx, score = match_semantic(store, q_sem, k=1)      # Eq. 4
     mask, count = select_prefetch(store, idx, score, layer_begin, layer_end,
@@ -28,7 +29,7 @@ from ._lib import (FM_BF16, FM_BLEND_NONE, FM_BLEND_SCORE, FM_F32, FM_FLAG_DEPTH
 _lib.load()
 
 __all__ = ["Store", "Workspace", "match_semantic", "match_trajectory", "select_prefetch", "debug_scores",
-           "map_bytes", "store_bytes", "workspace_bytes", "FmError"]
+           "map_bytes", "store_bytes", "workspace_bytes", "dedup_scratch_bytes", "FmError"]
 
 _DTYPES = {"f32": FM_F32, "bf16": FM_BF16}
 _TORCH = {FM_F32: torch.float32, FM_BF16: torch.bfloat16}
@@ -62,6 +63,10 @@ def store_bytes(cap: int, L: int, E: int, d_emb: int = 0, map_dtype: str = "f32"
 def workspace_bytes(L: int, E: int, d_emb: int = 0, map_dtype: str = "f32", B_max: int = 1024,
                     k_max: int = 8) -> int:
     return int(_lib.load().fm_workspace_bytes(L, E, d_emb, _DTYPES[map_dtype], B_max, k_max))
+
+
+def dedup_scratch_bytes(cap: int, n_max: int) -> int:
+    return int(_lib.load().fm_dedup_scratch_bytes(cap, n_max))
 
 
 class Workspace:
@@ -99,6 +104,7 @@ class Store:
             _lib.check(_lib.load().fm_store_build(C.byref(h), C.byref(desc)), "fm_store_build")
         self.handle = h
         self.workspace = None
+        self._dedup_scratch = None
 
     def __del__(self):
         h = getattr(self, "handle", None)
@@ -127,6 +133,34 @@ class Store:
         slots = torch.empty(n, dtype=torch.int32, device=self.device) if return_slots else None
         _lib.check(_lib.load().fm_store_insert(self.handle, _ptr(maps), _ptr(embs), n, _ptr(slots),
                                                _stream(stream)), "fm_store_insert")
+        return slots
+
+    def insert_dedup(self, maps: torch.Tensor, embs: Optional[torch.Tensor], d: int,
+                     workspace: Optional["Workspace"] = None, scratch: Optional[torch.Tensor] = None,
+                     stream=None) -> torch.Tensor:
+        """Insert with deduplication (Section 4.4): append while there is room,
+        then replace the most redundant stored iterations (RDY with prefetch
+        distance d).  Returns the slot of each new iteration (int32, -1 if
+        dropped) on the device."""
+        maps = maps.contiguous()
+        if maps.dtype != _TORCH[self.dtype_code] or maps.dim() != 3 or tuple(maps.shape[1:]) != (self.L, self.E):
+            raise ValueError(f"maps must be [n][{self.L}][{self.E}] {_TORCH[self.dtype_code]}, got "
+                             f"{tuple(maps.shape)} {maps.dtype}")
+        n = maps.shape[0]
+        if embs is not None:
+            embs = embs.contiguous()
+            if embs.dtype != torch.bfloat16 or tuple(embs.shape) != (n, self.d_emb):
+                raise ValueError(f"embs must be [{n}][{self.d_emb}] bfloat16")
+        ws = workspace if workspace is not None else self.ensure_workspace()
+        if scratch is None:
+            need = dedup_scratch_bytes(self.cap, max(n, 1))
+            if self._dedup_scratch is None or self._dedup_scratch.numel() < need:
+                self._dedup_scratch = _aligned_bytes(need, self.device)
+            scratch = self._dedup_scratch
+        slots = torch.empty(n, dtype=torch.int32, device=self.device)
+        _lib.check(_lib.load().fm_store_insert_dedup(self.handle, _ptr(maps), _ptr(embs), n, int(d), _ptr(slots),
+                                                     ws.ptr, ws.nbytes, _ptr(scratch), scratch.numel(),
+                                                     _stream(stream)), "fm_store_insert_dedup")
         return slots
 
     def check(self, stream=None) -> int:

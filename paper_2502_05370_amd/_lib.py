@@ -44,6 +44,8 @@ SIGNATURES = {
     "fm_workspace_bytes": (_sz, [_i32, _i32, _i32, C.c_int, _i32, _i32]),
     "fm_store_build": (C.c_int, [C.POINTER(_vp), C.POINTER(StoreDesc)]),
     "fm_store_insert": (C.c_int, [_vp, _vp, _vp, _i32, _vp, _vp]),
+    "fm_dedup_scratch_bytes": (_sz, [_i32, _i32]),
+    "fm_store_insert_dedup": (C.c_int, [_vp, _vp, _vp, _i32, _i32, _vp, _vp, _sz, _vp, _sz, _vp]),
     "fm_store_size": (C.c_int, [_vp, C.POINTER(_i32)]),
     "fm_store_check": (C.c_int, [_vp, _vp, C.POINTER(C.c_uint32)]),
     "fm_store_destroy": (C.c_int, [_vp]),

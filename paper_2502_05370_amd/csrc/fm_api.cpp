@@ -243,9 +243,46 @@ fm_status fm_store_insert(fm_store* s, const void* maps, const void* embs, int32
     return fail(FM_ERR_FULL, "inserting %d into a store holding %d of %d", n, s->v.n, s->v.cap);
   DeviceGuard dg(s->device);
   if (!dg.ok) return fail(FM_ERR_HIP, "cannot select the store's device %d", s->device);
-  hipError_t e = fm::launch_insert(s->v, maps, embs, n, slots_out, static_cast<hipStream_t>(stream));
+  hipError_t e = fm::launch_insert(s->v, maps, embs, n, nullptr, slots_out, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "insert launch");
   s->v.n += n;
+  return ok();
+}
+
+size_t fm_dedup_scratch_bytes(int32_t cap, int32_t n_max) {
+  if (cap < 1 || n_max < 1 || n_max > fm::kChunkB) return 0;
+  return fm::dedup_scratch_bytes(cap, n_max);
+}
+
+fm_status fm_store_insert_dedup(fm_store* s, const void* maps, const void* embs, int32_t n, int32_t d,
+                                int32_t* slots_out, void* ws, size_t ws_bytes, void* scratch, size_t scratch_bytes,
+                                void* stream) {
+  if (fm_status st = check_store(s)) return st;
+  if (n < 0 || n > fm::kChunkB) return fail(FM_ERR_INVALID, "n=%d outside [0, %d]", n, fm::kChunkB);
+  if (n == 0) return ok();
+  if (maps == nullptr) return fail(FM_ERR_INVALID, "maps is NULL");
+  if (d < 0 || d > s->v.L) return fail(FM_ERR_INVALID, "prefetch distance d=%d outside [0, L=%d]", d, s->v.L);
+  if (d > 0 && s->v.d_emb == 0)
+    return fail(FM_ERR_INVALID, "prefetch distance d=%d weighs semantic scores but the store has no embeddings", d);
+  if (s->v.d_emb > 0 && embs == nullptr) return fail(FM_ERR_INVALID, "store has d_emb=%d but embs is NULL", s->v.d_emb);
+  if (s->v.d_emb > 0 && reinterpret_cast<uintptr_t>(embs) % 16 != 0)
+    return fail(FM_ERR_INVALID, "embs must be 16-byte aligned");
+  if (fm_status st = check_workspace(s, ws, ws_bytes)) return st;
+  if (scratch == nullptr) return fail(FM_ERR_INVALID, "scratch is NULL");
+  if (reinterpret_cast<uintptr_t>(scratch) % fm::kAlign != 0)
+    return fail(FM_ERR_INVALID, "scratch must be %zu-byte aligned", fm::kAlign);
+  const size_t need = fm::dedup_scratch_bytes(s->v.cap, n);
+  if (scratch_bytes < need)
+    return fail(FM_ERR_INVALID, "scratch of %zu bytes is smaller than fm_dedup_scratch_bytes(cap=%d, n=%d) = %zu",
+                scratch_bytes, s->v.cap, n, need);
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(FM_ERR_HIP, "cannot select the store's device %d", s->device);
+  const fm::DedupScratch sc = fm::carve_dedup_scratch(scratch, s->v.cap, n);
+  hipError_t e = fm::launch_insert_dedup(s->v, maps, embs, n, d, slots_out, carve(s, ws), sc,
+                                         static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "deduplicating insert launch");
+  const int32_t room = s->v.cap - s->v.n;
+  s->v.n += n < room ? n : room;
   return ok();
 }
 

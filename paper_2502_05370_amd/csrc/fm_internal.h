@@ -63,6 +63,20 @@ struct Workspace {
   void* qrows;        // staged query rows of every layer group (trajectory)
 };
 size_t workspace_bytes_needed(int32_t L, int32_t E, int32_t d_emb, fm_dtype map_dtype);
+
+// Scratch of a deduplicating insert: [depth][slots][cand][cand_score] sized
+// for kChunkB new iterations, then the two dense score matrices of n_max x
+// cap float32 (each part 256-byte aligned).  Rewritten by every call.
+struct DedupScratch {
+  int32_t* depth;       // [kChunkB] full depth L for the trajectory scan
+  int32_t* slots;       // [kChunkB] slot of each new iteration (-1: dropped)
+  int32_t* cand;        // [kChunkB][8] best replacement candidates
+  float* cand_score;    // [kChunkB][8] their RDY
+  float* sem;           // [m][size] semantic scores
+  float* traj;          // [m][size] full-depth trajectory scores
+};
+size_t dedup_scratch_bytes(int32_t cap, int32_t n_max);
+DedupScratch carve_dedup_scratch(void* base, int32_t cap, int32_t n_max);
 Workspace carve_workspace(void* base);
 size_t traj_qrows_bytes(int L, int E, fm_dtype dt, int b_pad);
 hipError_t launch_finalize(const uint64_t* partial, const int32_t* perm, int32_t B, int32_t R, int32_t k, int KTOP,
@@ -78,7 +92,9 @@ ScanEvents& scan_events();
 
 // Launchers (return hipSuccess or the first HIP error).
 hipError_t launch_insert(const StoreView& s, const void* maps, const void* embs, int32_t n_new,
-                         int32_t* slots_out, hipStream_t st);
+                         const int32_t* slot_of, int32_t* slots_out, hipStream_t st);
+hipError_t launch_insert_dedup(const StoreView& s, const void* maps, const void* embs, int32_t n, int32_t d,
+                               int32_t* slots_out, const Workspace& ws, const DedupScratch& sc, hipStream_t st);
 hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int32_t* depth,
                                    int32_t max_depth, int32_t B, int32_t k, int32_t* idx_out,
                                    float* score_out, float* dbg_scores, const Workspace& ws,

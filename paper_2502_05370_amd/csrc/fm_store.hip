@@ -11,6 +11,12 @@
 
 namespace fm {
 
+// Slot of new iteration i: first_slot + i, or slot_of[i] when a slot array
+// is given (deduplicating inserts; -1 means the iteration is dropped).
+__device__ __forceinline__ int64_t slot_for(int32_t first_slot, const int32_t* slot_of, int i) {
+  return slot_of != nullptr ? static_cast<int64_t>(slot_of[i]) : static_cast<int64_t>(first_slot) + i;
+}
+
 // One wavefront per new map: each layer row is copied into its plane (with
 // zeros in the row padding), and the running float64 sum of squares over
 // layers 0..l gives the prefix inverse norm 1/|x[y][0:l+1]| that the
@@ -18,13 +24,15 @@ namespace fm {
 template <typename T>
 __global__ void __launch_bounds__(256) k_insert_maps(const T* __restrict__ src, T* __restrict__ planes,
                                                      int64_t plane_elems, float* __restrict__ rnorm,
-                                                     int64_t rn_stride, int32_t first_slot, int32_t n_new,
+                                                     int64_t rn_stride, int32_t first_slot,
+                                                     const int32_t* __restrict__ slot_of, int32_t n_new,
                                                      int32_t L, int32_t E, int32_t row,
                                                      int32_t* __restrict__ slots_out) {
   const int lane = threadIdx.x % kWave;
   const int i = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
   if (i >= n_new) return;
-  const int64_t y = static_cast<int64_t>(first_slot) + i;
+  const int64_t y = slot_for(first_slot, slot_of, i);
+  if (y < 0) return;
   double cum = 0.0;
   for (int l = 0; l < L; ++l) {
     double sq = 0.0;
@@ -56,13 +64,14 @@ __global__ void __launch_bounds__(256) k_insert_maps(const T* __restrict__ src, 
 // (emb_offset, 8 consecutive dimensions per 16-byte store) and compute its
 // norm.
 __global__ void __launch_bounds__(256) k_insert_embs(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst,
-                                                     float* __restrict__ norms, int32_t first_slot, int32_t n_new,
-                                                     int32_t d) {
+                                                     float* __restrict__ norms, int32_t first_slot,
+                                                     const int32_t* __restrict__ slot_of, int32_t n_new, int32_t d) {
   const int lane = threadIdx.x % kWave;
   const int row = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
   if (row >= n_new) return;
   const uint16_t* s = src + static_cast<int64_t>(row) * d;
-  const int64_t y = static_cast<int64_t>(first_slot) + row;
+  const int64_t y = slot_for(first_slot, slot_of, row);
+  if (y < 0) return;
   double acc = 0.0;
   for (int j0 = 8 * lane; j0 < d; j0 += 8 * kWave) {
     const u16x8 h = *reinterpret_cast<const u16x8*>(s + j0);
@@ -76,28 +85,28 @@ __global__ void __launch_bounds__(256) k_insert_embs(const uint16_t* __restrict_
   // Fixed-order tree reduction across the wave.
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, kWave);
-  if (lane == 0) norms[first_slot + row] = static_cast<float>(sqrt(acc));
+  if (lane == 0) norms[y] = static_cast<float>(sqrt(acc));
 }
 
 hipError_t launch_insert(const StoreView& s, const void* maps, const void* embs, int32_t n_new,
-                         int32_t* slots_out, hipStream_t st) {
+                         const int32_t* slot_of, int32_t* slots_out, hipStream_t st) {
   if (n_new <= 0) return hipSuccess;
   const int rows_per_block = 256 / kWave;
   const dim3 grid((n_new + rows_per_block - 1) / rows_per_block);
   if (s.map_dtype == FM_F32) {
     hipLaunchKernelGGL(k_insert_maps<float>, grid, dim3(256), 0, st, static_cast<const float*>(maps),
-                       static_cast<float*>(s.planes), s.plane_elems, s.rnorm, s.rn_stride, s.n, n_new, s.L, s.E,
-                       s.row, slots_out);
+                       static_cast<float*>(s.planes), s.plane_elems, s.rnorm, s.rn_stride, s.n, slot_of, n_new, s.L,
+                       s.E, s.row, slots_out);
   } else {
     hipLaunchKernelGGL(k_insert_maps<uint16_t>, grid, dim3(256), 0, st, static_cast<const uint16_t*>(maps),
-                       static_cast<uint16_t*>(s.planes), s.plane_elems, s.rnorm, s.rn_stride, s.n, n_new, s.L,
-                       s.E, s.row, slots_out);
+                       static_cast<uint16_t*>(s.planes), s.plane_elems, s.rnorm, s.rn_stride, s.n, slot_of, n_new,
+                       s.L, s.E, s.row, slots_out);
   }
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   if (s.d_emb > 0) {
     hipLaunchKernelGGL(k_insert_embs, dim3((n_new + rows_per_block - 1) / rows_per_block), dim3(256), 0, st,
-                       static_cast<const uint16_t*>(embs), s.embs, s.emb_norm, s.n, n_new, s.d_emb);
+                       static_cast<const uint16_t*>(embs), s.embs, s.emb_norm, s.n, slot_of, n_new, s.d_emb);
     err = hipGetLastError();
   }
   return err;

@@ -39,6 +39,7 @@ _STREAMS = (
     "query_src", "query_noise", "depth",
     "emb_centroids", "emb_assign", "emb_noise",
     "qemb_assign", "qemb_noise",
+    "new_assign", "new_map_noise", "new_emb_noise", "new_dup",
 )
 
 F32 = "f32"
@@ -235,6 +236,42 @@ def generate(s: Spec) -> Dict[str, np.ndarray]:
         le += [L] * s.B_traj
     out["lb"] = np.asarray(lb, dtype=np.int32)
     out["le"] = np.asarray(le, dtype=np.int32)
+    return out
+
+
+def generate_new(s: Spec, m: int, stored: Dict[str, np.ndarray], dup_frac: float = 0.125) -> Dict[str, np.ndarray]:
+    """A batch of ``m`` new iterations for a store drawn by ``generate(s)``.
+
+    New maps and embeddings come from the same clusters as the stored ones
+    (fresh noise streams); a fraction ``dup_frac`` of them are exact copies of
+    randomly chosen stored iterations (repeated prompts).  Returns
+      new_maps [m][L][E] (store dtype), new_embs [m][d_emb] bf16 bits (absent
+      when d_emb == 0), dup_src [m] int32 (stored index copied, -1 if none).
+    """
+    L, E = s.L, s.E
+    n = stored["maps"].shape[0]
+    Zc = rng(s.config_no, "map_centroids").standard_normal((s.map_centroids, L, E), dtype=np.float32)
+    g = rng(s.config_no, "new_assign")
+    out: Dict[str, np.ndarray] = {}
+    if s.d_emb:
+        mu = _emb_centroids(s)
+        ea = g.integers(0, s.emb_centroids, size=m)
+        out["new_embs"] = _draw_embeddings(s, mu, ea, rng(s.config_no, "new_emb_noise"))
+        cent = ea % s.map_of_emb_mod if s.map_of_emb_mod else g.integers(0, s.map_centroids, size=m)
+    else:
+        cent = g.integers(0, s.map_centroids, size=m)
+    z = Zc[cent] + np.float32(s.map_sigma) * rng(s.config_no, "new_map_noise").standard_normal(
+        (m, L, E), dtype=np.float32)
+    out["new_maps"] = _cast(_row_softmax_f32(z), s.map_dtype)
+    d = rng(s.config_no, "new_dup")
+    dup = np.full(m, -1, dtype=np.int32)
+    if n > 0:
+        pick = d.random(m) < dup_frac
+        dup[pick] = d.integers(0, n, size=int(pick.sum()))
+        out["new_maps"][pick] = stored["maps"][dup[pick]]
+        if s.d_emb:
+            out["new_embs"][pick] = stored["embs"][dup[pick]]
+    out["dup_src"] = dup
     return out
 
 

@@ -158,3 +158,79 @@ def compare_select(s, a, g: GpuResult, tau_mode=None, tau=None, k_min=None, k_ma
         s.k_max if k_max is None else k_max, s.blend)
     bad = np.argwhere((mask != g.mask) | (count != g.count))
     return bad, mask, count
+
+
+# ---------------------------------------------------------------- deduplicating inserts (Section 4.4)
+
+# RDY combines two float32 scores with weights summing to 1 and rounds once
+# to float32, so its error stays within the score tolerance plus 2^-24.
+RDY_TOL = SCORE_TOL + 2.0 ** -24
+
+
+@dataclasses.dataclass
+class DedupReport:
+    replaced: int = 0
+    near_ties: int = 0
+    exact: bool = True
+    failures: list = dataclasses.field(default_factory=list)
+
+
+def compare_dedup(slots, old_maps, old_embs, cap, new_maps, new_embs, dtype, d) -> DedupReport:
+    """Check GPU slots of a deduplicating insert against the oracle.
+
+    Appended slots must be exact.  Replacements are replayed in batch order:
+    each GPU victim must be a pre-batch entry not taken before, and its oracle
+    RDY must be within the near-tie margin 2 * RDY_TOL of the best oracle RDY
+    among the entries still available; where no near-tie exists this makes the
+    victim the oracle's.  A new iteration may be dropped (-1) only when no
+    entry is left."""
+    rep = DedupReport()
+    slots = np.asarray(slots, dtype=np.int64)
+    size = old_maps.shape[0]
+    m = new_maps.shape[0]
+    free = max(0, cap - size)
+    n_app = min(m, free)
+    if not np.array_equal(slots[:n_app], size + np.arange(n_app)):
+        rep.failures.append(("appended slots", slots[:n_app].tolist()))
+        return rep
+    rest = np.arange(n_app, m)
+    ref = oracle.insert_dedup(old_maps, old_embs, cap, new_maps, new_embs, dtype, d)
+    rep.exact = bool(np.array_equal(ref, slots))
+    if rest.size == 0:
+        return rep
+    rdy = oracle.redundancy(old_maps, old_embs, new_maps[rest], None if new_embs is None else new_embs[rest],
+                            dtype, d) if size > 0 else np.zeros((rest.size, 0))
+    taken = np.zeros(size, dtype=bool)
+    margin = 2 * RDY_TOL
+    for i, x in enumerate(rest):
+        y = int(slots[x])
+        avail = np.flatnonzero(~taken)
+        if avail.size == 0:
+            if y != -1:
+                rep.failures.append((int(x), "slot given with nothing left", y))
+            continue
+        if y < 0 or y >= size or taken[y]:
+            rep.failures.append((int(x), "invalid victim", y))
+            continue
+        rep.replaced += 1
+        row = rdy[i, avail]
+        best_y, _ = oracle.rank(row, 1, avail)
+        best = rdy[i, best_y[0]]
+        if y != best_y[0]:
+            if np.isnan(best) or not rdy[i, y] >= best - margin:
+                rep.failures.append((int(x), "victim", y, float(rdy[i, y]), int(best_y[0]), float(best)))
+            else:
+                rep.near_ties += 1
+        taken[y] = True
+    return rep
+
+
+def apply_slots(old, new, slots, cap):
+    """The store contents after writing ``new`` rows at ``slots`` (appends extend)."""
+    size = old.shape[0]
+    grow = int(max([s + 1 for s in slots if s >= 0] + [size]))
+    out = np.concatenate([old, np.zeros((grow - size,) + old.shape[1:], dtype=old.dtype)])
+    for x, y in enumerate(slots):
+        if y >= 0:
+            out[y] = new[x]
+    return out

@@ -92,6 +92,7 @@ def test_null_handles_and_pointers_are_rejected():
     assert lib.fm_select_prefetch(None, None, None, 1, 1, None, None, C.byref(p), None, None, None) == L.FM_ERR_INVALID
     assert lib.fm_match_semantic(None, None, 1, 1, None, None, None, 0, None) == L.FM_ERR_INVALID
     assert lib.fm_match_trajectory(None, None, None, 1, 1, 1, None, None, None, 0, None) == L.FM_ERR_INVALID
+    assert lib.fm_store_insert_dedup(None, None, None, 1, 0, None, None, 0, None, 0, None) == L.FM_ERR_INVALID
     assert "NULL" in lib.fm_last_error().decode()
 
 
@@ -115,3 +116,15 @@ def test_scan_events_need_both_or_neither():
     assert lib.fm_debug_scan_events(C.c_void_p(0x1000), None) == L.FM_ERR_INVALID
     assert lib.fm_debug_scan_events(None, C.c_void_p(0x1000)) == L.FM_ERR_INVALID
     assert lib.fm_debug_scan_events(None, None) == L.FM_OK
+
+
+def test_dedup_scratch_size():
+    L, lib = _lib()
+    small = 2 * 4096 + 2 * 32768   # depth, slots, candidates and their scores for 1024 new iterations
+    # two dense float32 score matrices of n_max x cap, each 256-byte aligned
+    assert lib.fm_dedup_scratch_bytes(1000, 4) == small + 2 * 16128
+    assert lib.fm_dedup_scratch_bytes(100000, 256) == small + 2 * 102400000
+    assert lib.fm_dedup_scratch_bytes(1, 1) == small + 2 * 256
+    assert lib.fm_dedup_scratch_bytes(0, 4) == 0
+    assert lib.fm_dedup_scratch_bytes(10, 0) == 0
+    assert lib.fm_dedup_scratch_bytes(10, 1025) == 0

@@ -53,3 +53,23 @@ def test_geometric_depths_skew_shallow():
     d = synth.generate(s.scaled(n=64))["depth"]
     assert d.shape == (512,) and d.min() >= 1 and d.max() <= 31
     assert 4.5 < d.mean() < 9.0
+
+
+@pytest.mark.parametrize("cfg", [2, 3, 5])
+def test_new_iterations(cfg):
+    s = synth.spec(cfg).scaled(n=200, B_traj=0, B_sem=0)
+    a = synth.generate(s)
+    b = synth.generate_new(s, 64, a, dup_frac=0.25)
+    assert b["new_maps"].shape == (64, s.L, s.E) and b["new_maps"].dtype == a["maps"].dtype
+    dup = b["dup_src"]
+    assert 0 < int((dup >= 0).sum()) < 64
+    for x in np.flatnonzero(dup >= 0):
+        assert np.array_equal(b["new_maps"][x], a["maps"][dup[x]])
+        if s.d_emb:
+            assert np.array_equal(b["new_embs"][x], a["embs"][dup[x]])
+    p = synth.values_f32(b["new_maps"], s.map_dtype).astype(np.float64)
+    tol = s.E * (2.0 ** -8 if s.map_dtype == "bf16" else 2.0 ** -24)
+    assert np.max(np.abs(p.sum(-1) - 1.0)) <= tol
+    # deterministic
+    c = synth.generate_new(s, 64, a, dup_frac=0.25)
+    assert all(np.array_equal(b[k], c[k]) for k in b)
