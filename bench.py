@@ -15,6 +15,10 @@ timed by HIP events that the library records right around its launch on the
 stream it runs on (fm_debug_scan_events); ``match_call_us`` is the whole match
 call (staging, scan, merge).  ``cpu_baseline`` is the CPU oracle timed on a
 bounded sample of the same batch.
+
+``--path dedup`` measures the deduplicating insert instead (Section 4.4):
+batches of 256 new iterations into the full 100,000-entry store of d = 4096
+embeddings, prefetch distance 3; one step = one insert call.
 """
 from __future__ import annotations
 
@@ -105,6 +109,8 @@ def parse():
     p.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--path", default="match", choices=["match", "dedup"],
+                   help="match: search + selection (default); dedup: deduplicating inserts (Section 4.4)")
     p.add_argument("--copy-probe", action="store_true",
                    help="only copy 256 MiB device-to-device three times (reference for HBM traffic counters)")
     return p.parse_args()
@@ -157,6 +163,129 @@ def cpu_baseline(s, a, gpu_idx, budget_s):
             "top1_index_mismatches_vs_gpu": mism}
 
 
+# Deduplicating-insert workload: the Mixtral-shaped store with d = 4096
+# embeddings at capacity (100,000 iterations), batches of 256 new iterations
+# (one in eight an exact copy of a stored one), prefetch distance 3 (the
+# paper's setting for Mixtral, Section 6).
+DEDUP_CONFIG = 3
+DEDUP_BATCH = 256
+DEDUP_D = 3
+DEDUP_BATCHES = 8
+
+
+def dedup_cost(s, m):
+    """Algorithmic bytes and flops of one deduplicating insert of m new
+    iterations into a full store: every stored embedding and map is read once
+    and scored against every new iteration (the dense score matrices are this
+    implementation's choice and are not counted)."""
+    esz = 2 if s.map_dtype == "bf16" else 4
+    return {"sem_bytes": s.n * s.d_emb * 2 + 4 * s.n, "sem_flops": 2 * m * s.n * s.d_emb,
+            "traj_bytes": s.n * s.L * s.E * esz + 4 * s.n, "traj_flops": 2 * m * s.n * s.L * s.E}
+
+
+def dedup_cpu_baseline(s, a, b, d, gpu_slots, budget_s):
+    """Oracle RDY rows and victim choice for the first new iterations of the
+    batch (all of them find the store full), one at a time."""
+    import oracle
+    from threadpoolctl import threadpool_info
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    taken = np.zeros(s.n, dtype=bool)
+    t_total, rows, mism = 0.0, 0, 0
+    m = b["new_maps"].shape[0]
+    for x in range(m):
+        t0 = time.perf_counter()
+        r = oracle.redundancy(a["maps"], a["embs"], b["new_maps"][x:x + 1], b["new_embs"][x:x + 1], s.map_dtype, d)
+        cand = np.flatnonzero(~taken)
+        y = int(oracle.rank(r[0, cand], 1, cand)[0][0])
+        taken[y] = True
+        t_total += time.perf_counter() - t0
+        rows += 1
+        mism += int(y != int(gpu_slots[x]))
+        if t_total >= budget_s:
+            break
+    return {"value": rows / t_total, "unit": "new iterations/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{rows} of {m} new iterations against the full {s.n}-entry store (RDY row + victim), "
+                      "one at a time", "victim_mismatches_vs_gpu": mism}
+
+
+def bench_dedup(args):
+    import torch
+    import synth
+    import paper_2502_05370_amd as fm
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from parity import to_device
+
+    s = synth.spec(DEDUP_CONFIG).scaled(B_traj=0, B_sem=0)
+    a = synth.generate(s)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    store = fm.Store(s.n, s.L, s.E, s.d_emb, s.map_dtype, device=dev)
+    store.insert(to_device(a["maps"], s.map_dtype), to_device(a["embs"], "bf16"))
+    big = synth.generate_new(s, DEDUP_BATCH * DEDUP_BATCHES, a)
+    maps = to_device(big["new_maps"], s.map_dtype)
+    embs = to_device(big["new_embs"], "bf16")
+    batches = [(maps[i * DEDUP_BATCH:(i + 1) * DEDUP_BATCH], embs[i * DEDUP_BATCH:(i + 1) * DEDUP_BATCH])
+               for i in range(DEDUP_BATCHES)]
+    ws = fm.Workspace(store)
+    scratch = fm._aligned_bytes(fm.dedup_scratch_bytes(s.n, DEDUP_BATCH), dev)
+    stream = torch.cuda.current_stream()
+    hip = hip_runtime()
+    lib = fm._lib.load()
+    timer = ScanTimer(hip, lib, args.steps)
+
+    # the first batch against the untouched store, kept for the CPU baseline
+    first = store.insert_dedup(*batches[0], DEDUP_D, workspace=ws, scratch=scratch, stream=stream)
+    first = first.cpu().numpy()
+    for i in range(args.warmup):
+        store.insert_dedup(*batches[(i + 1) % DEDUP_BATCHES], DEDUP_D, workspace=ws, scratch=scratch, stream=stream)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        timer.arm(i)
+        store.insert_dedup(*batches[(i + 1 + args.warmup) % DEDUP_BATCHES], DEDUP_D, workspace=ws, scratch=scratch,
+                           stream=stream)
+        timer.disarm()
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    call_ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
+    scan_ms = timer.mean_ms(args.steps)
+
+    # the events bracket the last scan kernel of each call: the semantic one
+    cost = dedup_cost(s, DEDUP_BATCH)
+    byts, flops = cost["sem_bytes"], cost["sem_flops"]
+    dur_s = scan_ms * 1e-3
+    if flops / (BF16_MFMA_PEAK_TFS * 1e12) > byts / (HBM_PEAK_GBS * 1e9):
+        achieved = flops / dur_s / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": BF16_MFMA_PEAK_TFS, "unit": "TFLOP/s",
+                "frac": achieved / BF16_MFMA_PEAK_TFS}
+    else:
+        achieved = byts / dur_s / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS}
+    roof.update({"traffic": None, "kernel": "k_sem_scan", "mfma_dtype": "bf16", "duration_us": scan_ms * 1e3,
+                 "algorithmic_bytes": byts, "algorithmic_flops": flops, "call_us": call_ms * 1e3})
+    cpu = None
+    if not args.no_cpu_baseline:
+        b0 = {"new_maps": big["new_maps"][:DEDUP_BATCH], "new_embs": big["new_embs"][:DEDUP_BATCH]}
+        cpu = dedup_cpu_baseline(s, a, b0, DEDUP_D, first, args.cpu_seconds)
+    line = {
+        "metric": "new iterations/sec inserted with deduplication (RDY, Section 4.4) at 1 GPU",
+        "value": DEDUP_BATCH * args.steps / elapsed, "unit": "new iterations/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": elapsed / args.steps * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32+bf16",
+        "data": "synthetic",
+        "config": {"workload": f"dedup_semantic_d{s.d_emb}_n{s.n // 1000}k_b{DEDUP_BATCH}", "store_maps": s.n,
+                   "capacity": s.n, "layers": s.L, "experts": s.E, "map_dtype": s.map_dtype, "d_emb": s.d_emb,
+                   "batch": DEDUP_BATCH, "prefetch_distance": DEDUP_D},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -173,6 +302,9 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes": src.numel() * 4, "launches": 3}))
+        return
+    if args.path == "dedup":
+        bench_dedup(args)
         return
     import synth
     import paper_2502_05370_amd as fm

@@ -4,15 +4,17 @@
 // iteration y it is most redundant with,
 //     RDY[x][y] = (d/L) score_sem[x][y] + ((L-d)/L) score_traj[x][y],
 // with score_sem the Eq. 4 cosine of the embeddings and score_traj the Eq. 5
-// cosine over all L layers.  The two score matrices come from the semantic
-// and trajectory scan kernels in their dense-output form (same arithmetic
-// as the match calls).  Then
-//   k_rdy_partial   RDY of each (x, y), weighted in float64 and rounded once
-//                   to float32, and the 8 best y of each chunk of a row as
-//                   packed keys (RDY descending, y ascending, NaN last);
+// cosine over all L layers, both from the semantic and trajectory scan
+// kernels in their dense-output form (same arithmetic as the match calls).
+// The trajectory scan writes its scores, the semantic scan reads them in its
+// epilogue and writes the dense RDY matrix (weighted in float64, rounded once
+// to float32); with d = 0 or d = L only one scan runs and its scores are RDY.
+// Then
+//   k_rdy_partial   the 8 best y of each chunk of a row of RDY as packed
+//                   keys (RDY descending, y ascending, NaN last);
 //   k_finalize      (shared with the scans) merges the chunks of a row into
 //                   its 8 best candidates;
-//   k_dedup_assign  one workgroup takes the new iterations in batch order:
+//   k_dedup_assign  one wavefront takes the new iterations in batch order:
 //                   each takes its first candidate not yet taken by an
 //                   earlier one (the highest remaining RDY); if all 8 are
 //                   taken it rescans its whole row, skipping taken entries;
@@ -27,26 +29,16 @@ namespace {
 constexpr int kCand = 8;         // candidates kept per new iteration
 constexpr int kHashSlots = 4096;  // taken-set table (at most kChunkB entries)
 
-// RDY of one pair from the float32 scores; a term with weight 0 is not read.
-__device__ __forceinline__ float rdy_value(const float* S, const float* T, int64_t off, double w_sem,
-                                           double w_traj) {
-  double r = 0.0;
-  if (w_sem > 0.0) r = r + w_sem * static_cast<double>(S[off]);
-  if (w_traj > 0.0) r = r + w_traj * static_cast<double>(T[off]);
-  return static_cast<float>(r);
-}
-
 struct RdyArgs {
-  const float* S;      // [m][ld] semantic scores (unused when w_sem == 0)
-  const float* T;      // [m][ld] trajectory scores (unused when w_traj == 0)
-  int64_t ld;          // row stride = number of stored iterations scored
+  const float* rdy;    // [m][size] dense RDY
   int32_t size;        // stored iterations y in [0, size)
   int32_t m;           // new iterations (rows)
   int32_t R;           // chunks per row
-  int32_t per;         // y per chunk
-  double w_sem, w_traj;
+  int32_t per;         // y per chunk, a multiple of 256 * kUnroll
   uint64_t* partial;   // [m][R][kCand] packed keys
 };
+
+constexpr int kUnroll = 8;   // RDY values loaded per thread before they are ranked (sort8_desc)
 
 __global__ void __launch_bounds__(256) k_rdy_partial(RdyArgs a) {
   __shared__ uint64_t lists[256 / kWave][kCand];
@@ -56,11 +48,27 @@ __global__ void __launch_bounds__(256) k_rdy_partial(RdyArgs a) {
   const int w = threadIdx.x / kWave;
   const int lo = rr * a.per;
   const int hi = lo + a.per < a.size ? lo + a.per : a.size;
-  const int64_t row = static_cast<int64_t>(r) * a.ld;
+  const float* row = a.rdy + static_cast<int64_t>(r) * a.size;
   TopK<kCand> t;
   t.clear();
-  for (int y = lo + static_cast<int>(threadIdx.x); y < hi; y += 256)
-    t.push(make_key(rdy_value(a.S, a.T, row + y, a.w_sem, a.w_traj), y));
+  // batches of 8 values per thread: loaded together, sorted by a network and
+  // merged into the thread's list
+  for (int y0 = lo + static_cast<int>(threadIdx.x); y0 < hi; y0 += 256 * kUnroll) {
+    float v[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int y = y0 + 256 * u;
+      v[u] = y < hi ? row[y] : 0.0f;
+    }
+    uint64_t keys[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int y = y0 + 256 * u;
+      keys[u] = y < hi ? make_key(v[u], y) : 0ull;
+    }
+    sort8_desc(keys);
+    t.merge(keys);
+  }
   // lanes l and l ^ m hold lists of disjoint lane groups before each merge
 #pragma unroll
   for (int m = 1; m < kWave; m <<= 1) {
@@ -104,10 +112,7 @@ __device__ __forceinline__ void taken_add(int32_t* set, int32_t y) {
 
 struct AssignArgs {
   const int32_t* cand;   // [m][kCand] candidates in ranking order (-1: none)
-  const float* S;
-  const float* T;
-  int64_t ld;
-  double w_sem, w_traj;
+  const float* rdy;      // [m][size] dense RDY
   int32_t size;          // stored iterations before the batch
   int32_t n_app;         // new iterations appended at size, size + 1, ...
   int32_t m;             // new iterations that replace a stored one
@@ -115,40 +120,41 @@ struct AssignArgs {
   int32_t* slots_out;    // caller's copy, or null
 };
 
-__global__ void __launch_bounds__(256) k_dedup_assign(AssignArgs a) {
+// One wavefront: the candidate lists are staged in LDS, then the new
+// iterations are taken in batch order with the taken set in LDS (LDS
+// operations of one wave complete in issue order, so each step sees the
+// previous one's insert).
+__global__ void __launch_bounds__(kWave) k_dedup_assign(AssignArgs a) {
   __shared__ int32_t taken[kHashSlots];
-  __shared__ uint64_t red[256 / kWave];
-  __shared__ int32_t pick;
-  const int tid = threadIdx.x;
-  const int lane = tid % kWave;
-  const int w = tid / kWave;
-  for (int i = tid; i < kHashSlots; i += 256) taken[i] = -1;
-  for (int i = tid; i < a.n_app; i += 256) {
+  __shared__ int32_t cand[kChunkB * kCand];
+  __shared__ int32_t picked[kChunkB];
+  const int lane = threadIdx.x;
+  for (int i = lane; i < kHashSlots; i += kWave) taken[i] = -1;
+  if (a.size > 0)
+    for (int i = lane; i < a.m * kCand; i += kWave) cand[i] = a.cand[i];
+  for (int i = lane; i < a.n_app; i += kWave) {
     a.slots[i] = a.size + i;
     if (a.slots_out != nullptr) a.slots_out[i] = a.size + i;
   }
   __syncthreads();
   for (int r = 0; r < a.m; ++r) {
-    if (w == 0) {
-      int32_t y = -1;
-      bool ok = false;
-      if (lane < kCand && a.size > 0) {
-        y = a.cand[static_cast<int64_t>(r) * kCand + lane];
-        ok = y >= 0 && !taken_has(taken, y);
-      }
-      const uint64_t bal = __ballot(ok);
-      const int first = bal != 0 ? __builtin_ctzll(bal) : 0;
-      const int32_t yf = __shfl(y, first, kWave);
-      // -2: every candidate is taken, the row must be rescanned
-      if (lane == 0) pick = bal != 0 ? yf : (a.size > 0 ? -2 : -1);
+    int32_t y = -1;
+    bool ok = false;
+    if (lane < kCand && a.size > 0) {
+      y = cand[r * kCand + lane];
+      ok = y >= 0 && !taken_has(taken, y);
     }
-    __syncthreads();
-    if (pick == -2) {
+    const uint64_t bal = __ballot(ok);
+    int32_t pick;
+    if (bal != 0) {
+      pick = __shfl(y, __builtin_ctzll(bal), kWave);
+    } else if (a.size > 0) {
+      // every candidate is taken: rescan the whole row
       uint64_t best = 0;
-      const int64_t row = static_cast<int64_t>(r) * a.ld;
-      for (int y = tid; y < a.size; y += 256) {
-        if (taken_has(taken, y)) continue;
-        const uint64_t key = make_key(rdy_value(a.S, a.T, row + y, a.w_sem, a.w_traj), y);
+      const float* row = a.rdy + static_cast<int64_t>(r) * a.size;
+      for (int yy = lane; yy < a.size; yy += kWave) {
+        if (taken_has(taken, yy)) continue;
+        const uint64_t key = make_key(row[yy], yy);
         best = key > best ? key : best;
       }
 #pragma unroll
@@ -156,22 +162,19 @@ __global__ void __launch_bounds__(256) k_dedup_assign(AssignArgs a) {
         const uint64_t o = shfl_xor_u64(best, m);
         best = o > best ? o : best;
       }
-      if (lane == 0) red[w] = best;
-      __syncthreads();
-      if (tid == 0) {
-        uint64_t b = 0;
-#pragma unroll
-        for (int ww = 0; ww < 256 / kWave; ++ww) b = red[ww] > b ? red[ww] : b;
-        pick = key_index(b);
-      }
+      pick = key_index(best);
+    } else {
+      pick = -1;
     }
-    if (tid == 0) {
-      const int32_t y = pick;
-      if (y >= 0) taken_add(taken, y);
-      a.slots[a.n_app + r] = y;
-      if (a.slots_out != nullptr) a.slots_out[a.n_app + r] = y;
+    if (lane == 0) {
+      if (pick >= 0) taken_add(taken, pick);
+      picked[r] = pick;
     }
-    __syncthreads();
+  }
+  __syncthreads();
+  for (int i = lane; i < a.m; i += kWave) {
+    a.slots[a.n_app + i] = picked[i];
+    if (a.slots_out != nullptr) a.slots_out[a.n_app + i] = picked[i];
   }
 }
 
@@ -194,7 +197,7 @@ DedupScratch carve_dedup_scratch(void* base, int32_t cap, int32_t n_max) {
   d.cand_score = reinterpret_cast<float*>(p);
   p += align_up(sizeof(float) * kChunkB * kCand, kAlign);
   const size_t dense = align_up(sizeof(float) * static_cast<size_t>(n_max) * static_cast<size_t>(cap), kAlign);
-  d.sem = reinterpret_cast<float*>(p);
+  d.rdy = reinterpret_cast<float*>(p);
   p += dense;
   d.traj = reinterpret_cast<float*>(p);
   return d;
@@ -224,27 +227,33 @@ hipError_t launch_insert_dedup(const StoreView& s, const void* maps, const void*
       err = hipGetLastError();
       if (err != hipSuccess) return err;
       const char* q = static_cast<const char*>(maps) + static_cast<int64_t>(n_app) * s.L * s.E * esz;
-      err = launch_match_trajectory(s, q, sc.depth, s.L, m, 1, nullptr, nullptr, sc.traj, ws, st);
+      // trajectory scores alone are RDY when d = 0
+      err = launch_match_trajectory(s, q, sc.depth, s.L, m, 1, nullptr, nullptr, w_sem > 0.0 ? sc.traj : sc.rdy,
+                                    ws, st);
       if (err != hipSuccess) return err;
     }
     if (w_sem > 0.0) {
       const uint16_t* q = static_cast<const uint16_t*>(embs) + static_cast<int64_t>(n_app) * s.d_emb;
-      err = launch_match_semantic(s, q, m, 1, nullptr, nullptr, sc.sem, ws, st);
+      err = w_traj > 0.0 ? launch_match_semantic(s, q, m, 1, nullptr, nullptr, sc.rdy, ws, st, sc.traj, w_sem, w_traj)
+                         : launch_match_semantic(s, q, m, 1, nullptr, nullptr, sc.rdy, ws, st);
       if (err != hipSuccess) return err;
     }
     RdyArgs ra;
-    ra.S = sc.sem;
-    ra.T = sc.traj;
-    ra.ld = size;
+    ra.rdy = sc.rdy;
     ra.size = size;
     ra.m = m;
-    // chunks of at least 4096 stored iterations, at most kMaxPartials per row
-    int R = (size + 4095) / 4096;
-    if (R > kMaxPartials) R = kMaxPartials;
+    // chunks of 16384 stored iterations (a multiple of 256 * kUnroll), at
+    // most kMaxPartials per row
+    constexpr int kStep = 256 * kUnroll;
+    int per = 16384;
+    int R = (size + per - 1) / per;
+    if (R > kMaxPartials) {
+      R = kMaxPartials;
+      per = ((size + R - 1) / R + kStep - 1) / kStep * kStep;
+      R = (size + per - 1) / per;
+    }
     ra.R = R;
-    ra.per = (size + R - 1) / R;
-    ra.w_sem = w_sem;
-    ra.w_traj = w_traj;
+    ra.per = per;
     ra.partial = ws.partial;
     hipLaunchKernelGGL(k_rdy_partial, dim3(R, m), dim3(256), 0, st, ra);
     err = hipGetLastError();
@@ -255,17 +264,13 @@ hipError_t launch_insert_dedup(const StoreView& s, const void* maps, const void*
 
   AssignArgs aa;
   aa.cand = sc.cand;
-  aa.S = sc.sem;
-  aa.T = sc.traj;
-  aa.ld = size;
-  aa.w_sem = w_sem;
-  aa.w_traj = w_traj;
+  aa.rdy = sc.rdy;
   aa.size = size;
   aa.n_app = n_app;
   aa.m = m;
   aa.slots = sc.slots;
   aa.slots_out = slots_out;
-  hipLaunchKernelGGL(k_dedup_assign, dim3(1), dim3(256), 0, st, aa);
+  hipLaunchKernelGGL(k_dedup_assign, dim3(1), dim3(kWave), 0, st, aa);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   return launch_insert(s, maps, embs, n, sc.slots, nullptr, st);

@@ -115,12 +115,45 @@ struct TopK {
 #pragma unroll
     for (int j = 0; j < K; ++j) v[j] = nv[j];
   }
-  // Merge another sorted list; keeps the K largest.
+  // Merge another list sorted descending; keeps the K largest.  Bitonic:
+  // the elementwise maximum of this list and the other one reversed holds
+  // the K largest of both as a bitonic sequence, which a half-cleaner
+  // network then sorts.
   __device__ __forceinline__ void merge(const uint64_t* o) {
+    if constexpr (K == 1) {
+      v[0] = o[0] > v[0] ? o[0] : v[0];
+    } else {
 #pragma unroll
-    for (int j = 0; j < K; ++j) push(o[j]);
+      for (int j = 0; j < K; ++j) v[j] = o[K - 1 - j] > v[j] ? o[K - 1 - j] : v[j];
+#pragma unroll
+      for (int st = K / 2; st >= 1; st /= 2) {
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+          if ((j & st) == 0) {
+            const uint64_t hi = v[j] > v[j + st] ? v[j] : v[j + st];
+            const uint64_t lo = v[j] > v[j + st] ? v[j + st] : v[j];
+            v[j] = hi;
+            v[j + st] = lo;
+          }
+        }
+      }
+    }
   }
 };
+
+// Sort 8 keys descending in place (19-comparator network).
+__device__ __forceinline__ void sort8_desc(uint64_t* x) {
+  constexpr int kNet[19][2] = {{0, 2}, {1, 3}, {4, 6}, {5, 7}, {0, 4}, {1, 5}, {2, 6}, {3, 7}, {0, 1}, {2, 3},
+                               {4, 5}, {6, 7}, {2, 4}, {3, 5}, {1, 4}, {3, 6}, {1, 2}, {3, 4}, {5, 6}};
+#pragma unroll
+  for (int c = 0; c < 19; ++c) {
+    const int i = kNet[c][0], j = kNet[c][1];
+    const uint64_t hi = x[i] > x[j] ? x[i] : x[j];
+    const uint64_t lo = x[i] > x[j] ? x[j] : x[i];
+    x[i] = hi;
+    x[j] = lo;
+  }
+}
 
 
 }  // namespace fm

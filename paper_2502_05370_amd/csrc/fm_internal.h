@@ -72,8 +72,8 @@ struct DedupScratch {
   int32_t* slots;       // [kChunkB] slot of each new iteration (-1: dropped)
   int32_t* cand;        // [kChunkB][8] best replacement candidates
   float* cand_score;    // [kChunkB][8] their RDY
-  float* sem;           // [m][size] semantic scores
-  float* traj;          // [m][size] full-depth trajectory scores
+  float* rdy;           // [m][size] RDY (or the one weighted score when d is 0 or L)
+  float* traj;          // [m][size] full-depth trajectory scores (0 < d < L)
 };
 size_t dedup_scratch_bytes(int32_t cap, int32_t n_max);
 DedupScratch carve_dedup_scratch(void* base, int32_t cap, int32_t n_max);
@@ -99,9 +99,12 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
                                    int32_t max_depth, int32_t B, int32_t k, int32_t* idx_out,
                                    float* score_out, float* dbg_scores, const Workspace& ws,
                                    hipStream_t st);
+// With dbg_scores set, the dense scores are written there; with mix also set
+// (a dense [B][n] matrix), the dense output is w_self * score + w_mix * mix.
 hipError_t launch_match_semantic(const StoreView& s, const void* q, int32_t B, int32_t k,
                                  int32_t* idx_out, float* score_out, float* dbg_scores,
-                                 const Workspace& ws, hipStream_t st);
+                                 const Workspace& ws, hipStream_t st, const float* mix = nullptr,
+                                 double w_self = 1.0, double w_mix = 0.0);
 hipError_t launch_select(const StoreView& s, const int32_t* idx, const float* score, int32_t B,
                          int32_t k, const int32_t* lb, const int32_t* le,
                          const fm_select_params& p, uint64_t* mask_out, uint8_t* count_out,

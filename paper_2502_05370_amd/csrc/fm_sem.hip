@@ -45,6 +45,10 @@ struct SemArgs {
   int32_t grid;
   Workspace ws;
   float* dbg;            // optional dense scores [B][n]
+  // Optional second dense matrix [B][n]: when set, the dense output is the
+  // weighted sum w_self * score + w_mix * mix (float64, rounded once).
+  const float* mix;
+  double w_self, w_mix;
 };
 
 }  // namespace
@@ -266,7 +270,14 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
               if (y >= a.n) continue;
               const float rx = xn[i] > 0.0f ? 1.0f / xn[i] : (xn[i] != xn[i] ? xn[i] : 0.0f);
               const float s = acc[nb][t][i] * rq * rx;
-              if constexpr (DBG) a.dbg[static_cast<int64_t>(b) * a.n + y] = s;
+              if constexpr (DBG) {
+                const int64_t o = static_cast<int64_t>(b) * a.n + y;
+                float v = s;
+                if (a.mix != nullptr)
+                  v = static_cast<float>(__dadd_rn(__dmul_rn(a.w_self, static_cast<double>(s)),
+                                                   __dmul_rn(a.w_mix, static_cast<double>(a.mix[o]))));
+                a.dbg[o] = v;
+              }
               best[t].push(make_key(s, y));
             }
           }
@@ -357,14 +368,14 @@ hipError_t sem_launch(const SemArgs& a, hipStream_t st) {
   return hipEventRecord(ev.stop, st);
 }
 
-template <int KTOP>
+template <int KTOP, bool DBG = false>
 hipError_t sem_tq(int TQ, const SemArgs& a, hipStream_t st) {
   switch (TQ) {
-    case 1: return sem_launch<1, KTOP>(a, st);
-    case 2: return sem_launch<2, KTOP>(a, st);
-    case 4: return sem_launch<4, KTOP>(a, st);
+    case 1: return sem_launch<1, KTOP, DBG>(a, st);
+    case 2: return sem_launch<2, KTOP, DBG>(a, st);
+    case 4: return sem_launch<4, KTOP, DBG>(a, st);
     case 8:
-      if constexpr (sem_tq_limit(KTOP) >= 8) return sem_launch<8, KTOP>(a, st);
+      if constexpr (sem_tq_limit(KTOP) >= 8) return sem_launch<8, KTOP, DBG>(a, st);
       break;
     default: break;
   }
@@ -374,9 +385,11 @@ hipError_t sem_tq(int TQ, const SemArgs& a, hipStream_t st) {
 }  // namespace
 
 hipError_t launch_match_semantic(const StoreView& s, const void* q, int32_t B, int32_t k, int32_t* idx_out,
-                                 float* score_out, float* dbg_scores, const Workspace& ws, hipStream_t st) {
+                                 float* score_out, float* dbg_scores, const Workspace& ws, hipStream_t st,
+                                 const float* mix, double w_self, double w_mix) {
   const int KTOP = k == 1 ? 1 : (k <= 4 ? 4 : 8);
-  const int tq_max = dbg_scores != nullptr ? 1 : sem_tq_limit(KTOP);
+  // the dense-output form keeps top-1 lists (k = 1)
+  const int tq_max = sem_tq_limit(dbg_scores != nullptr ? 1 : KTOP);
   const int n_blocks = (s.n + 15) / 16;
   for (int b0 = 0; b0 < B; b0 += kChunkB) {
     const int Bc = (B - b0) < kChunkB ? (B - b0) : kChunkB;
@@ -417,7 +430,10 @@ hipError_t launch_match_semantic(const StoreView& s, const void* q, int32_t B, i
     a.grid = (n_qg * R + 7) / 8 * 8;
     a.ws = ws;
     a.dbg = dbg_scores != nullptr ? dbg_scores + static_cast<int64_t>(b0) * s.n : nullptr;
-    if (dbg_scores != nullptr) err = sem_launch<1, 1, true>(a, st);
+    a.mix = mix != nullptr ? mix + static_cast<int64_t>(b0) * s.n : nullptr;
+    a.w_self = w_self;
+    a.w_mix = w_mix;
+    if (dbg_scores != nullptr) err = sem_tq<1, true>(TQ, a, st);
     else if (KTOP == 1) err = sem_tq<1>(TQ, a, st);
     else if (KTOP == 4) err = sem_tq<4>(TQ, a, st);
     else err = sem_tq<8>(TQ, a, st);

@@ -17,10 +17,12 @@ __device__ __forceinline__ int64_t slot_for(int32_t first_slot, const int32_t* s
   return slot_of != nullptr ? static_cast<int64_t>(slot_of[i]) : static_cast<int64_t>(first_slot) + i;
 }
 
-// One wavefront per new map: each layer row is copied into its plane (with
-// zeros in the row padding), and the running float64 sum of squares over
-// layers 0..l gives the prefix inverse norm 1/|x[y][0:l+1]| that the
-// trajectory scan (Eq. 5) divides by at depth l+1.
+// One workgroup per new map; wave w handles layers w, w + 4, ... and lane e
+// expert e of a layer row (row <= 64).  Every row is copied into its plane
+// (with zeros in the row padding).  The float64 sum of squares of a layer is
+// a fixed-order tree reduction across the wave; the running sum over layers
+// 0..l, taken in layer order, gives the prefix inverse norm 1/|x[y][0:l+1]|
+// that the trajectory scan (Eq. 5) divides by at depth l+1.
 template <typename T>
 __global__ void __launch_bounds__(256) k_insert_maps(const T* __restrict__ src, T* __restrict__ planes,
                                                      int64_t plane_elems, float* __restrict__ rnorm,
@@ -28,52 +30,65 @@ __global__ void __launch_bounds__(256) k_insert_maps(const T* __restrict__ src, 
                                                      const int32_t* __restrict__ slot_of, int32_t n_new,
                                                      int32_t L, int32_t E, int32_t row,
                                                      int32_t* __restrict__ slots_out) {
+  constexpr int kLayersPerWave = kMaxL / 4;
+  __shared__ double sq[kMaxL];
   const int lane = threadIdx.x % kWave;
-  const int i = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
-  if (i >= n_new) return;
+  const int w = threadIdx.x / kWave;
+  const int i = blockIdx.x;
   const int64_t y = slot_for(first_slot, slot_of, i);
   if (y < 0) return;
-  double cum = 0.0;
-  for (int l = 0; l < L; ++l) {
-    double sq = 0.0;
-    for (int e = lane; e < row; e += kWave) {
-      T v = T(0);
-      if (e < E) v = src[(static_cast<int64_t>(i) * L + l) * E + e];
-      planes[l * plane_elems + tile_offset(y, e, row)] = v;
-      double f;
-      if constexpr (sizeof(T) == 2) f = static_cast<double>(bf16_to_f32(v));
-      else f = static_cast<double>(v);
-      sq += f * f;
-    }
-    // fixed-order tree reduction across the wave
+  // all loads first, then the stores and the per-layer reductions
+  T v[kLayersPerWave];
 #pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) sq += __shfl_xor(sq, m, kWave);
-    cum += sq;
-    if (lane == 0) {
+  for (int j = 0; j < kLayersPerWave; ++j) {
+    const int l = w + 4 * j;
+    v[j] = T(0);
+    if (l < L && lane < E) v[j] = src[(static_cast<int64_t>(i) * L + l) * E + lane];
+  }
+#pragma unroll
+  for (int j = 0; j < kLayersPerWave; ++j) {
+    const int l = w + 4 * j;
+    if (l >= L) break;
+    if (lane < row) planes[l * plane_elems + tile_offset(y, lane, row)] = v[j];
+    double f;
+    if constexpr (sizeof(T) == 2) f = static_cast<double>(bf16_to_f32(v[j]));
+    else f = static_cast<double>(v[j]);
+    double s2 = f * f;
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) s2 += __shfl_xor(s2, m, kWave);
+    if (lane == 0) sq[l] = s2;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double cum = 0.0;
+    for (int l = 0; l < L; ++l) {
+      cum += sq[l];
       float r;
       if (cum != cum) r = __uint_as_float(0x7fc00000u);
       else if (cum == 0.0) r = 0.0f;
       else r = static_cast<float>(1.0 / sqrt(cum));
       rnorm[l * rn_stride + y] = r;
     }
+    if (slots_out != nullptr) slots_out[i] = static_cast<int32_t>(y);
   }
-  if (slots_out != nullptr && lane == 0) slots_out[i] = static_cast<int32_t>(y);
 }
 
-// One wavefront per embedding row: copy it into the tiled layout
+// One workgroup per embedding row: copy it into the tiled layout
 // (emb_offset, 8 consecutive dimensions per 16-byte store) and compute its
-// norm.
+// norm (float64: each thread sums its chunks in order, then a fixed-order
+// tree across the wave and the 4 waves in order).
 __global__ void __launch_bounds__(256) k_insert_embs(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst,
                                                      float* __restrict__ norms, int32_t first_slot,
                                                      const int32_t* __restrict__ slot_of, int32_t n_new, int32_t d) {
+  __shared__ double part[4];
   const int lane = threadIdx.x % kWave;
-  const int row = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
-  if (row >= n_new) return;
+  const int w = threadIdx.x / kWave;
+  const int row = blockIdx.x;
   const uint16_t* s = src + static_cast<int64_t>(row) * d;
   const int64_t y = slot_for(first_slot, slot_of, row);
   if (y < 0) return;
   double acc = 0.0;
-  for (int j0 = 8 * lane; j0 < d; j0 += 8 * kWave) {
+  for (int j0 = 8 * static_cast<int>(threadIdx.x); j0 < d; j0 += 8 * 256) {
     const u16x8 h = *reinterpret_cast<const u16x8*>(s + j0);
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
@@ -82,17 +97,17 @@ __global__ void __launch_bounds__(256) k_insert_embs(const uint16_t* __restrict_
     }
     *reinterpret_cast<u16x8*>(dst + emb_offset(y, j0, d)) = h;
   }
-  // Fixed-order tree reduction across the wave.
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, kWave);
-  if (lane == 0) norms[y] = static_cast<float>(sqrt(acc));
+  if (lane == 0) part[w] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) norms[y] = static_cast<float>(sqrt(((part[0] + part[1]) + part[2]) + part[3]));
 }
 
 hipError_t launch_insert(const StoreView& s, const void* maps, const void* embs, int32_t n_new,
                          const int32_t* slot_of, int32_t* slots_out, hipStream_t st) {
   if (n_new <= 0) return hipSuccess;
-  const int rows_per_block = 256 / kWave;
-  const dim3 grid((n_new + rows_per_block - 1) / rows_per_block);
+  const dim3 grid(n_new);
   if (s.map_dtype == FM_F32) {
     hipLaunchKernelGGL(k_insert_maps<float>, grid, dim3(256), 0, st, static_cast<const float*>(maps),
                        static_cast<float*>(s.planes), s.plane_elems, s.rnorm, s.rn_stride, s.n, slot_of, n_new, s.L,
@@ -105,8 +120,8 @@ hipError_t launch_insert(const StoreView& s, const void* maps, const void* embs,
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   if (s.d_emb > 0) {
-    hipLaunchKernelGGL(k_insert_embs, dim3((n_new + rows_per_block - 1) / rows_per_block), dim3(256), 0, st,
-                       static_cast<const uint16_t*>(embs), s.embs, s.emb_norm, s.n, slot_of, n_new, s.d_emb);
+    hipLaunchKernelGGL(k_insert_embs, grid, dim3(256), 0, st, static_cast<const uint16_t*>(embs), s.embs,
+                       s.emb_norm, s.n, slot_of, n_new, s.d_emb);
     err = hipGetLastError();
   }
   return err;

@@ -749,27 +749,28 @@ constexpr int tq_limit(bool bf, int ksg, int ktop) {
 }
 
 // NBA (16-map blocks per wave) follows from TQ: 2 up to 4 query tiles, else 1.
-template <bool BF, int KSG, int KTOP, int TQ>
+template <bool BF, int KSG, int KTOP, int TQ, bool DBG>
 hipError_t scan_tq1(const ScanArgs& a, size_t lds, hipStream_t st) {
-  if constexpr (TQ <= tq_limit(BF, KSG, KTOP)) return scan_launch<BF, TQ, (TQ <= 4 ? 2 : 1), KSG, KTOP>(a, lds, st);
+  if constexpr (TQ <= tq_limit(BF, KSG, KTOP))
+    return scan_launch<BF, TQ, (TQ <= 4 ? 2 : 1), KSG, KTOP, DBG>(a, lds, st);
   return hipErrorInvalidValue;
 }
 
-template <bool BF, int KSG, int KTOP>
+template <bool BF, int KSG, int KTOP, bool DBG>
 hipError_t scan_tq(int TQ, const ScanArgs& a, size_t lds, hipStream_t st) {
   switch (TQ) {
-    case 1: return scan_tq1<BF, KSG, KTOP, 1>(a, lds, st);
-    case 2: return scan_tq1<BF, KSG, KTOP, 2>(a, lds, st);
-    case 4: return scan_tq1<BF, KSG, KTOP, 4>(a, lds, st);
-    case 8: return scan_tq1<BF, KSG, KTOP, 8>(a, lds, st);
-    case 16: return scan_tq1<BF, KSG, KTOP, 16>(a, lds, st);
+    case 1: return scan_tq1<BF, KSG, KTOP, 1, DBG>(a, lds, st);
+    case 2: return scan_tq1<BF, KSG, KTOP, 2, DBG>(a, lds, st);
+    case 4: return scan_tq1<BF, KSG, KTOP, 4, DBG>(a, lds, st);
+    case 8: return scan_tq1<BF, KSG, KTOP, 8, DBG>(a, lds, st);
+    case 16: return scan_tq1<BF, KSG, KTOP, 16, DBG>(a, lds, st);
     default: return hipErrorInvalidValue;
   }
 }
 
-template <bool BF, int KTOP>
+template <bool BF, int KTOP, bool DBG = false>
 hipError_t scan_ksg(int KSG, int TQ, const ScanArgs& a, size_t lds, hipStream_t st) {
-  return KSG == 1 ? scan_tq<BF, 1, KTOP>(TQ, a, lds, st) : scan_tq<BF, 2, KTOP>(TQ, a, lds, st);
+  return KSG == 1 ? scan_tq<BF, 1, KTOP, DBG>(TQ, a, lds, st) : scan_tq<BF, 2, KTOP, DBG>(TQ, a, lds, st);
 }
 
 }  // namespace
@@ -788,7 +789,8 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
   const bool bf = s.map_dtype == FM_BF16;
   const int esz = bf ? 2 : 4;
   const Geo geo = geometry(s.E);
-  const int KTOP = k == 1 ? 1 : (k <= 4 ? 4 : 8);
+  // the dense-output form keeps top-1 lists (k = 1)
+  const int KTOP = (k == 1 || dbg_scores != nullptr) ? 1 : (k <= 4 ? 4 : 8);
   const int tq_max = tq_limit(bf, geo.ksg, KTOP);
   constexpr size_t kLds = 160 * 1024;
 
@@ -796,7 +798,6 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
     const int Bc = (B - b0) < kChunkB ? (B - b0) : kChunkB;
     int TQ = 1;
     while (16 * TQ < Bc && TQ < tq_max) TQ *= 2;
-    if (dbg_scores != nullptr) TQ = 1;   // the dense-output variant exists for one shape only
     // smaller query groups when the staged planes of one would not fit the ring
     while (TQ > 1 && scan_lds(bf, TQ, geo.ksg, KTOP) > kLds) TQ /= 2;
     const int QG = 16 * TQ;
@@ -857,8 +858,7 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
     a.dbg = dbg_scores != nullptr ? dbg_scores + static_cast<int64_t>(b0) * s.n : nullptr;
     if (dbg_scores != nullptr) {
       // same arithmetic as the match kernels, plus the dense score stores
-      if (bf) err = geo.ksg == 1 ? scan_launch<true, 1, 2, 1, 1, true>(a, lds, st) : scan_launch<true, 1, 2, 2, 1, true>(a, lds, st);
-      else err = geo.ksg == 1 ? scan_launch<false, 1, 2, 1, 1, true>(a, lds, st) : scan_launch<false, 1, 2, 2, 1, true>(a, lds, st);
+      err = bf ? scan_ksg<true, 1, true>(geo.ksg, TQ, a, lds, st) : scan_ksg<false, 1, true>(geo.ksg, TQ, a, lds, st);
     } else if (bf) {
       err = KTOP == 1 ? scan_ksg<true, 1>(geo.ksg, TQ, a, lds, st)
           : KTOP == 4 ? scan_ksg<true, 4>(geo.ksg, TQ, a, lds, st)

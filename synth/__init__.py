@@ -26,8 +26,10 @@ round-to-nearest-even from float32.
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
 import dataclasses
 import hashlib
+import os
 from typing import Dict, Optional
 
 import numpy as np
@@ -55,11 +57,18 @@ def rng(config_no: int, stream: str) -> np.random.Generator:
 def bf16_bits(x: np.ndarray) -> np.ndarray:
     """float32 -> bf16 bit patterns (uint16), round to nearest, ties to even."""
     u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    nan = (u & 0x7FFFFFFF) > 0x7F800000
-    bias = ((u >> 16) & 1) + np.uint32(0x7FFF)
-    out = ((u + bias) >> 16).astype(np.uint16)
+    # in-place uint32 steps with uint32 constants (the same values as the
+    # plain expression, several times faster on large arrays)
+    r = u >> np.uint32(16)
+    r &= np.uint32(1)
+    r += np.uint32(0x7FFF)
+    r += u
+    r >>= np.uint32(16)
+    out = r.astype(np.uint16)
+    mag = u & np.uint32(0x7FFFFFFF)
+    nan = mag > np.uint32(0x7F800000)
     if nan.any():
-        out[nan] = ((u[nan] >> 16) | 0x40).astype(np.uint16)
+        out[nan] = ((u[nan] >> np.uint32(16)) | np.uint32(0x40)).astype(np.uint16)
     return out
 
 
@@ -172,14 +181,36 @@ def _emb_centroids(s: Spec) -> np.ndarray:
     return rng(s.config_no, "emb_centroids").standard_normal((s.emb_centroids, s.d_emb), dtype=np.float32)
 
 
+def _chunked(n: int, draw, finish) -> None:
+    """For chunks [a, b) of n rows in order: draw(a, b) in this thread (the
+    random streams are consumed in chunk order), finish(a, b, drawn) on a
+    worker thread (elementwise NumPy work, so the result does not depend on
+    the threads)."""
+    workers = max(1, min(8, os.cpu_count() or 1))
+    with cf.ThreadPoolExecutor(max_workers=workers) as ex:
+        pending = []
+        for a in range(0, n, _CHUNK):
+            b = min(a + _CHUNK, n)
+            pending.append(ex.submit(finish, a, b, draw(a, b)))
+            if len(pending) >= workers:
+                pending.pop(0).result()
+        for f in pending:
+            f.result()
+
+
 def _draw_embeddings(s: Spec, mu: np.ndarray, assign: np.ndarray, noise: np.random.Generator) -> np.ndarray:
     out = np.empty((assign.shape[0], s.d_emb), dtype=np.uint16)
-    for a in range(0, assign.shape[0], _CHUNK):
-        b = min(a + _CHUNK, assign.shape[0])
-        x = mu[assign[a:b]] + np.float32(s.emb_sigma) * noise.standard_normal((b - a, s.d_emb), dtype=np.float32)
+
+    def draw(a, b):
+        return noise.standard_normal((b - a, s.d_emb), dtype=np.float32)
+
+    def finish(a, b, eps):
+        x = mu[assign[a:b]] + np.float32(s.emb_sigma) * eps
         x = x.astype(np.float64)
         x /= np.linalg.norm(x, axis=1, keepdims=True)
         out[a:b] = bf16_bits(x.astype(np.float32))
+
+    _chunked(assign.shape[0], draw, finish)
     return out
 
 
@@ -209,10 +240,15 @@ def generate(s: Spec) -> Dict[str, np.ndarray]:
         cent = rng(s.config_no, "map_assign").integers(0, s.map_centroids, size=n)
     maps = np.empty((n, L, E), dtype=np.uint16 if s.map_dtype == BF16 else np.float32)
     noise = rng(s.config_no, "map_noise")
-    for a in range(0, n, _CHUNK):
-        b = min(a + _CHUNK, n)
-        z = Zc[cent[a:b]] + np.float32(s.map_sigma) * noise.standard_normal((b - a, L, E), dtype=np.float32)
+
+    def draw(a, b):
+        return noise.standard_normal((b - a, L, E), dtype=np.float32)
+
+    def finish(a, b, eps):
+        z = Zc[cent[a:b]] + np.float32(s.map_sigma) * eps
         maps[a:b] = _cast(_row_softmax_f32(z), s.map_dtype)
+
+    _chunked(n, draw, finish)
     out["maps"] = maps
 
     lb = []
