@@ -121,14 +121,17 @@ struct AssignArgs {
 };
 
 // One wavefront: the candidate lists are staged in LDS, then the new
-// iterations are taken in batch order with the taken set in LDS (LDS
-// operations of one wave complete in issue order, so each step sees the
-// previous one's insert).
+// iterations are taken in batch order with the taken set in LDS.  Lane j < 8
+// probes candidate j; the lane of the first candidate not taken writes it
+// into the empty slot its own probe ended on (one LDS round trip per step;
+// LDS operations of one wave complete in issue order, so each step sees the
+// previous one's write).  The next row's candidates are read a step ahead.
 __global__ void __launch_bounds__(kWave) k_dedup_assign(AssignArgs a) {
   __shared__ int32_t taken[kHashSlots];
   __shared__ int32_t cand[kChunkB * kCand];
   __shared__ int32_t picked[kChunkB];
   const int lane = threadIdx.x;
+  const bool reader = lane < kCand && a.size > 0;
   for (int i = lane; i < kHashSlots; i += kWave) taken[i] = -1;
   if (a.size > 0)
     for (int i = lane; i < a.m * kCand; i += kWave) cand[i] = a.cand[i];
@@ -137,17 +140,28 @@ __global__ void __launch_bounds__(kWave) k_dedup_assign(AssignArgs a) {
     if (a.slots_out != nullptr) a.slots_out[i] = a.size + i;
   }
   __syncthreads();
+  int32_t next = reader && a.m > 0 ? cand[lane] : -1;
   for (int r = 0; r < a.m; ++r) {
-    int32_t y = -1;
+    const int32_t y = next;
+    if (reader && r + 1 < a.m) next = cand[(r + 1) * kCand + lane];
     bool ok = false;
-    if (lane < kCand && a.size > 0) {
-      y = cand[r * kCand + lane];
-      ok = y >= 0 && !taken_has(taken, y);
+    int h = 0;
+    if (y >= 0) {
+      for (h = hash_slot(y);; h = (h + 1) & (kHashSlots - 1)) {
+        const int32_t v = taken[h];
+        if (v == y) break;
+        if (v < 0) {
+          ok = true;
+          break;
+        }
+      }
     }
     const uint64_t bal = __ballot(ok);
-    int32_t pick;
     if (bal != 0) {
-      pick = __shfl(y, __builtin_ctzll(bal), kWave);
+      if (lane == __builtin_ctzll(bal)) {
+        taken[h] = y;
+        picked[r] = y;
+      }
     } else if (a.size > 0) {
       // every candidate is taken: rescan the whole row
       uint64_t best = 0;
@@ -162,13 +176,13 @@ __global__ void __launch_bounds__(kWave) k_dedup_assign(AssignArgs a) {
         const uint64_t o = shfl_xor_u64(best, m);
         best = o > best ? o : best;
       }
-      pick = key_index(best);
-    } else {
-      pick = -1;
-    }
-    if (lane == 0) {
-      if (pick >= 0) taken_add(taken, pick);
-      picked[r] = pick;
+      const int32_t pick = key_index(best);
+      if (lane == 0) {
+        if (pick >= 0) taken_add(taken, pick);
+        picked[r] = pick;
+      }
+    } else if (lane == 0) {
+      picked[r] = -1;
     }
   }
   __syncthreads();
