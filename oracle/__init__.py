@@ -8,7 +8,8 @@ baseline leg of the benchmark use it.  It shares no code with the HIP path
 It is a plain, slow, obviously correct restatement of what the paper defines:
 
 * ``finemoe``  NumPy float64 implementation of semantic and trajectory cosine
-  search (Eq. 4, Eq. 5), ranking by highest score, the redundancy score and
+  search (Eq. 4, Eq. 5), ranking by highest score, the per-layer trajectory
+  re-search schedule of one pass (Section 4.2.2), the redundancy score and
   victim choice of store deduplication (Section 4.4), the optional
   similarity-weighted blend, the similarity-aware threshold of Section 4.3 and
   the minimum-cardinality prefetch set of Eq. 6-8.
@@ -22,6 +23,6 @@ invariants and brute force; none is "parity unpinned".
 from . import finemoe, brute  # noqa: F401
 from .finemoe import (  # noqa: F401
     widen, cosine, trajectory_scores, semantic_scores, rank, match_trajectory,
-    match_semantic, redundancy, dedup_slots, insert_dedup, threshold, select_row, blend_rows, select_prefetch,
+    match_semantic, research_schedule, redundancy, dedup_slots, insert_dedup, threshold, select_row, blend_rows, select_prefetch,
     TAU_FIXED, TAU_DYNAMIC, BLEND_NONE, BLEND_SCORE,
 )

@@ -157,6 +157,23 @@ def match_semantic(embs: np.ndarray, Qs: np.ndarray, k: int, n: int = None) -> T
     return out_i, out_s
 
 
+def research_schedule(maps: np.ndarray, dtype: str, Q: np.ndarray, k: int, d: int):
+    """The per-layer trajectory re-search of one pass (Section 4.2.2): the
+    prediction for target layer l in [d+1, L] (1-based) uses the trajectory
+    of layers 1 .. l-d, i.e. a search of prefix depth p = l - d for every
+    query.  Returns {l: (idx [B][k], score [B][k])} for l = d+1 .. L, each a
+    plain ``match_trajectory`` at that depth."""
+    n, L, E = maps.shape
+    if not 0 <= d < L:
+        raise ValueError(f"prefetch distance {d} outside [0, {L})")
+    B = Q.shape[0]
+    out = {}
+    for l in range(d + 1, L + 1):
+        p = l - d
+        out[l] = match_trajectory(maps, dtype, Q, np.full(B, p, dtype=np.int64), k)
+    return out
+
+
 # ---------------------------------------------------------------- store deduplication (Section 4.4)
 
 def redundancy(old_maps: np.ndarray, old_embs, new_maps: np.ndarray, new_embs, dtype: str,

@@ -275,6 +275,48 @@ def check_select_prefetch_layout(seed=11):
     assert mask[2, 4] == m and cnt[2, 4] == c
 
 
+# ------------------------------------------------------------------ per-layer re-search (Section 4.2.2)
+
+def check_research_schedule_depths():
+    """Target layer l uses layers 1 .. l-d: map 2 agrees with the query on
+    layer 1 only, map 1 on layers 1-2, map 0 on layers 1-3; each wins from
+    the layer whose prefix first tells it apart."""
+    L, E, d = 5, 4, 2
+    q = np.zeros((1, L, E), np.float32)
+    for l in range(L):
+        q[0, l, l % E] = 1.0
+    maps = np.zeros((3, L, E), np.float32)
+    for y, agree in enumerate((3, 2, 1)):
+        for l in range(L):
+            maps[y, l, l % E if l < agree else (l + 1) % E] = 1.0
+    res = F.research_schedule(maps, "f32", q, 3, d)
+    assert sorted(res) == list(range(d + 1, L + 1))
+    # p = 1: all three agree (score 1), lowest index first
+    assert list(res[d + 1][0][0]) == [0, 1, 2] and np.allclose(res[d + 1][1][0], 1.0)
+    # p = 2: maps 0 and 1 agree on both layers, map 2 on one of two
+    assert list(res[d + 2][0][0]) == [0, 1, 2]
+    assert abs(res[d + 2][1][0][2] - 0.5) <= 1e-15
+    # p = 3: only map 0 agrees on all three layers
+    assert res[d + 3][0][0][0] == 0 and abs(res[d + 3][1][0][1] - 2.0 / 3.0) <= 1e-15
+    assert abs(res[d + 3][1][0][2] - 1.0 / 3.0) <= 1e-15
+
+
+def check_research_schedule_vs_fsum(seed=17):
+    rng = np.random.default_rng(seed)
+    L, E, d = 6, 5, 1
+    maps = _rand_maps(rng, 9, L, E, zero_frac=0.2)
+    Q = _rand_maps(rng, 3, L, E)
+    res = F.research_schedule(maps, "f32", Q, 2, d)
+    assert len(res) == L - d
+    for l, (idx, sc) in res.items():
+        p = l - d
+        for b in range(3):
+            ref = [brute.cosine_fsum(F.widen(Q[b, :p], "f32").ravel(), F.widen(maps[y, :p], "f32").ravel())
+                   for y in range(9)]
+            assert list(idx[b]) == brute.best_matches(ref, 2), (l, b)
+            assert all(abs(sc[b][j] - ref[idx[b][j]]) <= 1e-14 for j in range(2))
+
+
 # ------------------------------------------------------------------ store deduplication (Section 4.4)
 
 def _bf16(x):
@@ -400,4 +442,5 @@ ALL_CHECKS = [
     check_select_vs_enumeration, check_select_nesting_and_minimality, check_blend,
     check_select_prefetch_layout, check_redundancy_vs_fsum, check_redundancy_closed_forms,
     check_dedup_vs_enumeration, check_dedup_duplicates, check_dedup_appends_first,
+    check_research_schedule_depths, check_research_schedule_vs_fsum,
 ]

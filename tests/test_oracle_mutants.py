@@ -191,6 +191,19 @@ def dedup_never_appends(rdy, size, cap):
     return _orig_dedup_slots(rdy, size, min(cap, size) if size > 0 else cap)
 
 
+_orig_research = F.research_schedule
+
+
+def research_one_layer_late(maps, dtype, Q, k, d):
+    return {l: F.match_trajectory(maps, dtype, Q, np.full(Q.shape[0], min(l - d + 1, maps.shape[1])), k)
+            for l in range(d + 1, maps.shape[1] + 1)}
+
+
+def research_all_layers(maps, dtype, Q, k, d):
+    return {l: F.match_trajectory(maps, dtype, Q, np.full(Q.shape[0], l), k)
+            for l in range(d + 1, maps.shape[1] + 1)}
+
+
 MUTANTS = [
     ("select_row", strict_threshold_select),
     ("select_row", high_index_first_select),
@@ -212,6 +225,8 @@ MUTANTS = [
     ("dedup_slots", dedup_reuses_victims),
     ("dedup_slots", dedup_least_redundant),
     ("dedup_slots", dedup_never_appends),
+    ("research_schedule", research_one_layer_late),
+    ("research_schedule", research_all_layers),
 ]
 
 
