@@ -19,6 +19,11 @@ bounded sample of the same batch.
 ``--path dedup`` measures the deduplicating insert instead (Section 4.4):
 batches of 256 new iterations into the full 100,000-entry store of d = 4096
 embeddings, prefetch distance 3; one step = one insert call.
+
+``--path step`` measures the incremental per-layer trajectory re-search
+(Section 4.2.2): 64 queries against the 50,000-map Qwen store, one step = one
+pass of L - d = 18 searches (prefix depths 1 .. 18), each an fm_traj_step
+call; the same searches as full re-scans are timed for reference.
 """
 from __future__ import annotations
 
@@ -109,8 +114,9 @@ def parse():
     p.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--path", default="match", choices=["match", "dedup"],
-                   help="match: search + selection (default); dedup: deduplicating inserts (Section 4.4)")
+    p.add_argument("--path", default="match", choices=["match", "dedup", "step"],
+                   help="match: search + selection (default); dedup: deduplicating inserts (Section 4.4); "
+                        "step: incremental per-layer trajectory re-search passes (Section 4.2.2)")
     p.add_argument("--copy-probe", action="store_true",
                    help="only copy 256 MiB device-to-device three times (reference for HBM traffic counters)")
     return p.parse_args()
@@ -286,6 +292,131 @@ def bench_dedup(args):
     print(json.dumps(line), flush=True)
 
 
+# Incremental re-search workload: the Qwen-shaped store (50,000 maps of
+# 24 x 60 float32) and 64 queries; one pass observes layers 1 .. L-d and
+# searches after each (d = 6, the paper's setting for Qwen, Section 6), i.e.
+# L - d = 18 searches at prefix depths 1 .. 18.
+STEP_CONFIG = 2
+STEP_D = 6
+
+
+def bench_step(args):
+    import torch
+    import synth
+    import paper_2502_05370_amd as fm
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from parity import to_device
+
+    s = synth.spec(STEP_CONFIG)
+    a = synth.generate(s)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    store = fm.Store(s.n, s.L, s.E, s.d_emb, s.map_dtype, device=dev)
+    store.insert(to_device(a["maps"], s.map_dtype))
+    B, n_layers = s.B_traj, s.L - STEP_D
+    q = to_device(a["q_traj"], s.map_dtype)
+    q_layers = [q[:, l].contiguous() for l in range(n_layers)]
+    ws = fm.Workspace(store)
+    tp = fm.TrajPass(store, B)
+    idx = torch.empty((B, s.k), dtype=torch.int32, device=dev)
+    score = torch.empty((B, s.k), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    hip = hip_runtime()
+    lib = fm._lib.load()
+    timer = ScanTimer(hip, lib, args.steps * n_layers)
+
+    def one_pass(i=None):
+        for l in range(n_layers):
+            if i is not None:
+                timer.arm(i * n_layers + l)
+            tp.step(q_layers[l], l, s.k, out=(idx, score), workspace=ws, stream=stream)
+        if i is not None:
+            timer.disarm()
+
+    for _ in range(args.warmup):
+        one_pass()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        one_pass(i)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    step_ms = timer.mean_ms(args.steps * n_layers)
+
+    # reference: the same searches as full re-scans (fm_match_trajectory at
+    # each depth), timed the same way
+    depths = [torch.full((B,), l + 1, dtype=torch.int32, device=dev) for l in range(n_layers)]
+
+    def rescan_pass():
+        for l in range(n_layers):
+            fm.match_trajectory(store, q, depths[l], s.k, max_depth=l + 1, out=(idx, score), workspace=ws,
+                                stream=stream)
+
+    rescan_pass()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for _ in range(args.steps):
+        rescan_pass()
+    torch.cuda.synchronize()
+    rescan_s = (time.perf_counter() - t1) / args.steps
+
+    # algorithmic cost of one step launch, averaged over the pass: the new
+    # layer's plane and inverse norms, and the running dots (written at the
+    # first layer, read and written after)
+    esz = 2 if s.map_dtype == "bf16" else 4
+    plane = s.n * s.E * esz + 4 * s.n
+    dots = [4 * B * s.n] + [8 * B * s.n] * (n_layers - 1)
+    byts = plane + float(np.mean(dots))
+    flops = 2 * B * s.n * s.E
+    dur_s = step_ms * 1e-3
+    if flops / (FP32_MFMA_PEAK_TFS * 1e12) > byts / (HBM_PEAK_GBS * 1e9):
+        achieved = flops / dur_s / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": FP32_MFMA_PEAK_TFS, "unit": "TFLOP/s",
+                "frac": achieved / FP32_MFMA_PEAK_TFS}
+    else:
+        achieved = byts / dur_s / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS}
+    roof.update({"traffic": None, "kernel": "k_traj_step", "mfma_dtype": "f32", "duration_us": step_ms * 1e3,
+                 "algorithmic_bytes": byts, "algorithmic_flops": flops,
+                 "pass_us": elapsed / args.steps * 1e6, "rescan_pass_us": rescan_s * 1e6})
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = step_cpu_baseline(s, a, n_layers, idx.cpu().numpy(), args.cpu_seconds)
+    line = {
+        "metric": "per-layer trajectory re-searches/sec (queries x searched layers, Section 4.2.2) at 1 GPU",
+        "value": B * n_layers * args.steps / elapsed, "unit": "query-layer searches/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": elapsed / args.steps * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"step_qwen_n{s.n // 1000}k_b{B}_d{STEP_D}", "store_maps": s.n, "layers": s.L,
+                   "experts": s.E, "map_dtype": s.map_dtype, "batch": B, "prefetch_distance": STEP_D,
+                   "searches_per_pass": n_layers, "top_k": s.k},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def step_cpu_baseline(s, a, n_layers, gpu_idx_last, budget_s):
+    """Oracle passes (Section 4.2.2 schedule: a search at every depth
+    1 .. L-d) for one query at a time."""
+    import oracle
+    from threadpoolctl import threadpool_info
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    t_total, done, mism = 0.0, 0, 0
+    for b in range(s.B_traj):
+        t0 = time.perf_counter()
+        res = oracle.research_schedule(a["maps"], s.map_dtype, a["q_traj"][b:b + 1], s.k, STEP_D)
+        t_total += time.perf_counter() - t0
+        done += 1
+        mism += int(res[s.L][0][0, 0] != gpu_idx_last[b, 0])
+        if t_total >= budget_s:
+            break
+    return {"value": done * n_layers / t_total, "unit": "query-layer searches/s", "cores": int(threads),
+            "kind": "oracle", "sample": f"{done} of {s.B_traj} queries, each a whole pass of {n_layers} searches "
+                                        f"against the full {s.n}-map store", "last_layer_mismatches_vs_gpu": mism}
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -305,6 +436,9 @@ def main():
         return
     if args.path == "dedup":
         bench_dedup(args)
+        return
+    if args.path == "step":
+        bench_step(args)
         return
     import synth
     import paper_2502_05370_amd as fm

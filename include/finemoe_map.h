@@ -72,6 +72,7 @@ typedef enum { FM_BLEND_NONE = 0, FM_BLEND_SCORE = 1 } fm_blend;
 /* Sticky device-side flags reported by fm_store_check. */
 #define FM_FLAG_DEPTH_CLAMPED 0x1u   /* a trajectory depth was outside [1, max_depth] and was clamped */
 #define FM_FLAG_INDEX_RANGE   0x2u   /* fm_select_prefetch met an index >= the store size (row skipped) */
+#define FM_FLAG_STATE_STALE   0x4u   /* fm_traj_step: the store size changed since layer 0, or layers out of order */
 
 typedef struct fm_store fm_store;   /* opaque host-side handle */
 
@@ -224,6 +225,36 @@ fm_status fm_select_prefetch(const fm_store* store, const int32_t* idx, const fl
                              const int32_t* layer_end, const fm_select_params* params,
                              uint64_t* mask_out, uint8_t* count_out, void* stream);
 
+/* Bytes of state (device memory owned by the caller, 256-byte aligned) for
+ * fm_traj_step passes of up to B_max queries (1..65536) on a store of
+ * capacity cap: per group of 64 queries a 1,280-byte header (store size at
+ * layer 0, last layer, float64 running query sums of squares in two slots)
+ * and the running float32 dot products of each query with each stored map
+ * (cap rounded up to 16, 4 query tiles of 16): 1,280 + 1,024 * ceil(cap / 16)
+ * * 4 bytes per group, each group 256-byte aligned.
+ * 0 for invalid arguments. */
+size_t fm_traj_state_bytes(int32_t cap, int32_t B_max);
+
+/* Incremental trajectory re-search (Section 4.2.2: after each newly observed
+ * layer the trajectory search runs again with the prefix grown by one layer).
+ * q_layer: device [B][E] of map_dtype, each query's gate probabilities at
+ * layer `layer` (0-based).  layer == 0 starts a pass and overwrites the
+ * state; every later call of the pass passes the next layer for the same B
+ * queries, in the same order, on an unchanged store.  The state keeps the
+ * running dot product of every (query, stored map) pair, so a step reads one
+ * layer plane of the store instead of layer + 1.  Outputs as for
+ * fm_match_trajectory with depth[b] = layer + 1 for every b (Eq. 5 over the
+ * first layer + 1 layers, float32 accumulation, rows of the store beyond its
+ * size at the call never ranked).  A step whose store size differs from the
+ * size at layer 0, or whose layer does not follow the previous one, sets
+ * FM_FLAG_STATE_STALE and its results are unspecified.  1 <= k <= 8,
+ * 1 <= B <= 65536, 0 <= layer < L.  Errors: FM_ERR_INVALID for NULL or
+ * misaligned pointers, out-of-range arguments, or a short state or
+ * workspace; nothing is enqueued then. */
+fm_status fm_traj_step(fm_store* store, void* state, size_t state_bytes, const void* q_layer, int32_t layer,
+                       int32_t B, int32_t k, int32_t* idx_out, float* score_out, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
 /* Test support: the dense float32 score matrix of a trajectory (q, depth
  * non-NULL) or semantic (q_sem non-NULL) search, written to scores_out device
  * [B][size] by the same kernels and arithmetic as the match calls.
@@ -235,9 +266,9 @@ fm_status fm_debug_scores(const fm_store* store, const void* q, const int32_t* d
 /* Measurement support: start and stop are hipEvent_t handles (passed as
  * void*) created by the caller, or both NULL to switch this off.  While set,
  * every match call made on this thread records start on its stream right
- * before the launch of its scan kernel (k_traj_scan or k_sem_scan) and stop
- * right after it, so the events bracket exactly that kernel (for a batch of
- * more than 1024 queries, the last chunk's).  The library does not own or
+ * before the launch of its scan kernel (k_traj_scan or k_sem_scan; k_traj_step
+ * for fm_traj_step) and stop right after it, so the events bracket exactly
+ * that kernel (for a batch of more than one launch, the last launch's).  The library does not own or
  * destroy the events.  FM_ERR_INVALID if exactly one of them is NULL. */
 fm_status fm_debug_scan_events(void* start, void* stop);
 

@@ -12,6 +12,8 @@ been built.
     slots = store.insert_dedup(maps, embs, d)           # Section 4.4, replaces when full
     idx, score = match_trajectory(store, q, depth, k=1) # Eq. 5
     idx, score = match_semantic(store, q_sem, k=1)      # Eq. 4
+    tp = TrajPass(store, B)                             # Section 4.2.2, one pass
+    idx, score = tp.step(q_layer, layer, k=1)           # after each observed layer
     mask, count = select_prefetch(store, idx, score, layer_begin, layer_end,
                                   tau=0.8, k_min=1, k_max=8)   # Eq. 6-8
 """
@@ -24,12 +26,13 @@ import torch
 
 from . import _lib
 from ._lib import (FM_BF16, FM_BLEND_NONE, FM_BLEND_SCORE, FM_F32, FM_FLAG_DEPTH_CLAMPED,  # noqa: F401
-                   FM_FLAG_INDEX_RANGE, FM_TAU_DYNAMIC, FM_TAU_FIXED, FmError, SelectParams)
+                   FM_FLAG_INDEX_RANGE, FM_FLAG_STATE_STALE, FM_TAU_DYNAMIC, FM_TAU_FIXED, FmError, SelectParams)
 
 _lib.load()
 
 __all__ = ["Store", "Workspace", "match_semantic", "match_trajectory", "select_prefetch", "debug_scores",
-           "map_bytes", "store_bytes", "workspace_bytes", "dedup_scratch_bytes", "FmError"]
+           "map_bytes", "store_bytes", "workspace_bytes", "dedup_scratch_bytes", "traj_state_bytes", "TrajPass",
+           "FmError"]
 
 _DTYPES = {"f32": FM_F32, "bf16": FM_BF16}
 _TORCH = {FM_F32: torch.float32, FM_BF16: torch.bfloat16}
@@ -176,6 +179,40 @@ class Store:
         if self.workspace is None:
             self.workspace = Workspace(self)
         return self.workspace
+
+
+def traj_state_bytes(cap: int, B_max: int) -> int:
+    return int(_lib.load().fm_traj_state_bytes(cap, B_max))
+
+
+class TrajPass:
+    """State of one incremental trajectory re-search pass (Section 4.2.2) of
+    B queries: call ``step`` with layer 0, 1, 2, ... as the layers are
+    observed; each step returns the Eq. 5 top-k at prefix depth layer + 1."""
+
+    def __init__(self, store: Store, B: int, device=None):
+        self.store, self.B = store, int(B)
+        self.nbytes = traj_state_bytes(store.cap, self.B)
+        if self.nbytes == 0:
+            raise ValueError(f"invalid pass size B={B}")
+        self.buf = _aligned_bytes(self.nbytes, store.device if device is None else device)
+
+    def step(self, q_layer: torch.Tensor, layer: int, k: int = 1,
+             out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None, workspace: Optional[Workspace] = None,
+             stream=None):
+        """q_layer [B][E] (store dtype): every query's gate probabilities at ``layer``."""
+        q_layer = q_layer.contiguous()
+        if tuple(q_layer.shape) != (self.B, self.store.E) or q_layer.dtype != _TORCH[self.store.dtype_code]:
+            raise ValueError(f"q_layer must be [{self.B}][{self.store.E}] {_TORCH[self.store.dtype_code]}")
+        if out is None:
+            out = (torch.empty((self.B, k), dtype=torch.int32, device=self.store.device),
+                   torch.empty((self.B, k), dtype=torch.float32, device=self.store.device))
+        idx, score = out
+        ws = _ws(self.store, workspace)
+        _lib.check(_lib.load().fm_traj_step(self.store.handle, C.c_void_p(self.buf.data_ptr()), self.nbytes,
+                                            _ptr(q_layer), int(layer), self.B, k, _ptr(idx), _ptr(score), ws.ptr,
+                                            ws.nbytes, _stream(stream)), "fm_traj_step")
+        return idx, score
 
 
 def _ws(store: Store, workspace: Optional[Workspace]) -> Workspace:

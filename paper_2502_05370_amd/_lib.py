@@ -18,6 +18,7 @@ FM_TAU_FIXED, FM_TAU_DYNAMIC = 0, 1
 FM_BLEND_NONE, FM_BLEND_SCORE = 0, 1
 FM_FLAG_DEPTH_CLAMPED = 0x1
 FM_FLAG_INDEX_RANGE = 0x2
+FM_FLAG_STATE_STALE = 0x4
 
 STATUS_NAMES = {0: "FM_OK", 1: "FM_ERR_INVALID", 2: "FM_ERR_UNSUPPORTED", 3: "FM_ERR_FULL",
                 4: "FM_ERR_HIP", 5: "FM_ERR_DEVICE"}
@@ -52,6 +53,8 @@ SIGNATURES = {
     "fm_match_semantic": (C.c_int, [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _sz, _vp]),
     "fm_match_trajectory": (C.c_int, [_vp, _vp, _vp, _i32, _i32, _i32, _vp, _vp, _vp, _sz, _vp]),
     "fm_select_prefetch": (C.c_int, [_vp, _vp, _vp, _i32, _i32, _vp, _vp, C.POINTER(SelectParams), _vp, _vp, _vp]),
+    "fm_traj_state_bytes": (_sz, [_i32, _i32]),
+    "fm_traj_step": (C.c_int, [_vp, _vp, _sz, _vp, _i32, _i32, _i32, _vp, _vp, _vp, _sz, _vp]),
     "fm_debug_scores": (C.c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _sz, _vp]),
     "fm_debug_scan_events": (C.c_int, [_vp, _vp]),
     "fm_last_error": (C.c_char_p, []),

@@ -306,7 +306,8 @@ fm_status fm_store_check(fm_store* s, void* stream, uint32_t* flags_out) {
   e = hipMemset(s->v.flags, 0, sizeof(uint32_t));
   if (e != hipSuccess) return hip_fail(e, "hipMemset(flags)");
   if (flags_out != nullptr) *flags_out = flags;
-  if (flags != 0) return fail(FM_ERR_DEVICE, "device flags 0x%x (1: depth clamped, 2: index out of range)", flags);
+  if (flags != 0)
+    return fail(FM_ERR_DEVICE, "device flags 0x%x (1: depth clamped, 2: index out of range, 4: stale step state)", flags);
   return ok();
 }
 
@@ -351,6 +352,31 @@ fm_status fm_match_trajectory(const fm_store* s, const void* q, const int32_t* d
   hipError_t e = fm::launch_match_trajectory(s->v, q, depth, max_depth, B, k, idx_out, score_out, nullptr,
                                              carve(s, ws), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "trajectory match launch");
+  return ok();
+}
+
+size_t fm_traj_state_bytes(int32_t cap, int32_t B_max) {
+  if (cap < 1 || B_max < 1 || B_max > 65536) return 0;
+  return fm::traj_state_bytes(cap, B_max);
+}
+
+fm_status fm_traj_step(fm_store* s, void* state, size_t state_bytes, const void* q, int32_t layer, int32_t B,
+                       int32_t k, int32_t* idx_out, float* score_out, void* ws, size_t ws_bytes, void* stream) {
+  if (fm_status st = check_match_common(s, B, k, idx_out, score_out, ws, ws_bytes)) return st;
+  if (q == nullptr) return fail(FM_ERR_INVALID, "q_layer is NULL");
+  if (layer < 0 || layer >= s->v.L) return fail(FM_ERR_INVALID, "layer=%d outside [0, L=%d)", layer, s->v.L);
+  if (state == nullptr) return fail(FM_ERR_INVALID, "state is NULL");
+  if (reinterpret_cast<uintptr_t>(state) % fm::kAlign != 0)
+    return fail(FM_ERR_INVALID, "state must be %zu-byte aligned", fm::kAlign);
+  const size_t need = fm::traj_state_bytes(s->v.cap, B);
+  if (state_bytes < need)
+    return fail(FM_ERR_INVALID, "state of %zu bytes is smaller than fm_traj_state_bytes(cap=%d, B=%d) = %zu",
+                state_bytes, s->v.cap, B, need);
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(FM_ERR_HIP, "cannot select the store's device %d", s->device);
+  hipError_t e = fm::launch_traj_step(s->v, state, q, layer, B, k, idx_out, score_out, carve(s, ws),
+                                      static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "trajectory step launch");
   return ok();
 }
 

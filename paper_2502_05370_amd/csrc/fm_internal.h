@@ -105,6 +105,9 @@ hipError_t launch_match_semantic(const StoreView& s, const void* q, int32_t B, i
                                  int32_t* idx_out, float* score_out, float* dbg_scores,
                                  const Workspace& ws, hipStream_t st, const float* mix = nullptr,
                                  double w_self = 1.0, double w_mix = 0.0);
+size_t traj_state_bytes(int32_t cap, int32_t B_max);
+hipError_t launch_traj_step(const StoreView& s, void* state, const void* q, int32_t layer, int32_t B, int32_t k,
+                            int32_t* idx_out, float* score_out, const Workspace& ws, hipStream_t st);
 hipError_t launch_select(const StoreView& s, const int32_t* idx, const float* score, int32_t B,
                          int32_t k, const int32_t* lb, const int32_t* le,
                          const fm_select_params& p, uint64_t* mask_out, uint8_t* count_out,

@@ -234,3 +234,51 @@ def apply_slots(old, new, slots, cap):
         if y >= 0:
             out[y] = new[x]
     return out
+
+
+# ---------------------------------------------------------------- incremental re-search (Section 4.2.2)
+
+def compare_topk(gpu_idx, gpu_score, orc_idx, orc_score, score_of) -> MatchReport:
+    """compare_match for any search: ``score_of(row, y)`` is the oracle's
+    float64 score of stored index y for query row."""
+    rep = MatchReport()
+    margin = 2 * SCORE_TOL
+    for r in range(orc_idx.shape[0]):
+        rep.checked += 1
+        gi, gs, oi, os_ = gpu_idx[r], gpu_score[r], orc_idx[r], orc_score[r]
+        k = oi.shape[0]
+        valid = [j for j in range(k) if oi[j] >= 0]
+        if list(gi[len(valid):]) != [-1] * (k - len(valid)):
+            rep.failures.append((r, "missing slots", list(gi), list(oi)))
+            continue
+        if len(set(int(x) for x in gi[:len(valid)])) != len(valid):
+            rep.failures.append((r, "duplicate indices", list(gi)))
+            continue
+        for j in valid:
+            y = int(gi[j])
+            ref = score_of(r, y)
+            if np.isnan(ref) and np.isnan(gs[j]):
+                continue
+            err = abs(gs[j] - ref)
+            rep.max_score_err = max(rep.max_score_err, float(err))
+            if not err <= SCORE_TOL:
+                rep.failures.append((r, j, "score", float(gs[j]), ref))
+            if y == oi[j]:
+                continue
+            if ref >= os_[j] - margin:
+                rep.near_ties += 1
+            else:
+                rep.failures.append((r, j, "index", y, int(oi[j]), ref, float(os_[j])))
+    return rep
+
+
+def compare_depth(maps, dtype, Q, p, gpu_idx, gpu_score, rows=None) -> MatchReport:
+    """GPU top-k of queries Q (all at prefix depth p) against the oracle."""
+    rows = np.arange(Q.shape[0]) if rows is None else np.asarray(rows)
+    k = gpu_idx.shape[1]
+    oi, os_ = oracle.match_trajectory(maps, dtype, Q[rows], np.full(len(rows), p), k)
+
+    def score_of(r, y):
+        return oracle.cosine(oracle.widen(Q[rows[r], :p], dtype), oracle.widen(maps[y, :p], dtype))
+
+    return compare_topk(gpu_idx[rows], gpu_score[rows], oi, os_, score_of)

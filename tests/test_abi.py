@@ -128,3 +128,15 @@ def test_dedup_scratch_size():
     assert lib.fm_dedup_scratch_bytes(0, 4) == 0
     assert lib.fm_dedup_scratch_bytes(10, 0) == 0
     assert lib.fm_dedup_scratch_bytes(10, 1025) == 0
+
+
+def test_traj_state_size():
+    L, lib = _lib()
+    # per group of 64 queries: 1,280-byte header + 4 KB per 16-map tile, 256-byte aligned
+    assert lib.fm_traj_state_bytes(50000, 64) == 1280 + 3125 * 4096
+    assert lib.fm_traj_state_bytes(50000, 65) == 2 * (1280 + 3125 * 4096)
+    assert lib.fm_traj_state_bytes(1, 1) == 1280 + 4096
+    assert lib.fm_traj_state_bytes(0, 1) == 0
+    assert lib.fm_traj_state_bytes(10, 0) == 0
+    assert lib.fm_traj_state_bytes(10, 65537) == 0
+    assert lib.fm_traj_step(None, None, 0, None, 0, 1, 1, None, None, None, 0, None) == L.FM_ERR_INVALID
