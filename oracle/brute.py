@@ -102,3 +102,26 @@ def dedup_by_enumeration(rdy: Sequence[Sequence[float]], size: int, cap: int) ->
             best, best_key = perm, key
     tail = list(best) if best is not None else []
     return head + tail + [-1] * (len(rest) - len(tail))
+
+
+def priority_list(p_rows: Sequence[Sequence[float]], bits: Sequence[int], pri_of) -> List[Tuple[float, int]]:
+    """Section 4.5 ordering by exhaustive comparison: every candidate (l, j)
+    with bit j of bits[l] set gets pri_of(l, j, p) with p its guiding
+    probability (a Python float rounded as the caller defines); a candidate
+    is placed after exactly
+    the candidates that beat it (larger priority, or equal and lower
+    l * E + j; NaN below every number)."""
+    E = len(p_rows[0])
+    cand = [(pri_of(l, j, float(p_rows[l][j])), l * E + j)
+            for l in range(len(bits)) for j in range(E) if (bits[l] >> j) & 1]
+
+    def beats(a, b):
+        an, bn = math.isnan(a[0]), math.isnan(b[0])
+        if an or bn:
+            return (not an and bn) or (an and bn and a[1] < b[1])
+        return a[0] > b[0] or (a[0] == b[0] and a[1] < b[1])
+
+    out = [None] * len(cand)
+    for c in cand:
+        out[sum(1 for d in cand if d is not c and beats(d, c))] = c
+    return out

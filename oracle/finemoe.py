@@ -344,16 +344,89 @@ def select_prefetch(maps: np.ndarray, dtype: str, idx: np.ndarray, score: np.nda
         if idx[b, 0] < 0:
             continue
         t = threshold(mode, tau, score[b, 0])
-        valid = [i for i in range(idx.shape[1]) if idx[b, i] >= 0]
         lo = max(0, int(lb[b]))
         hi = min(L, int(le[b]))
         for l in range(lo, hi):
-            if blend == BLEND_SCORE:
-                rows = np.stack([widen(maps[idx[b, i], l], dtype) for i in valid])
-                p = blend_rows(rows, [score[b, i] for i in valid])
-            else:
-                p = widen(maps[idx[b, 0], l], dtype)
+            p = guide_row(maps, dtype, idx[b], score[b], blend, l)
             m, c, _ = select_row(p, t, k_min, k_max)
             mask[b, l] = np.uint64(m)
             count[b, l] = c
     return mask, count
+
+
+def guide_row(maps: np.ndarray, dtype: str, idx_row: np.ndarray, score_row: np.ndarray, blend: int,
+              l: int) -> np.ndarray:
+    """The guiding probabilities of layer l for one query [E] (float64):
+    layer l of the best match idx_row[0] (BLEND_NONE), or the
+    similarity-weighted mean of layer l over the valid matches (BLEND_SCORE,
+    ``blend_rows``)."""
+    if blend == BLEND_SCORE:
+        valid = [i for i in range(len(idx_row)) if idx_row[i] >= 0]
+        rows = np.stack([widen(maps[idx_row[i], l], dtype) for i in valid])
+        return blend_rows(rows, [score_row[i] for i in valid])
+    return widen(maps[idx_row[0], l], dtype)
+
+
+# ---------------------------------------------------------------- prefetch and eviction priorities (Section 4.5)
+
+PRI_PREFETCH = 0
+PRI_EVICT = 1
+
+
+def priority_order(maps: np.ndarray, dtype: str, idx: np.ndarray, score: np.ndarray, blend: int, kind: int,
+                   masks: np.ndarray, l_now=None, freq=None, cap: int = None):
+    """Experts of each query in the order of the Section 4.5 priorities.
+
+    PRI_PREFETCH: the candidates are the experts j of the query's prefetch
+    set masks[b][l] (bit j) in the layers after the current one, l > l_now[b];
+    PRI = p_{l,j} / (l - l_now[b]).
+    PRI_EVICT: the candidates are the cached experts (masks[l], one mask per
+    layer for the cache); PRI = 1 / (p_{l,j} * freq[l][j]) with freq the
+    cache's visit counts.
+    p_{l,j} is the query's guiding probability (``guide_row``, as for the
+    selection).  PRI is computed in float64 and rounded to float32; the
+    candidates are ordered by PRI descending, lower l * E + j first on equal
+    values, NaN last.  A query without a match has no candidates.
+
+    Returns order [B][cap] int64 (l * E + j, -1 past the candidates), pri
+    [B][cap] float32 (-inf past the candidates) and count [B] (all candidates,
+    before the first ``cap`` are kept; cap defaults to L * E).
+    """
+    n, L, E = maps.shape
+    idx = np.asarray(idx, dtype=np.int64)
+    score = np.asarray(score, dtype=np.float64)
+    B = idx.shape[0]
+    cap = L * E if cap is None else cap
+    order = np.full((B, cap), -1, dtype=np.int64)
+    pri = np.full((B, cap), -np.inf, dtype=np.float32)
+    count = np.zeros(B, dtype=np.int64)
+    for b in range(B):
+        if idx[b, 0] < 0:
+            continue
+        cand = []
+        for l in range(L):
+            if kind == PRI_PREFETCH:
+                if l <= int(l_now[b]):
+                    continue
+                bits = int(masks[b, l])
+            else:
+                bits = int(masks[l])
+            if bits == 0:
+                continue
+            p = guide_row(maps, dtype, idx[b], score[b], blend, l)
+            for j in range(E):
+                if not (bits >> j) & 1:
+                    continue
+                with np.errstate(divide="ignore", invalid="ignore"):
+                    if kind == PRI_PREFETCH:
+                        v = np.float64(p[j]) / np.float64(l - int(l_now[b]))
+                    else:
+                        v = np.float64(1.0) / (np.float64(p[j]) * np.float64(np.float32(freq[l, j])))
+                cand.append((np.float32(v), l * E + j))
+        key = lambda c: (1, 0.0, c[1]) if np.isnan(c[0]) else (0, -float(c[0]), c[1])
+        cand.sort(key=key)
+        count[b] = len(cand)
+        for i, (v, e) in enumerate(cand[:cap]):
+            order[b, i] = e
+            pri[b, i] = v
+    return order, pri, count

@@ -435,6 +435,89 @@ def check_dedup_appends_first():
     assert 0 <= slots[0] < 3
 
 
+# ------------------------------------------------------------------ priorities (Section 4.5)
+
+def _f32(x):
+    return float(np.float32(x))
+
+
+def check_priority_closed_forms():
+    L, E = 4, 3
+    maps = np.zeros((1, L, E), np.float32)
+    maps[0, 1] = [0.5, 0.3, 0.2]
+    maps[0, 2] = [0.6, 0.25, 0.15]
+    maps[0, 3] = [0.4, 0.4, 0.2]
+    idx, score = np.array([[0]]), np.array([[0.9]])
+    full = (1 << E) - 1
+    masks = np.array([[full] * L], dtype=np.uint64)
+    # prefetch from layer 0: p / distance, layers 1, 2, 3 at distances 1, 2, 3
+    order, pri, cnt = F.priority_order(maps, "f32", idx, score, F.BLEND_NONE, F.PRI_PREFETCH, masks, l_now=[0])
+    assert cnt[0] == 9
+    exp = sorted([(_f32(maps[0, l, j] / (l - 0.0)), l * E + j) for l in (1, 2, 3) for j in range(E)],
+                 key=lambda t: (-t[0], t[1]))
+    assert [int(o) for o in order[0, :9]] == [e for _, e in exp]
+    # the nearest layer's 0.5 outranks the next layer's 0.6 (0.6 / 2 = 0.3)
+    assert order[0, 0] == 1 * E + 0 and abs(pri[0, 0] - 0.5) == 0.0
+    assert list(order[0, 9:]) == [-1] * (L * E - 9) and np.all(np.isneginf(pri[0, 9:]))
+    # equal priorities (layer 3: 0.4 and 0.4 at distance 3) keep expert order
+    pos = {int(e): i for i, e in enumerate(order[0, :9])}
+    assert pos[3 * E + 0] < pos[3 * E + 1]
+    # layers at or before the current one are never listed
+    order, pri, cnt = F.priority_order(maps, "f32", idx, score, F.BLEND_NONE, F.PRI_PREFETCH, masks, l_now=[2])
+    assert cnt[0] == 3 and set(int(e) for e in order[0, :3]) == {9, 10, 11}
+    assert abs(pri[0, 0] - _f32(0.4)) == 0.0
+    # eviction: 1 / (p * freq), least used and least likely first; zero use first of all
+    freq = np.ones((L, E), np.float32)
+    freq[2, 1] = 0.0
+    freq[1, 0] = 10.0
+    cache = np.array([0, 0b011, 0b110, 0], dtype=np.uint64)
+    order, pri, cnt = F.priority_order(maps, "f32", idx, score, F.BLEND_NONE, F.PRI_EVICT, cache, freq=freq)
+    assert cnt[0] == 4
+    assert int(order[0, 0]) == 2 * E + 1 and np.isposinf(pri[0, 0])
+    assert [int(e) for e in order[0, 1:4]] == [2 * E + 2, 1 * E + 1, 1 * E + 0]
+    assert abs(pri[0, 3] - _f32(1.0 / (0.5 * 10.0))) == 0.0
+    # a query without a match lists nothing; a cap keeps the first entries
+    order, pri, cnt = F.priority_order(maps, "f32", np.array([[-1]]), np.array([[-np.inf]]), F.BLEND_NONE,
+                                       F.PRI_PREFETCH, masks, l_now=[0], cap=2)
+    assert cnt[0] == 0 and list(order[0]) == [-1, -1]
+    order, pri, cnt = F.priority_order(maps, "f32", idx, score, F.BLEND_NONE, F.PRI_PREFETCH, masks, l_now=[0],
+                                       cap=2)
+    assert cnt[0] == 9 and [int(o) for o in order[0]] == [e for _, e in exp[:2]]
+
+
+def check_priority_vs_brute(seed=18):
+    rng = np.random.default_rng(seed)
+    for trial in range(40):
+        L, E, n, k = int(rng.integers(1, 6)), int(rng.integers(1, 9)), 5, 3
+        maps = _rand_maps(rng, n, L, E, zero_frac=0.3)
+        if trial % 3 == 0:
+            maps = np.round(maps * 4) / 4   # ties
+        if trial % 7 == 0:
+            maps[1, 0, 0] = np.nan
+        idx = rng.permutation(n)[:k][None, :]
+        score = np.sort(rng.uniform(-0.2, 1, k))[::-1][None, :]
+        blend = F.BLEND_SCORE if trial % 2 else F.BLEND_NONE
+        rows = [F.guide_row(maps, "f32", idx[0], score[0], blend, l) for l in range(L)]
+        masks = rng.integers(0, 1 << E, size=(1, L)).astype(np.uint64)
+        l_now = int(rng.integers(-1, L))
+        order, pri, cnt = F.priority_order(maps, "f32", idx, score, blend, F.PRI_PREFETCH, masks, l_now=[l_now])
+        bits = [int(masks[0, l]) if l > l_now else 0 for l in range(L)]
+        ref = brute.priority_list(rows, bits, lambda l, j, p: _f32(p / (l - l_now)))
+        assert cnt[0] == len(ref) and [int(o) for o in order[0, :cnt[0]]] == [e for _, e in ref], trial
+        freq = rng.integers(0, 4, size=(L, E)).astype(np.float32)
+        cache = rng.integers(0, 1 << E, size=L).astype(np.uint64)
+        order, pri, cnt = F.priority_order(maps, "f32", idx, score, blend, F.PRI_EVICT, cache, freq=freq)
+
+        def evict(l, j, p):
+            prod = p * float(freq[l, j])
+            return _f32(math.nan if math.isnan(prod) else (math.inf if prod == 0.0 else 1.0 / prod))
+
+        ref = brute.priority_list(rows, [int(c) for c in cache], evict)
+        assert cnt[0] == len(ref) and [int(o) for o in order[0, :cnt[0]]] == [e for _, e in ref], trial
+        got = pri[0, :cnt[0]]
+        assert all((math.isnan(a) and math.isnan(b)) or a == b for a, b in zip(got.tolist(), [v for v, _ in ref]))
+
+
 ALL_CHECKS = [
     check_cosine_vs_fsum, check_cosine_vs_torch, check_self_match, check_disjoint_support,
     check_depth_special_cases, check_unobserved_layers_ignored, check_semantic_vs_fsum,
@@ -443,4 +526,5 @@ ALL_CHECKS = [
     check_select_prefetch_layout, check_redundancy_vs_fsum, check_redundancy_closed_forms,
     check_dedup_vs_enumeration, check_dedup_duplicates, check_dedup_appends_first,
     check_research_schedule_depths, check_research_schedule_vs_fsum,
+    check_priority_closed_forms, check_priority_vs_brute,
 ]

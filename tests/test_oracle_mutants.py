@@ -204,6 +204,30 @@ def research_all_layers(maps, dtype, Q, k, d):
             for l in range(d + 1, maps.shape[1] + 1)}
 
 
+_orig_priority = F.priority_order
+
+
+def priority_distance_off_by_one(maps, dtype, idx, score, blend, kind, masks, l_now=None, freq=None, cap=None):
+    if kind == F.PRI_PREFETCH:
+        return _orig_priority(maps, dtype, idx, score, blend, kind, masks, l_now=[x - 1 for x in l_now], freq=freq,
+                              cap=cap)
+    return _orig_priority(maps, dtype, idx, score, blend, kind, masks, l_now=l_now, freq=freq, cap=cap)
+
+
+def priority_ascending(maps, dtype, idx, score, blend, kind, masks, l_now=None, freq=None, cap=None):
+    order, pri, cnt = _orig_priority(maps, dtype, idx, score, blend, kind, masks, l_now=l_now, freq=freq, cap=cap)
+    for b in range(order.shape[0]):
+        order[b, :cnt[b]] = order[b, :cnt[b]][::-1]
+        pri[b, :cnt[b]] = pri[b, :cnt[b]][::-1]
+    return order, pri, cnt
+
+
+def evict_by_ratio(maps, dtype, idx, score, blend, kind, masks, l_now=None, freq=None, cap=None):
+    if kind == F.PRI_EVICT:
+        freq = np.where(freq == 0, 0, 1.0 / np.where(freq == 0, 1, freq)).astype(np.float32)
+    return _orig_priority(maps, dtype, idx, score, blend, kind, masks, l_now=l_now, freq=freq, cap=cap)
+
+
 MUTANTS = [
     ("select_row", strict_threshold_select),
     ("select_row", high_index_first_select),
@@ -227,6 +251,9 @@ MUTANTS = [
     ("dedup_slots", dedup_never_appends),
     ("research_schedule", research_one_layer_late),
     ("research_schedule", research_all_layers),
+    ("priority_order", priority_distance_off_by_one),
+    ("priority_order", priority_ascending),
+    ("priority_order", evict_by_ratio),
 ]
 
 
