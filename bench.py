@@ -24,6 +24,9 @@ embeddings, prefetch distance 3; one step = one insert call.
 (Section 4.2.2): 64 queries against the 50,000-map Qwen store, one step = one
 pass of L - d = 18 searches (prefix depths 1 .. 18), each an fm_traj_step
 call; the same searches as full re-scans are timed for reference.
+
+``--path order`` measures the Section 4.5 prefetch ordering of a workload's
+selected sets (``--config``; one step = one fm_priority_order call).
 """
 from __future__ import annotations
 
@@ -114,9 +117,10 @@ def parse():
     p.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--path", default="match", choices=["match", "dedup", "step"],
+    p.add_argument("--path", default="match", choices=["match", "dedup", "step", "order"],
                    help="match: search + selection (default); dedup: deduplicating inserts (Section 4.4); "
-                        "step: incremental per-layer trajectory re-search passes (Section 4.2.2)")
+                        "step: incremental per-layer trajectory re-search passes (Section 4.2.2); "
+                        "order: prefetch priority ordering of the selected sets (Section 4.5)")
     p.add_argument("--copy-probe", action="store_true",
                    help="only copy 256 MiB device-to-device three times (reference for HBM traffic counters)")
     return p.parse_args()
@@ -417,6 +421,97 @@ def step_cpu_baseline(s, a, n_layers, gpu_idx_last, budget_s):
                                         f"against the full {s.n}-map store", "last_layer_mismatches_vs_gpu": mism}
 
 
+def bench_order(args):
+    """Section 4.5 prefetch ordering of workload ``--config``'s batch: the
+    matches and prefetch sets are computed once (resident), then each step
+    orders every query's set by p / (l - l_now) with l_now = the layer before
+    its first selected one."""
+    import torch
+    import synth
+    import paper_2502_05370_amd as fm
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from parity import to_device
+
+    s = synth.spec(args.config)
+    a = synth.generate(s)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    store = fm.Store(s.n, s.L, s.E, s.d_emb, s.map_dtype, device=dev)
+    store.insert(to_device(a["maps"], s.map_dtype), to_device(a["embs"], "bf16") if s.d_emb else None)
+    idx = torch.empty((s.B, s.k), dtype=torch.int32, device=dev)
+    score = torch.empty((s.B, s.k), dtype=torch.float32, device=dev)
+    max_depth = int(np.clip(a["depth"], 1, s.L).max()) if s.B_traj else s.L
+    if s.B_sem:
+        fm.match_semantic(store, to_device(a["q_sem"], "bf16"), s.k, out=(idx[:s.B_sem], score[:s.B_sem]))
+    if s.B_traj:
+        fm.match_trajectory(store, to_device(a["q_traj"], s.map_dtype), to_device(a["depth"], "i32"), s.k,
+                            max_depth=max_depth, out=(idx[s.B_sem:], score[s.B_sem:]))
+    mask, count = fm.select_prefetch(store, idx, score, to_device(a["lb"], "i32"), to_device(a["le"], "i32"),
+                                     tau=s.tau, k_min=s.k_min, k_max=s.k_max, mode=s.tau_mode, blend=s.blend)
+    l_now = to_device(a["lb"].astype(np.int32) - 1, "i32")
+    cap = s.L * s.E
+    out = (torch.empty((s.B, cap), dtype=torch.int32, device=dev), torch.empty((s.B, cap), dtype=torch.float32, device=dev),
+           torch.empty((s.B,), dtype=torch.int32, device=dev))
+    stream = torch.cuda.current_stream()
+
+    def order():
+        fm.priority_order(store, idx, score, mask, l_now=l_now, blend=s.blend, cap=cap, out=out, stream=stream)
+
+    for _ in range(args.warmup):
+        order()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        order()
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    call_ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
+    cnt = out[2].cpu().numpy()
+    # algorithmic bytes: the prefetch sets, each candidate's stored
+    # probabilities (k rows when blending) and the ordered lists written
+    esz = 2 if s.map_dtype == "bf16" else 4
+    k_rows = s.k if s.blend else 1
+    byts = s.B * s.L * 8 + int(cnt.sum()) * k_rows * esz + s.B * cap * 8
+    achieved = byts / (call_ms * 1e-3) / 1e9
+    roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+            "traffic": None, "kernel": "k_priority", "duration_us": call_ms * 1e3, "algorithmic_bytes": byts,
+            "candidates_per_query": float(cnt.mean())}
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+        gi, gs, gm = idx.cpu().numpy(), score.cpu().numpy(), mask.cpu().numpy().view(np.uint64)
+        ln = a["lb"].astype(np.int64) - 1
+        t_total, done, mism = 0.0, 0, 0
+        go = out[0].cpu().numpy()
+        for b in range(s.B):
+            t1 = time.perf_counter()
+            o, _, _ = oracle.priority_order(a["maps"], s.map_dtype, gi[b:b + 1], gs[b:b + 1], s.blend,
+                                            oracle.PRI_PREFETCH, gm[b:b + 1], l_now=ln[b:b + 1], cap=cap)
+            t_total += time.perf_counter() - t1
+            done += 1
+            mism += int(not np.array_equal(o[0], go[b]))
+            if t_total >= args.cpu_seconds:
+                break
+        cpu = {"value": done / t_total, "unit": "ordered queries/s", "cores": int(threads), "kind": "oracle",
+               "sample": f"{done} of {s.B} queries, one at a time", "order_mismatches_vs_gpu": mism}
+    line = {
+        "metric": "prefetch-ordered queries/sec (Section 4.5 priorities of the selected sets) at 1 GPU",
+        "value": s.B * args.steps / elapsed, "unit": "queries/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": elapsed / args.steps * 1e3, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"order_{s.name}", "store_maps": s.n, "layers": s.L, "experts": s.E, "batch": s.B,
+                   "list_capacity": cap},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -439,6 +534,9 @@ def main():
         return
     if args.path == "step":
         bench_step(args)
+        return
+    if args.path == "order":
+        bench_order(args)
         return
     import synth
     import paper_2502_05370_amd as fm

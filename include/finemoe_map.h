@@ -69,6 +69,9 @@ typedef enum { FM_TAU_FIXED = 0, FM_TAU_DYNAMIC = 1 } fm_tau_mode;
  * max(score, 0) (plain mean if every weight is 0). */
 typedef enum { FM_BLEND_NONE = 0, FM_BLEND_SCORE = 1 } fm_blend;
 
+/* Which Section 4.5 priority fm_priority_order ranks by. */
+typedef enum { FM_PRI_PREFETCH = 0, FM_PRI_EVICT = 1 } fm_pri_kind;
+
 /* Sticky device-side flags reported by fm_store_check. */
 #define FM_FLAG_DEPTH_CLAMPED 0x1u   /* a trajectory depth was outside [1, max_depth] and was clamped */
 #define FM_FLAG_INDEX_RANGE   0x2u   /* fm_select_prefetch met an index >= the store size (row skipped) */
@@ -224,6 +227,31 @@ fm_status fm_select_prefetch(const fm_store* store, const int32_t* idx, const fl
                              int32_t B, int32_t k, const int32_t* layer_begin,
                              const int32_t* layer_end, const fm_select_params* params,
                              uint64_t* mask_out, uint8_t* count_out, void* stream);
+
+/* Expert priorities of Section 4.5, one ordered list per query.
+ * FM_PRI_PREFETCH: the candidates are the experts of query b's prefetch set
+ * (masks: device [B][L] uint64 as written by fm_select_prefetch) in the
+ * layers after its current layer, l > l_now[b] (l_now: device [B] int32,
+ * 0-based; -1 lists every layer); PRI = p_{l,j} / (l - l_now[b]).
+ * FM_PRI_EVICT: the candidates are the cached experts (masks: device [L]
+ * uint64, bit j of layer l = expert cached, one mask for all queries);
+ * PRI = 1 / (p_{l,j} * freq[l][j]) with freq device [L][E] float32 visit
+ * counts (p * freq = 0 gives +inf).  p_{l,j} is the query's guiding
+ * probability, exactly as fm_select_prefetch computes it from idx/score/blend.
+ * PRI is computed in float64 and rounded to float32.  Each query's
+ * candidates are ordered by PRI descending, the lower l * E + j first on
+ * equal values, NaN last; the first cap are written: order_out device
+ * [B][cap] int32 (l * E + j, -1 past the candidates), pri_out device [B][cap]
+ * float32 (-inf past the candidates); count_out device [B] int32 receives
+ * the number of candidates.  A query whose idx[b][0] is -1 has none (an
+ * index >= the store size also sets FM_FLAG_INDEX_RANGE).  1 <= k <= 8,
+ * 1 <= B <= 65536, 1 <= cap <= 4096.  Errors: FM_ERR_INVALID for NULL
+ * pointers (l_now for PREFETCH, freq for EVICT) or out-of-range arguments;
+ * nothing is enqueued then. */
+fm_status fm_priority_order(const fm_store* store, const int32_t* idx, const float* score, int32_t B, int32_t k,
+                            fm_blend blend, fm_pri_kind kind, const uint64_t* masks, const int32_t* l_now,
+                            const float* freq, int32_t cap, int32_t* order_out, float* pri_out,
+                            int32_t* count_out, void* stream);
 
 /* Bytes of state (device memory owned by the caller, 256-byte aligned) for
  * fm_traj_step passes of up to B_max queries (1..65536) on a store of

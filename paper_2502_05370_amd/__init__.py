@@ -16,6 +16,7 @@ been built.
     idx, score = tp.step(q_layer, layer, k=1)           # after each observed layer
     mask, count = select_prefetch(store, idx, score, layer_begin, layer_end,
                                   tau=0.8, k_min=1, k_max=8)   # Eq. 6-8
+    order, pri, n = priority_order(store, idx, score, mask, l_now=l_now)  # Section 4.5
 """
 from __future__ import annotations
 
@@ -26,11 +27,12 @@ import torch
 
 from . import _lib
 from ._lib import (FM_BF16, FM_BLEND_NONE, FM_BLEND_SCORE, FM_F32, FM_FLAG_DEPTH_CLAMPED,  # noqa: F401
-                   FM_FLAG_INDEX_RANGE, FM_FLAG_STATE_STALE, FM_TAU_DYNAMIC, FM_TAU_FIXED, FmError, SelectParams)
+                   FM_FLAG_INDEX_RANGE, FM_FLAG_STATE_STALE, FM_PRI_EVICT, FM_PRI_PREFETCH, FM_TAU_DYNAMIC, FM_TAU_FIXED, FmError, SelectParams)
 
 _lib.load()
 
-__all__ = ["Store", "Workspace", "match_semantic", "match_trajectory", "select_prefetch", "debug_scores",
+__all__ = ["Store", "Workspace", "match_semantic", "match_trajectory", "select_prefetch", "priority_order",
+           "debug_scores",
            "map_bytes", "store_bytes", "workspace_bytes", "dedup_scratch_bytes", "traj_state_bytes", "TrajPass",
            "FmError"]
 
@@ -269,6 +271,26 @@ def select_prefetch(store: Store, idx: torch.Tensor, score: torch.Tensor, layer_
                                               _ptr(layer_end), C.byref(p), _ptr(mask), _ptr(count),
                                               _stream(stream)), "fm_select_prefetch")
     return mask, count
+
+
+def priority_order(store: Store, idx: torch.Tensor, score: torch.Tensor, masks: torch.Tensor,
+                   l_now: Optional[torch.Tensor] = None, freq: Optional[torch.Tensor] = None,
+                   kind: int = FM_PRI_PREFETCH, blend: int = FM_BLEND_NONE, cap: Optional[int] = None,
+                   out=None, stream=None):
+    """Section 4.5 priorities -> order [B][cap] int32 (l * E + j), pri [B][cap] float32, count [B] int32.
+    PREFETCH: masks [B][L] (int64 holding uint64 bits) from select_prefetch, l_now [B] int32.
+    EVICT: masks [L] (cached experts), freq [L][E] float32."""
+    B, k = idx.shape
+    cap = store.L * store.E if cap is None else int(cap)
+    if out is None:
+        out = (torch.empty((B, cap), dtype=torch.int32, device=store.device),
+               torch.empty((B, cap), dtype=torch.float32, device=store.device),
+               torch.empty((B,), dtype=torch.int32, device=store.device))
+    order, pri, count = out
+    _lib.check(_lib.load().fm_priority_order(store.handle, _ptr(idx), _ptr(score), B, k, blend, kind,
+                                             _ptr(masks.contiguous()), _ptr(l_now), _ptr(freq), cap, _ptr(order),
+                                             _ptr(pri), _ptr(count), _stream(stream)), "fm_priority_order")
+    return order, pri, count
 
 
 def debug_scores(store: Store, q: Optional[torch.Tensor] = None, depth: Optional[torch.Tensor] = None,

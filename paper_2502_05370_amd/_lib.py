@@ -16,6 +16,7 @@ FM_OK, FM_ERR_INVALID, FM_ERR_UNSUPPORTED, FM_ERR_FULL, FM_ERR_HIP, FM_ERR_DEVIC
 FM_F32, FM_BF16 = 0, 1
 FM_TAU_FIXED, FM_TAU_DYNAMIC = 0, 1
 FM_BLEND_NONE, FM_BLEND_SCORE = 0, 1
+FM_PRI_PREFETCH, FM_PRI_EVICT = 0, 1
 FM_FLAG_DEPTH_CLAMPED = 0x1
 FM_FLAG_INDEX_RANGE = 0x2
 FM_FLAG_STATE_STALE = 0x4
@@ -53,6 +54,8 @@ SIGNATURES = {
     "fm_match_semantic": (C.c_int, [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _sz, _vp]),
     "fm_match_trajectory": (C.c_int, [_vp, _vp, _vp, _i32, _i32, _i32, _vp, _vp, _vp, _sz, _vp]),
     "fm_select_prefetch": (C.c_int, [_vp, _vp, _vp, _i32, _i32, _vp, _vp, C.POINTER(SelectParams), _vp, _vp, _vp]),
+    "fm_priority_order": (C.c_int, [_vp, _vp, _vp, _i32, _i32, C.c_int, C.c_int, _vp, _vp, _vp, _i32, _vp, _vp, _vp,
+                                    _vp]),
     "fm_traj_state_bytes": (_sz, [_i32, _i32]),
     "fm_traj_step": (C.c_int, [_vp, _vp, _sz, _vp, _i32, _i32, _i32, _vp, _vp, _vp, _sz, _vp]),
     "fm_debug_scores": (C.c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _sz, _vp]),

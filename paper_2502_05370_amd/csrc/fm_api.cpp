@@ -355,6 +355,29 @@ fm_status fm_match_trajectory(const fm_store* s, const void* q, const int32_t* d
   return ok();
 }
 
+fm_status fm_priority_order(const fm_store* s, const int32_t* idx, const float* score, int32_t B, int32_t k,
+                            fm_blend blend, fm_pri_kind kind, const uint64_t* masks, const int32_t* l_now,
+                            const float* freq, int32_t cap, int32_t* order_out, float* pri_out, int32_t* count_out,
+                            void* stream) {
+  if (fm_status st = check_store(s)) return st;
+  if (idx == nullptr || score == nullptr || masks == nullptr || order_out == nullptr || pri_out == nullptr ||
+      count_out == nullptr)
+    return fail(FM_ERR_INVALID, "idx, score, masks, order_out, pri_out and count_out must be non-NULL");
+  if (B < 1 || B > 65536) return fail(FM_ERR_INVALID, "B=%d outside [1, 65536]", B);
+  if (k < 1 || k > fm::kMaxK) return fail(FM_ERR_INVALID, "k=%d outside [1, %d]", k, fm::kMaxK);
+  if (blend != FM_BLEND_NONE && blend != FM_BLEND_SCORE) return fail(FM_ERR_INVALID, "blend %d", blend);
+  if (kind != FM_PRI_PREFETCH && kind != FM_PRI_EVICT) return fail(FM_ERR_INVALID, "priority kind %d", kind);
+  if (kind == FM_PRI_PREFETCH && l_now == nullptr) return fail(FM_ERR_INVALID, "l_now is NULL");
+  if (kind == FM_PRI_EVICT && freq == nullptr) return fail(FM_ERR_INVALID, "freq is NULL");
+  if (cap < 1 || cap > fm::kMaxL * fm::kMaxE) return fail(FM_ERR_INVALID, "cap=%d outside [1, %d]", cap, fm::kMaxL * fm::kMaxE);
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(FM_ERR_HIP, "cannot select the store's device %d", s->device);
+  hipError_t e = fm::launch_priority(s->v, idx, score, B, k, blend, kind, masks, l_now, freq, cap, order_out,
+                                     pri_out, count_out, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "priority launch");
+  return ok();
+}
+
 size_t fm_traj_state_bytes(int32_t cap, int32_t B_max) {
   if (cap < 1 || B_max < 1 || B_max > 65536) return 0;
   return fm::traj_state_bytes(cap, B_max);

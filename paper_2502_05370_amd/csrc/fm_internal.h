@@ -105,6 +105,10 @@ hipError_t launch_match_semantic(const StoreView& s, const void* q, int32_t B, i
                                  int32_t* idx_out, float* score_out, float* dbg_scores,
                                  const Workspace& ws, hipStream_t st, const float* mix = nullptr,
                                  double w_self = 1.0, double w_mix = 0.0);
+hipError_t launch_priority(const StoreView& s, const int32_t* idx, const float* score, int32_t B, int32_t k,
+                           int32_t blend, int32_t kind, const uint64_t* masks, const int32_t* l_now,
+                           const float* freq, int32_t cap, int32_t* order_out, float* pri_out, int32_t* count_out,
+                           hipStream_t st);
 size_t traj_state_bytes(int32_t cap, int32_t B_max);
 hipError_t launch_traj_step(const StoreView& s, void* state, const void* q, int32_t layer, int32_t B, int32_t k,
                             int32_t* idx_out, float* score_out, const Workspace& ws, hipStream_t st);

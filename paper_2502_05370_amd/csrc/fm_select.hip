@@ -11,6 +11,7 @@
 //      is the first prefix reaching the threshold (E if none), clamped to
 //      [k_min, k_max]; the mask is the ballot of lanes with rank < k.
 #include "fm_device.h"
+#include "fm_guide.h"
 #include "fm_internal.h"
 
 namespace fm {
@@ -34,12 +35,6 @@ struct SelArgs {
   uint8_t* count_out;
   uint32_t* flags;
 };
-
-__device__ __forceinline__ double stored_prob(const SelArgs& a, int y, int l, int j) {
-  const int64_t off = static_cast<int64_t>(l) * a.plane_elems + tile_offset(y, j, a.row);
-  if (a.dtype == FM_F32) return static_cast<double>(static_cast<const float*>(a.planes)[off]);
-  return static_cast<double>(bf16_to_f32(static_cast<const uint16_t*>(a.planes)[off]));
-}
 
 // (p_i, i) is ahead of (p_j, j): larger probability, or equal and lower index;
 // NaN is behind every number and NaNs keep index order.
@@ -79,30 +74,11 @@ __global__ void __launch_bounds__(256) k_select(SelArgs a) {
   }
 
   // 1. guiding probability of expert `lane`
+  const GuideView gv{a.planes, a.plane_elems, a.n, a.row, a.dtype};
   double p = 0.0;
-  if (lane < a.E) {
-    if (a.blend == FM_BLEND_SCORE) {
-      double num = 0.0, den = 0.0;
-      bool any_pos = false;
-      for (int i = 0; i < a.k; ++i) {
-        int y = a.idx[static_cast<int64_t>(b) * a.k + i];
-        if (y < 0 || y >= a.n) continue;
-        double s = static_cast<double>(a.score[static_cast<int64_t>(b) * a.k + i]);
-        if (s > 0.0) any_pos = true;
-      }
-      for (int i = 0; i < a.k; ++i) {
-        int y = a.idx[static_cast<int64_t>(b) * a.k + i];
-        if (y < 0 || y >= a.n) continue;
-        double s = static_cast<double>(a.score[static_cast<int64_t>(b) * a.k + i]);
-        double wgt = any_pos ? (s > 0.0 ? s : 0.0) : 1.0;
-        num = __dadd_rn(num, __dmul_rn(wgt, stored_prob(a, y, l, lane)));
-        den = __dadd_rn(den, wgt);
-      }
-      p = __ddiv_rn(num, den);
-    } else {
-      p = stored_prob(a, y0, l, lane);
-    }
-  }
+  if (lane < a.E)
+    p = guide_prob(gv, a.idx + static_cast<int64_t>(b) * a.k, a.score + static_cast<int64_t>(b) * a.k, a.k, a.blend, l,
+                   lane);
 
   // 2. threshold
   double tau;
