@@ -12,8 +12,8 @@ It is a plain, slow, obviously correct restatement of what the paper defines:
   re-search schedule of one pass (Section 4.2.2), the redundancy score and
   victim choice of store deduplication (Section 4.4), the optional
   similarity-weighted blend, the similarity-aware threshold of Section 4.3,
-  the minimum-cardinality prefetch set of Eq. 6-8 and the prefetch and
-  eviction priorities of Section 4.5.
+  the minimum-cardinality prefetch set of Eq. 6-8, the prefetch and
+  eviction priorities of Section 4.5 and the miss indicator of Section 3.
 * ``brute``    pure-Python brute force with correctly rounded sums
   (``math.fsum``) and full subset enumeration, used to pin ``finemoe`` on
   tiny inputs.
@@ -24,6 +24,6 @@ invariants and brute force; none is "parity unpinned".
 from . import finemoe, brute  # noqa: F401
 from .finemoe import (  # noqa: F401
     widen, cosine, trajectory_scores, semantic_scores, rank, match_trajectory,
-    match_semantic, research_schedule, redundancy, dedup_slots, insert_dedup, threshold, select_row, blend_rows, select_prefetch, guide_row, priority_order,
+    match_semantic, research_schedule, redundancy, dedup_slots, insert_dedup, threshold, select_row, blend_rows, select_prefetch, guide_row, priority_order, activated, miss_counts,
     TAU_FIXED, TAU_DYNAMIC, BLEND_NONE, BLEND_SCORE, PRI_PREFETCH, PRI_EVICT,
 )

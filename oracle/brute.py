@@ -125,3 +125,16 @@ def priority_list(p_rows: Sequence[Sequence[float]], bits: Sequence[int], pri_of
     for c in cand:
         out[sum(1 for d in cand if d is not c and beats(d, c))] = c
     return out
+
+
+def misses_by_enumeration(p: Sequence[float], K: int, chosen: int) -> int:
+    """Activated experts outside the set ``chosen`` (a bit mask), with the
+    activated set found as the K-subset of largest fsum (ties: the subset
+    whose sorted indices come first), by enumeration (no NaN in p)."""
+    E = len(p)
+    best, best_key = None, None
+    for S in itertools.combinations(range(E), min(K, E)):
+        key = (-math.fsum(p[j] for j in S), sorted(S))
+        if best_key is None or key < best_key:
+            best, best_key = S, key
+    return sum(1 for j in best if not (chosen >> j) & 1)

@@ -367,6 +367,38 @@ def guide_row(maps: np.ndarray, dtype: str, idx_row: np.ndarray, score_row: np.n
     return widen(maps[idx_row[0], l], dtype)
 
 
+# ---------------------------------------------------------------- misses (Section 3, problem formulation)
+
+def activated(p: np.ndarray, K: int) -> int:
+    """The K experts a gate with probabilities p [E] activates: the K
+    highest (lower index first on equal values, NaN last), as a bit mask."""
+    p = np.asarray(p, dtype=np.float64)
+    E = p.shape[0]
+    nan = np.isnan(p)
+    order = np.lexsort((np.arange(E), -np.where(nan, 0.0, p), nan))
+    m = 0
+    for j in order[:K]:
+        m |= 1 << int(j)
+    return m
+
+
+def miss_counts(Q: np.ndarray, dtype: str, masks: np.ndarray, K: int, lb: np.ndarray, le: np.ndarray) -> np.ndarray:
+    """Misses of the prefetch sets (Section 3): R_{l,j} = 1 iff expert j of
+    layer l is activated and not in the set; summed over j for every query b
+    and layer l in [lb[b], le[b]) (clamped to [0, L]), 0 elsewhere.  The
+    activated experts are the top-K of the query's own gate probabilities
+    Q [B][L][E] at that layer (``activated``); masks [B][L] are the sets.
+    Returns [B][L] uint8."""
+    Q64 = widen(Q, dtype)
+    B, L, E = Q64.shape
+    out = np.zeros((B, L), dtype=np.uint8)
+    for b in range(B):
+        for l in range(max(0, int(lb[b])), min(L, int(le[b]))):
+            act = activated(Q64[b, l], K)
+            out[b, l] = bin(act & ~int(masks[b, l])).count("1")
+    return out
+
+
 # ---------------------------------------------------------------- prefetch and eviction priorities (Section 4.5)
 
 PRI_PREFETCH = 0

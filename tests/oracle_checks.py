@@ -518,6 +518,40 @@ def check_priority_vs_brute(seed=18):
         assert all((math.isnan(a) and math.isnan(b)) or a == b for a, b in zip(got.tolist(), [v for v, _ in ref]))
 
 
+# ------------------------------------------------------------------ misses (Section 3)
+
+def check_misses_closed_forms():
+    Q = np.array([[[0.5, 0.3, 0.1, 0.1], [0.25, 0.25, 0.25, 0.25]]], np.float32)
+    full = np.array([[0b1111, 0b1111]], np.uint64)
+    empty = np.zeros((1, 2), np.uint64)
+    lb, le = np.array([0]), np.array([2])
+    assert F.miss_counts(Q, "f32", full, 2, lb, le).tolist() == [[0, 0]]
+    assert F.miss_counts(Q, "f32", empty, 2, lb, le).tolist() == [[2, 2]]
+    # layer 0 activates {0, 1}; the set {0, 2} misses expert 1
+    assert F.miss_counts(Q, "f32", np.array([[0b0101, 0]], np.uint64), 2, lb, np.array([1])).tolist() == [[1, 0]]
+    # equal probabilities activate the lower indices {0, 1}
+    assert F.activated(Q[0, 1], 2) == 0b0011
+    assert F.miss_counts(Q, "f32", np.array([[0, 0b1100]], np.uint64), 2, np.array([1]), le).tolist() == [[0, 2]]
+    # K = E: every expert is activated
+    assert F.activated(Q[0, 0], 4) == 0b1111
+    assert F.activated(np.array([np.nan, 0.1, 0.2]), 1) == 0b100
+
+
+def check_misses_vs_enumeration(seed=19):
+    rng = np.random.default_rng(seed)
+    for _ in range(200):
+        E = int(rng.integers(1, 9))
+        K = int(rng.integers(1, E + 1))
+        p = rng.dirichlet(np.ones(E))
+        if rng.random() < 0.3:
+            p = np.round(p * 4) / 4
+        chosen = int(rng.integers(0, 1 << E))
+        Q = p.astype(np.float32)[None, None, :]
+        got = int(F.miss_counts(Q, "f32", np.array([[chosen]], np.uint64), K, np.array([0]), np.array([1]))[0, 0])
+        ref = brute.misses_by_enumeration(F.widen(Q[0, 0], "f32").tolist(), K, chosen)
+        assert got == ref, (p, K, chosen, got, ref)
+
+
 ALL_CHECKS = [
     check_cosine_vs_fsum, check_cosine_vs_torch, check_self_match, check_disjoint_support,
     check_depth_special_cases, check_unobserved_layers_ignored, check_semantic_vs_fsum,
@@ -527,4 +561,5 @@ ALL_CHECKS = [
     check_dedup_vs_enumeration, check_dedup_duplicates, check_dedup_appends_first,
     check_research_schedule_depths, check_research_schedule_vs_fsum,
     check_priority_closed_forms, check_priority_vs_brute,
+    check_misses_closed_forms, check_misses_vs_enumeration,
 ]

@@ -228,6 +228,18 @@ def evict_by_ratio(maps, dtype, idx, score, blend, kind, masks, l_now=None, freq
     return _orig_priority(maps, dtype, idx, score, blend, kind, masks, l_now=l_now, freq=freq, cap=cap)
 
 
+_orig_activated = F.activated
+
+
+def activated_high_index_first(p, K):
+    p = np.asarray(p, dtype=np.float64)
+    return int(bin(_orig_activated(p[::-1], K))[2:].zfill(len(p))[::-1], 2) if len(p) else 0
+
+
+def activated_one_short(p, K):
+    return _orig_activated(p, max(K - 1, 0))
+
+
 MUTANTS = [
     ("select_row", strict_threshold_select),
     ("select_row", high_index_first_select),
@@ -254,6 +266,8 @@ MUTANTS = [
     ("priority_order", priority_distance_off_by_one),
     ("priority_order", priority_ascending),
     ("priority_order", evict_by_ratio),
+    ("activated", activated_high_index_first),
+    ("activated", activated_one_short),
 ]
 
 
