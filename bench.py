@@ -27,6 +27,11 @@ call; the same searches as full re-scans are timed for reference.
 
 ``--path order`` measures the Section 4.5 prefetch ordering of a workload's
 selected sets (``--config``; one step = one fm_priority_order call).
+
+``--path capacity`` runs the store-capacity study (Section 6 sensitivity):
+mean best-match similarity, the misses of the selected sets and the full-map
+similarity at the sphere-covering sizes 2LJ and LJ ln(LJ) / 2 (Section 4.4),
+for stores of 1,000 .. 1,000,000 Qwen-shaped iterations.
 """
 from __future__ import annotations
 
@@ -117,10 +122,11 @@ def parse():
     p.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--path", default="match", choices=["match", "dedup", "step", "order"],
+    p.add_argument("--path", default="match", choices=["match", "dedup", "step", "order", "capacity"],
                    help="match: search + selection (default); dedup: deduplicating inserts (Section 4.4); "
                         "step: incremental per-layer trajectory re-search passes (Section 4.2.2); "
-                        "order: prefetch priority ordering of the selected sets (Section 4.5)")
+                        "order: prefetch priority ordering of the selected sets (Section 4.5); "
+                        "capacity: similarity and misses against store capacity (Section 6 sensitivity)")
     p.add_argument("--copy-probe", action="store_true",
                    help="only copy 256 MiB device-to-device three times (reference for HBM traffic counters)")
     return p.parse_args()
@@ -512,6 +518,147 @@ def bench_order(args):
     print(json.dumps(line), flush=True)
 
 
+# Capacity study: the Qwen-shaped bf16 store with d = 2048 embeddings
+# (workload 5's generator), read at growing capacities; 1024 fresh iterations
+# as queries (half by embedding, guiding layers 1..d; half by trajectory at
+# depth p ~ U{1..L-d}, guiding layer p + d), prefetch distance d = 6.
+CAP_CONFIG = 5
+CAP_D = 6
+CAP_SIZES = (1_000, 2_000, 2_880, 5_000, 5_236, 10_000, 20_000, 50_000, 100_000, 200_000, 500_000, 1_000_000)
+
+
+def bench_capacity(args):
+    import math
+    import torch
+    import synth
+    import paper_2502_05370_amd as fm
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from parity import to_device
+
+    s = synth.spec(CAP_CONFIG).scaled(B_traj=0, B_sem=0)
+    print("generating the store", file=sys.stderr, flush=True)
+    a = synth.generate(s)
+    m = 1024
+    new = synth.generate_new(s, m, a, dup_frac=0.0)
+    with open(os.path.join(ROOT, "tests", "golden", "models.json")) as f:
+        K = json.load(f)["models"]["qwen1.5_moe"]["K"]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    store = fm.Store(s.n, s.L, s.E, s.d_emb, s.map_dtype, device=dev)
+    maps, embs = to_device(a["maps"], s.map_dtype), to_device(a["embs"], "bf16")
+    h = m // 2
+    rng = np.random.default_rng(250205370)
+    depth = rng.integers(1, s.L - CAP_D + 1, size=m - h).astype(np.int32)
+    q_maps = to_device(new["new_maps"], s.map_dtype)
+    q_sem = to_device(new["new_embs"][:h], "bf16")
+    q_traj = q_maps[h:]
+    lb = np.concatenate([np.zeros(h, np.int32), depth + CAP_D - 1])
+    le = np.concatenate([np.full(h, CAP_D, np.int32), depth + CAP_D])
+    lbt, let = to_device(lb, "i32"), to_device(le, "i32")
+    depth_t = to_device(depth, "i32")
+    full_depth = torch.full((m,), s.L, dtype=torch.int32, device=dev)
+    ws = fm.Workspace(store)
+    idx = torch.empty((m, 1), dtype=torch.int32, device=dev)
+    score = torch.empty((m, 1), dtype=torch.float32, device=dev)
+    fidx = torch.empty((m, 1), dtype=torch.int32, device=dev)
+    fscore = torch.empty((m, 1), dtype=torch.float32, device=dev)
+    hip = hip_runtime()
+    lib = fm._lib.load()
+    rows = []
+    inserted = 0
+    for C in CAP_SIZES:
+        store.insert(maps[inserted:C], embs[inserted:C])
+        inserted = C
+        timer = ScanTimer(hip, lib, 2 * args.steps)
+        # one untimed search per capacity (launch shapes change with the size)
+        fm.match_semantic(store, q_sem, 1, out=(idx[:h], score[:h]), workspace=ws)
+        fm.match_trajectory(store, q_traj, depth_t, 1, max_depth=s.L - CAP_D, out=(idx[h:], score[h:]),
+                            workspace=ws)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            timer.arm(2 * i)
+            fm.match_semantic(store, q_sem, 1, out=(idx[:h], score[:h]), workspace=ws)
+            timer.arm(2 * i + 1)
+            fm.match_trajectory(store, q_traj, depth_t, 1, max_depth=s.L - CAP_D,
+                                out=(idx[h:], score[h:]), workspace=ws)
+            timer.disarm()
+        torch.cuda.synchronize()
+        match_s = (time.perf_counter() - t0) / args.steps
+        durs = []
+        for i in range(2 * args.steps):
+            ms = timer.C.c_float()
+            assert hip.hipEventElapsedTime(timer.C.byref(ms), *timer.pairs[i]) == 0
+            durs.append(ms.value)
+        sem_ms, traj_ms = float(np.mean(durs[0::2])), float(np.mean(durs[1::2]))
+        mask, _ = fm.select_prefetch(store, idx, score, lbt, let, tau=s.tau, k_min=s.k_min, k_max=s.k_max,
+                                     mode=s.tau_mode, blend=s.blend)
+        miss = fm.miss_count(store, q_maps, mask, K, lbt, let)
+        # the covering claim concerns whole maps: full-depth trajectory search
+        fm.match_trajectory(store, q_maps, full_depth, 1, max_depth=s.L, out=(fidx, fscore), workspace=ws)
+        torch.cuda.synchronize()
+        sc = score.cpu().numpy()[:, 0].astype(np.float64)
+        fsc = fscore.cpu().numpy()[:, 0].astype(np.float64)
+        n_rows = int((le - lb).sum())
+        rows.append({"capacity": C, "mean_semantic": float(sc[:h].mean()), "mean_trajectory": float(sc[h:].mean()),
+                     "mean_full_map": float(fsc.mean()), "min_full_map": float(fsc.min()),
+                     "hit_rate": 1.0 - float(miss.cpu().numpy().sum()) / (K * n_rows),
+                     "sem_scan_us": sem_ms * 1e3, "traj_scan_us": traj_ms * 1e3, "match_us": match_s * 1e6})
+        print(json.dumps(rows[-1]), file=sys.stderr, flush=True)
+    LJ = s.L * s.E
+    bound = {"LJ": LJ, "2LJ": 2 * LJ, "half_LJ_lnLJ": round(0.5 * LJ * math.log(LJ)),
+             "min_full_map_at_2LJ": next(r["min_full_map"] for r in rows if r["capacity"] == 2 * LJ),
+             "min_full_map_at_half_LJ_lnLJ": next(r["min_full_map"] for r in rows
+                                                  if r["capacity"] == round(0.5 * LJ * math.log(LJ)))}
+    last = rows[-1]
+    sem_bytes = s.n * s.d_emb * 2 + 4 * s.n
+    sem_flops = 2 * h * s.n * s.d_emb
+    dur_s = last["sem_scan_us"] * 1e-6
+    if sem_flops / (BF16_MFMA_PEAK_TFS * 1e12) > sem_bytes / (HBM_PEAK_GBS * 1e9):
+        achieved = sem_flops / dur_s / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": BF16_MFMA_PEAK_TFS, "unit": "TFLOP/s",
+                "frac": achieved / BF16_MFMA_PEAK_TFS}
+    else:
+        achieved = sem_bytes / dur_s / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS}
+    roof.update({"traffic": None, "kernel": "k_sem_scan", "mfma_dtype": "bf16", "duration_us": last["sem_scan_us"],
+                 "algorithmic_bytes": sem_bytes, "algorithmic_flops": sem_flops})
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+        t_total, done, mism = 0.0, 0, 0
+        gi = idx.cpu().numpy()
+        for b in range(h):
+            t1 = time.perf_counter()
+            oi, _ = oracle.match_semantic(a["embs"], new["new_embs"][b:b + 1], 1)
+            t_total += time.perf_counter() - t1
+            done += 1
+            mism += int(oi[0, 0] != gi[b, 0])
+            if t_total >= args.cpu_seconds:
+                break
+        cpu = {"value": done / t_total, "unit": "queries/s", "cores": int(threads), "kind": "oracle",
+               "sample": f"{done} semantic queries against the full {s.n}-entry store, one at a time",
+               "top1_index_mismatches_vs_gpu": mism}
+    line = {
+        "metric": "expert-map queries/sec at the largest store capacity, with similarity and misses vs capacity "
+                  "(Section 6 sensitivity)",
+        "value": m / (last["match_us"] * 1e-6), "unit": "queries/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": 0, "ms_per_step": last["match_us"] * 1e-3, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"capacity_qwen_bf16_d{s.d_emb}_to{s.n // 1000}k_b{m}", "layers": s.L,
+                   "experts": s.E, "K": K, "prefetch_distance": CAP_D, "queries": m,
+                   "capacities": list(CAP_SIZES)},
+        "study": rows,
+        "covering_bound": bound,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -537,6 +684,9 @@ def main():
         return
     if args.path == "order":
         bench_order(args)
+        return
+    if args.path == "capacity":
+        bench_capacity(args)
         return
     import synth
     import paper_2502_05370_amd as fm

@@ -228,6 +228,19 @@ fm_status fm_select_prefetch(const fm_store* store, const int32_t* idx, const fl
                              const int32_t* layer_end, const fm_select_params* params,
                              uint64_t* mask_out, uint8_t* count_out, void* stream);
 
+/* Misses of prefetch sets (Section 3: R_{l,j} = 1 iff expert j of layer l is
+ * activated and not cached).  q: device [B][L][E] of map_dtype, each query's
+ * own gate probabilities (the experts its layers actually route to); the
+ * activated experts of a row are its K highest (lower expert index first on
+ * equal values, NaN last), the cached ones its prefetch set (masks: device
+ * [B][L] uint64 as written by fm_select_prefetch).  miss_out: device [B][L]
+ * uint8, the number of activated experts outside the set for layers in
+ * [layer_begin[b], layer_end[b]) (clamped to [0, L]), 0 elsewhere.
+ * 1 <= K <= E, 1 <= B <= 65536.  Errors: FM_ERR_INVALID for NULL pointers or
+ * out-of-range arguments; nothing is enqueued then. */
+fm_status fm_miss_count(const fm_store* store, const void* q, int32_t B, int32_t K, const uint64_t* masks,
+                        const int32_t* layer_begin, const int32_t* layer_end, uint8_t* miss_out, void* stream);
+
 /* Expert priorities of Section 4.5, one ordered list per query.
  * FM_PRI_PREFETCH: the candidates are the experts of query b's prefetch set
  * (masks: device [B][L] uint64 as written by fm_select_prefetch) in the

@@ -32,6 +32,7 @@ from ._lib import (FM_BF16, FM_BLEND_NONE, FM_BLEND_SCORE, FM_F32, FM_FLAG_DEPTH
 _lib.load()
 
 __all__ = ["Store", "Workspace", "match_semantic", "match_trajectory", "select_prefetch", "priority_order",
+           "miss_count",
            "debug_scores",
            "map_bytes", "store_bytes", "workspace_bytes", "dedup_scratch_bytes", "traj_state_bytes", "TrajPass",
            "FmError"]
@@ -291,6 +292,19 @@ def priority_order(store: Store, idx: torch.Tensor, score: torch.Tensor, masks: 
                                              _ptr(masks.contiguous()), _ptr(l_now), _ptr(freq), cap, _ptr(order),
                                              _ptr(pri), _ptr(count), _stream(stream)), "fm_priority_order")
     return order, pri, count
+
+
+def miss_count(store: Store, q: torch.Tensor, masks: torch.Tensor, K: int, layer_begin: torch.Tensor,
+               layer_end: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Section 3 misses: activated experts (top-K of q [B][L][E], store dtype) outside the sets
+    masks [B][L] -> [B][L] uint8 for layers in [layer_begin, layer_end)."""
+    B = q.shape[0]
+    if out is None:
+        out = torch.empty((B, store.L), dtype=torch.uint8, device=store.device)
+    q = q.contiguous()
+    _lib.check(_lib.load().fm_miss_count(store.handle, _ptr(q), B, int(K), _ptr(masks), _ptr(layer_begin),
+                                         _ptr(layer_end), _ptr(out), _stream(stream)), "fm_miss_count")
+    return out
 
 
 def debug_scores(store: Store, q: Optional[torch.Tensor] = None, depth: Optional[torch.Tensor] = None,

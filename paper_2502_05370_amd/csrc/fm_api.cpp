@@ -355,6 +355,20 @@ fm_status fm_match_trajectory(const fm_store* s, const void* q, const int32_t* d
   return ok();
 }
 
+fm_status fm_miss_count(const fm_store* s, const void* q, int32_t B, int32_t K, const uint64_t* masks,
+                        const int32_t* lb, const int32_t* le, uint8_t* miss_out, void* stream) {
+  if (fm_status st = check_store(s)) return st;
+  if (q == nullptr || masks == nullptr || lb == nullptr || le == nullptr || miss_out == nullptr)
+    return fail(FM_ERR_INVALID, "q, masks, layer_begin, layer_end and miss_out must be non-NULL");
+  if (B < 1 || B > 65536) return fail(FM_ERR_INVALID, "B=%d outside [1, 65536]", B);
+  if (K < 1 || K > s->v.E) return fail(FM_ERR_INVALID, "K=%d outside [1, E=%d]", K, s->v.E);
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(FM_ERR_HIP, "cannot select the store's device %d", s->device);
+  hipError_t e = fm::launch_miss(s->v, q, B, K, masks, lb, le, miss_out, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "miss count launch");
+  return ok();
+}
+
 fm_status fm_priority_order(const fm_store* s, const int32_t* idx, const float* score, int32_t B, int32_t k,
                             fm_blend blend, fm_pri_kind kind, const uint64_t* masks, const int32_t* l_now,
                             const float* freq, int32_t cap, int32_t* order_out, float* pri_out, int32_t* count_out,

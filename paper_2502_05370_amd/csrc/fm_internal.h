@@ -105,6 +105,8 @@ hipError_t launch_match_semantic(const StoreView& s, const void* q, int32_t B, i
                                  int32_t* idx_out, float* score_out, float* dbg_scores,
                                  const Workspace& ws, hipStream_t st, const float* mix = nullptr,
                                  double w_self = 1.0, double w_mix = 0.0);
+hipError_t launch_miss(const StoreView& s, const void* q, int32_t B, int32_t K, const uint64_t* masks,
+                       const int32_t* lb, const int32_t* le, uint8_t* miss_out, hipStream_t st);
 hipError_t launch_priority(const StoreView& s, const int32_t* idx, const float* score, int32_t B, int32_t k,
                            int32_t blend, int32_t kind, const uint64_t* masks, const int32_t* l_now,
                            const float* freq, int32_t cap, int32_t* order_out, float* pri_out, int32_t* count_out,

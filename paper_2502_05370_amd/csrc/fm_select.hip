@@ -138,6 +138,70 @@ __global__ void __launch_bounds__(256) k_select(SelArgs a) {
   }
 }
 
+// Misses of the prefetch sets (Section 3): one wavefront per (query, layer)
+// row; lane j ranks expert j of the query's own gate probabilities among the
+// row (the same order as the selection), the K best are the activated
+// experts, and the count of those outside the set is written.
+struct MissArgs {
+  const void* q;           // [B][L][E] of the map dtype
+  fm_dtype dtype;
+  int32_t B, L, E, K;
+  const uint64_t* masks;   // [B][L]
+  const int32_t* lb;
+  const int32_t* le;
+  uint8_t* miss_out;       // [B][L]
+};
+
+__global__ void __launch_bounds__(256) k_miss(MissArgs a) {
+  __shared__ float vals[4][kMaxE];
+  const int lane = threadIdx.x % kWave;
+  const int wv = threadIdx.x / kWave;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + wv;
+  if (row >= static_cast<int64_t>(a.B) * a.L) return;
+  const int b = static_cast<int>(row / a.L);
+  const int l = static_cast<int>(row - static_cast<int64_t>(b) * a.L);
+  int lo = a.lb[b], hi = a.le[b];
+  lo = lo < 0 ? 0 : (lo > a.L ? a.L : lo);
+  hi = hi < 0 ? 0 : (hi > a.L ? a.L : hi);
+  if (l < lo || l >= hi) {
+    if (lane == 0) a.miss_out[row] = 0;
+    return;
+  }
+  float p = 0.0f;
+  if (lane < a.E) {
+    const int64_t i = row * a.E + lane;
+    p = a.dtype == FM_F32 ? static_cast<const float*>(a.q)[i] : bf16_to_f32(static_cast<const uint16_t*>(a.q)[i]);
+    vals[wv][lane] = p;
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_wave_barrier();
+  int rank = 0;
+  for (int i = 0; i < a.E; ++i) {
+    const float pi = vals[wv][i];
+    if (i != lane && ahead(pi, i, p, lane)) ++rank;
+  }
+  const uint64_t act = __ballot(lane < a.E && rank < a.K);
+  if (lane == 0) a.miss_out[row] = static_cast<uint8_t>(__popcll(act & ~a.masks[row]));
+}
+
+hipError_t launch_miss(const StoreView& s, const void* q, int32_t B, int32_t K, const uint64_t* masks,
+                       const int32_t* lb, const int32_t* le, uint8_t* miss_out, hipStream_t st) {
+  MissArgs a;
+  a.q = q;
+  a.dtype = s.map_dtype;
+  a.B = B;
+  a.L = s.L;
+  a.E = s.E;
+  a.K = K;
+  a.masks = masks;
+  a.lb = lb;
+  a.le = le;
+  a.miss_out = miss_out;
+  const int64_t rows = static_cast<int64_t>(B) * s.L;
+  hipLaunchKernelGGL(k_miss, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_select(const StoreView& s, const int32_t* idx, const float* score, int32_t B, int32_t k,
                          const int32_t* lb, const int32_t* le, const fm_select_params& p, uint64_t* mask_out,
                          uint8_t* count_out, hipStream_t st) {
