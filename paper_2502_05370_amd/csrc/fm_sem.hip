@@ -85,23 +85,24 @@ __global__ void __launch_bounds__(256) k_sem_prep(SemPrepArgs a) {
 
 // 8 waves; wave w owns NBA blocks of 16 maps of every slice.  Stage j =
 // (slice j / NKC, k-steps KS * (j % NKC) ..).  During stage j every wave loads
-// its share of the query tiles of stage j+2 into LDS slot (j+2) % 3 and, after
-// its MFMAs, the map tiles of stage j+2 into the registers stage j used.  Every
-// wave issues the same loads per stage (out-of-range offsets and a repeated
-// query tile keep the count fixed), so "stage j+1 has landed" is vmcnt <= the
-// loads of one stage at the end of stage j.  Slot (j+2) % 3 was last read in
-// stage j-1, which every wave finished before the barrier of stage j.
+// its share of the query tiles of stage j+3 into LDS slot (j+3) % 4 and, after
+// its MFMAs, the map tiles of stage j+3 into the registers stage j used (three
+// register sets rotate), so a load has two stages to land.  Every wave issues
+// the same loads per stage (out-of-range offsets and a repeated query tile keep
+// the count fixed), so "stage j+1 has landed" is vmcnt <= the loads of two
+// stages at the end of stage j.  Slot (j+3) % 4 was last read in stage j-1,
+// which every wave finished before the barrier of stage j.
 template <int TQ, int KTOP, bool DBG>
 __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
   constexpr int W = 8;                        // waves per workgroup
   constexpr int NBA = 2;                      // 16-map blocks per wave and slice
   constexpr int KS = 2;                       // k-steps (32 dimensions each) per stage
-  constexpr int NS = 3;                       // query ring slots
+  constexpr int NS = 4;                       // query ring slots
   constexpr int QG = 16 * TQ;                 // queries per group
   constexpr int NQ = TQ * KS;                 // 1 KB query tiles per stage
   constexpr int NI_Q = (NQ + W - 1) / W;      // query tile loads per wave and stage
   constexpr int Q_STAGE = NQ * 1024;
-  constexpr int NI_A = NBA * KS + NBA;        // map tile and map norm loads per wave and stage
+  constexpr int NI_A = NBA * KS + 1;          // map tile loads and one map norm load per wave and stage
   constexpr int NI = NI_A + NI_Q;
   static_assert(NI < 64, "vmcnt field is 6 bits");
 
@@ -146,11 +147,12 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
 
     // Map tiles: descriptor based at the slice's first block; rows past the
     // store and blocks past the range read as zeros.  The first stage of a
-    // slice also loads the slice's map norms (lane group g: maps 4g .. 4g+3
-    // of each block); the other stages issue the same loads out of range.
+    // slice also loads the slice's map norms (one per lane, shuffled to the
+    // lanes that need them in the epilogue); the other stages issue the same
+    // load out of range.
     const __amdgpu_buffer_rsrc_t rs_norm = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<float*>(a.xnorm), static_cast<short>(0), static_cast<int>(static_cast<uint32_t>(a.n) * 4u), kBufWord3);
-    auto load_a = [&](int j, u16x8 (&dst)[NBA][KS], floatx4 (&dxn)[NBA]) {
+    auto load_a = [&](int j, u16x8 (&dst)[NBA][KS], float& dxn) {
       const bool real = j < nstages;
       const int si = real ? j / NKC : 0;
       const int kc = real ? j % NKC : 0;
@@ -171,9 +173,11 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
           const uint32_t off = ok ? base_off + static_cast<uint32_t>(ks * 1024) : kOutside;
           dst[nb][ks] = __builtin_bit_cast(u16x8, __builtin_amdgcn_raw_buffer_load_b128(rs, static_cast<int>(off), 0, 0));
         }
-        const uint32_t noff = (real && kc == 0 && blk < b_end) ? static_cast<uint32_t>((16 * blk + 4 * g) * 4) : kOutside;
-        dxn[nb] = __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(rs_norm, static_cast<int>(noff), 0, 0));
       }
+      // lane l: the norm of map l % 16 of the wave's block (l / 16) % NBA
+      const int nblk = blk0 + w * NBA + (lane / 16) % NBA;
+      const uint32_t noff = (real && kc == 0 && nblk < b_end) ? static_cast<uint32_t>((16 * nblk + c) * 4) : kOutside;
+      dxn = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs_norm, static_cast<int>(noff), 0, 0));
     };
     // Query tiles of stage j: tile (t, ks) is 1 KB at slot offset (t*KS+ks) KB;
     // wave w loads tiles w, w+8, ... (wrapping: a repeated tile rewrites
@@ -198,22 +202,24 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
 #pragma unroll
       for (int t = 0; t < TQ; ++t) acc[nb][t] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    // issue order: Q0 A0 Q1 A1, then during stage j: Q(j+2) A(j+2)
-    u16x8 ar0[NBA][KS], ar1[NBA][KS];
-    floatx4 xr0[NBA], xr1[NBA];
+    // issue order: Q0 A0 Q1 A1 Q2 A2, then during stage j: Q(j+3) A(j+3)
+    u16x8 ar0[NBA][KS], ar1[NBA][KS], ar2[NBA][KS];
+    float xr0, xr1, xr2;
     load_q(0);
     load_a(0, ar0, xr0);
     load_q(1);
     load_a(1, ar1, xr1);
+    load_q(2);
+    load_a(2, ar2, xr2);
 
     // The map registers of a stage pass through an empty asm placed after
     // the wait for them, so no use of them is scheduled above it (the
     // compiler would then wait for every outstanding load itself, emptying
     // the prefetch).
     u16x8 cur[NBA][KS];
-    floatx4 xn_slice[NBA];
-    auto take = [&](int j, u16x8 (&ring_regs)[NBA][KS], floatx4 (&ring_xn)[NBA]) {
-      wait_vmcnt<NI>();
+    float xn_slice = 0.0f;
+    auto take = [&](int j, u16x8 (&ring_regs)[NBA][KS], float& ring_xn) {
+      wait_vmcnt<2 * NI>();
 #pragma unroll
       for (int nb = 0; nb < NBA; ++nb) {
 #pragma unroll
@@ -221,33 +227,46 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
           cur[nb][ks] = ring_regs[nb][ks];
           asm volatile("" : "+v"(cur[nb][ks]));
         }
-        if (j % NKC == 0) {
-          xn_slice[nb] = ring_xn[nb];
-          asm volatile("" : "+v"(xn_slice[nb]));
-        }
+      }
+      if (j % NKC == 0) {
+        xn_slice = ring_xn;
+        asm volatile("" : "+v"(xn_slice));
       }
     };
 
-    auto stage = [&](int j, u16x8 (&ring_regs)[NBA][KS], floatx4 (&ring_xn)[NBA], u16x8 (&next_regs)[NBA][KS],
-                     floatx4 (&next_xn)[NBA]) {
+    auto stage = [&](int j, u16x8 (&ring_regs)[NBA][KS], float& ring_xn, u16x8 (&next_regs)[NBA][KS],
+                     float& next_xn) {
       const int si = j / NKC;
       const int kc = j % NKC;
       const int blk_wave = b_begin + si * (W * NBA) + w * NBA;
       const unsigned char* sq = ring + (j % NS) * Q_STAGE;
 
       raw_barrier();
-      load_q(j + 2);
+      load_q(j + 3);
+      // The query tiles of a k-step land in registers of their own before
+      // its MFMAs (the empty asm keeps the compiler from reusing one register
+      // set per tile, which would serialise one LDS round trip per tile);
+      // the next k-step's reads are issued before this k-step's MFMAs.
+      u16x8 bq[KS][TQ];
+      auto read_q = [&](int ks) {
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        u16x8 bq[TQ];
+        for (int t = 0; t < TQ; ++t) bq[ks][t] = *reinterpret_cast<const u16x8*>(sq + (t * KS + ks) * 1024 + lane * 16);
+      };
+      auto pin_q = [&](int ks) {
 #pragma unroll
-        for (int t = 0; t < TQ; ++t) bq[t] = *reinterpret_cast<const u16x8*>(sq + (t * KS + ks) * 1024 + lane * 16);
+        for (int t = 0; t < TQ; ++t) asm volatile("" : "+v"(bq[ks][t]));
+      };
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) read_q(ks);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) pin_q(ks);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
         for (int t = 0; t < TQ; ++t)
 #pragma unroll
-          for (int nb = 0; nb < NBA; ++nb) acc[nb][t] = mfma_bf16(cur[nb][ks], bq[t], acc[nb][t]);
-      }
-      load_a(j + 2, ring_regs, ring_xn);
+          for (int nb = 0; nb < NBA; ++nb) acc[nb][t] = mfma_bf16(cur[nb][ks], bq[ks][t], acc[nb][t]);
+      load_a(j + 3, ring_regs, ring_xn);
 
       if (kc == NKC - 1) {
         // End of a slice: cosine = dot * 1/|q| * 1/|x|; lane (g, c) holds maps
@@ -256,7 +275,9 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
         for (int nb = 0; nb < NBA; ++nb) {
           const bool blk_ok = blk_wave + nb < b_end;
           const int y0 = 16 * (blk_wave + nb) + 4 * g;
-          const floatx4 xn = xn_slice[nb];
+          floatx4 xn;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) xn[i] = __shfl(xn_slice, nb * 16 + 4 * g + i, kWave);
           if (!blk_ok) continue;
 #pragma unroll
           for (int t = 0; t < TQ; ++t) {
@@ -292,11 +313,13 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
 
     take(0, ar0, xr0);
     int j = 0;
-    for (; j + 2 <= nstages; j += 2) {
+    for (; j + 3 <= nstages; j += 3) {
       stage(j, ar0, xr0, ar1, xr1);
-      stage(j + 1, ar1, xr1, ar0, xr0);
+      stage(j + 1, ar1, xr1, ar2, xr2);
+      stage(j + 2, ar2, xr2, ar0, xr0);
     }
     if (j < nstages) stage(j, ar0, xr0, ar1, xr1);
+    if (j + 1 < nstages) stage(j + 1, ar1, xr1, ar2, xr2);
     wait_vmcnt<0>();   // drain the trailing loads
     __syncthreads();
   }
@@ -337,12 +360,12 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
 namespace {
 
 // Largest query-tile count per workgroup for each list size (registers).
-constexpr int sem_tq_limit(int ktop) { return ktop == 8 ? 4 : 8; }
+constexpr int sem_tq_limit(int ktop) { return ktop == 1 ? 8 : 4; }
 
-// LDS: three query ring slots and the query norms; the merge buffer reuses
+// LDS: four query ring slots and the query norms; the merge buffer reuses
 // the ring.
 size_t sem_lds(int TQ, int KTOP) {
-  size_t ring = static_cast<size_t>(3) * TQ * 2 * 1024;
+  size_t ring = static_cast<size_t>(4) * TQ * 2 * 1024;
   const size_t merge = static_cast<size_t>(8) * 16 * TQ * KTOP * 8;
   if (merge > ring) ring = merge;
   return ring + static_cast<size_t>(16) * TQ * 4;
