@@ -76,6 +76,8 @@ typedef enum { FM_PRI_PREFETCH = 0, FM_PRI_EVICT = 1 } fm_pri_kind;
 #define FM_FLAG_DEPTH_CLAMPED 0x1u   /* a trajectory depth was outside [1, max_depth] and was clamped */
 #define FM_FLAG_INDEX_RANGE   0x2u   /* fm_select_prefetch met an index >= the store size (row skipped) */
 #define FM_FLAG_STATE_STALE   0x4u   /* fm_traj_step: the store size changed since layer 0, or layers out of order */
+#define FM_FLAG_VALUE_RANGE   0x8u   /* a float32 map or trajectory-query value exceeds 8 in magnitude (gate
+                                        probabilities lie in [0, 1]); float32 trajectory scores are then unspecified */
 
 typedef struct fm_store fm_store;   /* opaque host-side handle */
 

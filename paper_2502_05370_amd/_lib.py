@@ -20,6 +20,7 @@ FM_PRI_PREFETCH, FM_PRI_EVICT = 0, 1
 FM_FLAG_DEPTH_CLAMPED = 0x1
 FM_FLAG_INDEX_RANGE = 0x2
 FM_FLAG_STATE_STALE = 0x4
+FM_FLAG_VALUE_RANGE = 0x8
 
 STATUS_NAMES = {0: "FM_OK", 1: "FM_ERR_INVALID", 2: "FM_ERR_UNSUPPORTED", 3: "FM_ERR_FULL",
                 4: "FM_ERR_HIP", 5: "FM_ERR_DEVICE"}

@@ -9,6 +9,7 @@ namespace fm {
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 halfx8 __attribute__((ext_vector_type(8)));
 
 typedef uint32_t uint32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t uint32x2 __attribute__((ext_vector_type(2)));
@@ -53,6 +54,11 @@ __device__ __forceinline__ void dma16(const void* src, void* lds_base) {
 __device__ __forceinline__ floatx4 mfma_bf16(const u16x8& a, const u16x8& b, floatx4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
                                                  0, 0, 0);
+}
+
+__device__ __forceinline__ floatx4 mfma_f16(const u16x8& a, const u16x8& b, floatx4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(halfx8, a), __builtin_bit_cast(halfx8, b), c, 0, 0,
+                                                0);
 }
 
 // Score used inside the scans for a NaN cosine: below every real cosine

@@ -29,7 +29,7 @@ __global__ void __launch_bounds__(256) k_insert_maps(const T* __restrict__ src, 
                                                      int64_t rn_stride, int32_t first_slot,
                                                      const int32_t* __restrict__ slot_of, int32_t n_new,
                                                      int32_t L, int32_t E, int32_t row,
-                                                     int32_t* __restrict__ slots_out) {
+                                                     int32_t* __restrict__ slots_out, uint32_t* __restrict__ flags) {
   constexpr int kLayersPerWave = kMaxL / 4;
   __shared__ double sq[kMaxL];
   const int lane = threadIdx.x % kWave;
@@ -44,6 +44,14 @@ __global__ void __launch_bounds__(256) k_insert_maps(const T* __restrict__ src, 
     const int l = w + 4 * j;
     v[j] = T(0);
     if (l < L && lane < E) v[j] = src[(static_cast<int64_t>(i) * L + l) * E + lane];
+  }
+  // float32 maps: the trajectory scan's float16 split holds for magnitudes
+  // up to 8; a larger (or infinite) value is flagged
+  if constexpr (sizeof(T) == 4) {
+    bool big = false;
+#pragma unroll
+    for (int j = 0; j < kLayersPerWave; ++j) big = big || __builtin_fabsf(v[j]) > 8.0f;
+    if (__any(big) && lane == 0) atomicOr(flags, static_cast<uint32_t>(FM_FLAG_VALUE_RANGE));
   }
 #pragma unroll
   for (int j = 0; j < kLayersPerWave; ++j) {
@@ -111,11 +119,11 @@ hipError_t launch_insert(const StoreView& s, const void* maps, const void* embs,
   if (s.map_dtype == FM_F32) {
     hipLaunchKernelGGL(k_insert_maps<float>, grid, dim3(256), 0, st, static_cast<const float*>(maps),
                        static_cast<float*>(s.planes), s.plane_elems, s.rnorm, s.rn_stride, s.n, slot_of, n_new, s.L,
-                       s.E, s.row, slots_out);
+                       s.E, s.row, slots_out, s.flags);
   } else {
     hipLaunchKernelGGL(k_insert_maps<uint16_t>, grid, dim3(256), 0, st, static_cast<const uint16_t*>(maps),
                        static_cast<uint16_t*>(s.planes), s.plane_elems, s.rnorm, s.rn_stride, s.n, slot_of, n_new,
-                       s.L, s.E, s.row, slots_out);
+                       s.L, s.E, s.row, slots_out, s.flags);
   }
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;

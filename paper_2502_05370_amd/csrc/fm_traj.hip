@@ -7,10 +7,10 @@
 //
 //  k_traj_prep      sorts the batch by depth (deepest first, stable), writes
 //                   1/|q[b][0:p_b]| (float64 sum) and, for every "layer
-//                   group", the sorted query rows as MFMA-ready bf16 planes
-//                   (three parts of each float32 value, one plane for bf16
-//                   stores), zero beyond each query's depth and padded, so
-//                   the scan copies them verbatim.
+//                   group", the sorted query rows as MFMA-ready planes (two
+//                   float16 parts of each float32 value, one bf16 plane for
+//                   bf16 stores), zero beyond each query's depth and padded,
+//                   so the scan copies them verbatim.
 //  k_traj_scan      workgroup = one group of 16*TQ sorted queries x an even
 //                   share of the store's 16-map blocks, walked as slices of
 //                   8 waves x NBA blocks.  The map quads of a stage two stages
@@ -18,11 +18,13 @@
 //                   planes into a three-slot LDS ring (direct global->LDS
 //                   loads); one barrier per stage.  A query tile (16 queries)
 //                   stops at the layer group of its deepest member.  float32
-//                   operands are split into three bf16 parts
-//                   a = a1 + a2 + a3 + r (|r| <= 2^-27 |a|) and a.b
-//                   accumulates the six terms a1b3 + a2b2 + a1b2 + a3b1 +
-//                   a2b1 + a1b1 on v_mfma_f32_16x16x32_bf16 (dropped terms
-//                   < 2^-25 |ab|); bf16 stores take one MFMA.  The slice
+//                   operands are scaled by 2^12 and split into two float16
+//                   parts, A = 2^12 a = a1 + a2 + r with |r| <= 2^-22 |A|
+//                   (absolute 2^-25 where a2 falls below the float16 normal
+//                   range), and a.b = 2^-24 (a1b2 + a1b1 + a2b1) accumulates
+//                   on v_mfma_f32_16x16x32_f16 (dropped a2b2 and residuals
+//                   < 3 * 2^-22 |ab| + 2^-37 (|a| + |b|), for |a|, |b| <= 8);
+//                   bf16 stores take one bf16 MFMA.  The slice
 //                   epilogue divides by the query's and the store's prefix
 //                   norms (the latter precomputed at insert), keeps a per-lane
 //                   top-K of packed (score, index) keys, merges it across the
@@ -48,7 +50,7 @@ constexpr int kWaves = kThreads / kWave;
 
 typedef float floatx8 __attribute__((ext_vector_type(8)));
 typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef float float2v __attribute__((ext_vector_type(2)));
 
 
@@ -132,25 +134,27 @@ __device__ __forceinline__ int position_of(int b, int dc, const unsigned long lo
   return start[dc - 1] + r;
 }
 
-// float32 -> three bf16 parts (bit patterns), each rounded to nearest even.
-// Pairs are converted with one packed conversion and read back as a whole
-// 32-bit word (element-wise extraction of a bf16 vector lane is avoided).
-__device__ __forceinline__ void split3(const floatx8& v, u16x8& h, u16x8& m, u16x8& l) {
-  uint32x4 hw, mw, lw;
+// float32 -> two float16 parts (bit patterns) of A = 2^12 a: hi = RN16(A),
+// lo = RN16(A - hi).  A - hi is exact in float32 (one fused multiply-add of
+// the widened hi); hi is finite for |a| < 16 (values above 8 are flagged
+// where they enter).  Pairs convert with one packed conversion each.
+constexpr float kSplitScale = 4096.0f;                        // 2^12
+constexpr float kDotUnscale = 1.0f / (4096.0f * 4096.0f);     // 2^-24
+constexpr float kRangeLimit = 8.0f;
+__device__ __forceinline__ void split2(const floatx8& v, u16x8& h, u16x8& l) {
+  uint32x4 hw, lw;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const float2v x = {v[2 * j], v[2 * j + 1]};
-    const bf16x2 hb = __builtin_convertvector(x, bf16x2);
-    const float2v r1 = x - __builtin_convertvector(hb, float2v);
-    const bf16x2 mb = __builtin_convertvector(r1, bf16x2);
-    const float2v r2 = r1 - __builtin_convertvector(mb, float2v);
-    const bf16x2 lb = __builtin_convertvector(r2, bf16x2);
+    const float2v x = {v[2 * j] * kSplitScale, v[2 * j + 1] * kSplitScale};
+    const half2v hb = __builtin_convertvector(x, half2v);
+    float2v r;
+    r[0] = __builtin_fmaf(static_cast<float>(hb[0]), -1.0f, x[0]);
+    r[1] = __builtin_fmaf(static_cast<float>(hb[1]), -1.0f, x[1]);
+    const half2v lb = __builtin_convertvector(r, half2v);
     hw[j] = __builtin_bit_cast(uint32_t, hb);
-    mw[j] = __builtin_bit_cast(uint32_t, mb);
     lw[j] = __builtin_bit_cast(uint32_t, lb);
   }
   h = __builtin_bit_cast(u16x8, hw);
-  m = __builtin_bit_cast(u16x8, mw);
   l = __builtin_bit_cast(u16x8, lw);
 }
 
@@ -195,7 +199,7 @@ __global__ void __launch_bounds__(256) k_traj_prep(PrepArgs a) {
     const int lg = blockIdx.y;
     const int upr = 4 * a.geo.ksg + 1;
     const int rb = qrow_bytes(a.geo.ksg);
-    constexpr int NP = BF ? 1 : 3;
+    constexpr int NP = BF ? 1 : 2;
     const int64_t plane_pitch = static_cast<int64_t>(a.qg) * rb;              // one plane of a group slab
     const int grp = p0 / a.qg;
     char* slab = static_cast<char*>(a.ws.qrows) + (static_cast<int64_t>(lg) * a.b_pad + grp * a.qg) * NP * rb;
@@ -204,7 +208,8 @@ __global__ void __launch_bounds__(256) k_traj_prep(PrepArgs a) {
       const int r = i / upr;
       const int unit = i - r * upr;
       const int row_in_grp = p0 - grp * a.qg + r;
-      u16x8 h = u16x8{}, m = u16x8{}, l = u16x8{};
+      u16x8 h = u16x8{}, l = u16x8{};
+      bool big = false;
       const int b = s_b[r];
       if (b >= 0 && unit < 4 * a.geo.ksg) {
         // k positions 8*unit .. 8*unit+7 hold the slot runs
@@ -228,13 +233,17 @@ __global__ void __launch_bounds__(256) k_traj_prep(PrepArgs a) {
             }
           }
         }
-        if constexpr (!BF) split3(v, h, m, l);
+        if constexpr (!BF) {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) big = big || __builtin_fabsf(v[k]) > kRangeLimit;
+          split2(v, h, l);
+        }
       }
       char* dst = slab + static_cast<int64_t>(row_in_grp) * rb + 16 * unit;
       *reinterpret_cast<u16x8*>(dst) = h;
       if constexpr (!BF) {
-        *reinterpret_cast<u16x8*>(dst + plane_pitch) = m;
-        *reinterpret_cast<u16x8*>(dst + 2 * plane_pitch) = l;
+        *reinterpret_cast<u16x8*>(dst + plane_pitch) = l;
+        if (big) atomicOr(a.flags, static_cast<uint32_t>(FM_FLAG_VALUE_RANGE));
       }
     }
     return;
@@ -305,7 +314,7 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
   constexpr int esz = BF ? 2 : 4;
   constexpr int QG = 16 * TQ;                 // queries per group
   constexpr int MW = 16 * NBA;                // maps per wave and slice
-  constexpr int NP = BF ? 1 : 3;              // bf16 parts per operand
+  constexpr int NP = BF ? 1 : 2;              // MFMA parts per operand (bf16, or two float16)
   constexpr int RB = 64 * KSG + 16;           // staged query plane row bytes
   constexpr int NI_Q = (NP * QG * RB + W * 1024 - 1) / (W * 1024);  // 1 KB query loads per wave and stage
   constexpr int Q_STAGE = W * NI_Q * 1024;
@@ -456,33 +465,32 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
 #pragma unroll
           for (int nb = 0; nb < NBA; ++nb) acc[nb][t] = mfma_bf16(ap[0][nb][ks], bq[0][t], acc[nb][t]);
       } else {
-        // the six cross terms, small ones first, grouped by query part so
-        // that each part's fragments die early
-        constexpr int TA[6] = {0, 1, 0, 2, 1, 0};
-        constexpr int TB[6] = {2, 1, 1, 0, 0, 0};
+        // hi x lo, hi x hi, lo x hi, term-major so that consecutive MFMAs
+        // update different accumulators
+        constexpr int TA[3] = {0, 0, 1};
+        constexpr int TB[3] = {1, 0, 0};
 #pragma unroll
-        for (int term = 0; term < 6; ++term)
+        for (int term = 0; term < 3; ++term)
 #pragma unroll
           for (int t = 0; t < NT; ++t)
 #pragma unroll
             for (int nb = 0; nb < NBA; ++nb)
-              acc[nb][t] = mfma_bf16(ap[TA[term]][nb][ks], bq[TB[term]][t], acc[nb][t]);
+              acc[nb][t] = mfma_f16(ap[TA[term]][nb][ks], bq[TB[term]][t], acc[nb][t]);
       }
     };
 
-    // bf16 parts of the map operand of one stage.  k-step 0 is converted at
+    // MFMA parts of the map operand of one stage.  k-step 0 is converted at
     // the end of the previous stage, once this wave's loads of the stage have
     // landed; further k-steps during the stage, between MFMAs.  The ring
     // registers pass through an empty asm placed after the wait, so no use of
     // them is scheduled above it (the compiler would then wait for every
     // outstanding load itself, emptying the prefetch).
     u16x8 ap[NP][NBA][KSG];
-    Raw held[NBA][KSG];
-    auto convert_ks = [&](int ks) {
+    auto convert_ks = [&](Raw (&src)[NBA][KSG], int ks) {
 #pragma unroll
       for (int nb = 0; nb < NBA; ++nb) {
-        if constexpr (BF) ap[0][nb][ks] = held[nb][ks];
-        else split3(held[nb][ks], ap[0][nb][ks], ap[1][nb][ks], ap[2][nb][ks]);
+        if constexpr (BF) ap[0][nb][ks] = src[nb][ks];
+        else split2(src[nb][ks], ap[0][nb][ks], ap[1][nb][ks]);
       }
     };
     auto convert = [&](Raw (&ring_regs)[NBA][KSG]) {
@@ -490,11 +498,8 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
 #pragma unroll
       for (int nb = 0; nb < NBA; ++nb)
 #pragma unroll
-        for (int ks = 0; ks < KSG; ++ks) {
-          held[nb][ks] = ring_regs[nb][ks];
-          asm volatile("" : "+v"(held[nb][ks]));
-        }
-      convert_ks(0);
+        for (int ks = 0; ks < KSG; ++ks) asm volatile("" : "+v"(ring_regs[nb][ks]));
+      convert_ks(ring_regs, 0);
     };
 
     // Stage j: the map operand was converted at the end of stage j-1 (by a
@@ -524,7 +529,7 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
       for (int t = 1; t < TQ; ++t) na += tmd[t] > l_first ? 1 : 0;
 #pragma unroll
       for (int ks = 0; ks < KSG; ++ks) {
-        if (ks > 0) convert_ks(ks);
+        if (ks > 0) convert_ks(ring_regs, ks);
         if (ks == KSG - 1) load_a(j + 2, ring_regs);
         if constexpr (TQ == 1) {
           mfma_tiles(std::integral_constant<int, 1>{}, ks, sq, ap);
@@ -554,15 +559,15 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
 #pragma unroll
                 for (int nb = 0; nb < NBA; ++nb) acc[nb][tc + tt] = mfma_bf16(ap[0][nb][ks], bq[0][tt], acc[nb][tc + tt]);
             } else {
-              constexpr int TA[6] = {0, 1, 0, 2, 1, 0};
-              constexpr int TB[6] = {2, 1, 1, 0, 0, 0};
+              constexpr int TA[3] = {0, 0, 1};
+              constexpr int TB[3] = {1, 0, 0};
 #pragma unroll
-              for (int term = 0; term < 6; ++term)
+              for (int term = 0; term < 3; ++term)
 #pragma unroll
                 for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
                   for (int nb = 0; nb < NBA; ++nb)
-                    acc[nb][tc + tt] = mfma_bf16(ap[TA[term]][nb][ks], bq[TB[term]][tt], acc[nb][tc + tt]);
+                    acc[nb][tc + tt] = mfma_f16(ap[TA[term]][nb][ks], bq[TB[term]][tt], acc[nb][tc + tt]);
             }
           }
         }
@@ -589,7 +594,8 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
             for (int i = 0; i < 4; ++i) {
               const int y = y0 + i;
               if (y >= a.n) continue;
-              const float s = acc[nb][t][i] * rq * rs[i];
+              const float dot = BF ? acc[nb][t][i] : acc[nb][t][i] * kDotUnscale;
+              const float s = dot * rq * rs[i];
               if constexpr (DBG) a.dbg[static_cast<int64_t>(gperm[r]) * a.n + y] = s;
               best[t].push(make_key(s, y));
             }
@@ -714,7 +720,7 @@ Geo geometry(int E) {
 // LDS of the scan: 3 ring slots of query planes (8 waves x NI_Q x 1 KB each)
 // and the group's sorted query info; the top-K merge buffer reuses the ring.
 size_t scan_lds(bool bf, int TQ, int KSG, int KTOP) {
-  const int NP = bf ? 1 : 3;
+  const int NP = bf ? 1 : 2;
   const int QG = 16 * TQ;
   const int ni_q = (NP * QG * qrow_bytes(KSG) + 8 * 1024 - 1) / (8 * 1024);
   size_t ring = static_cast<size_t>(3) * 8 * ni_q * 1024;
@@ -777,7 +783,7 @@ hipError_t scan_ksg(int KSG, int TQ, const ScanArgs& a, size_t lds, hipStream_t 
 
 size_t traj_qrows_bytes(int L, int E, fm_dtype dt, int b_pad) {
   const Geo g = geometry(E);
-  const int np = dt == FM_BF16 ? 1 : 3;
+  const int np = dt == FM_BF16 ? 1 : 2;
   const int nlg = (L + g.lpg - 1) / g.lpg;
   // + slack: a stage's loads round the last group slab up to whole 4 KB
   return static_cast<size_t>(nlg) * b_pad * np * qrow_bytes(g.ksg) + 16384;
