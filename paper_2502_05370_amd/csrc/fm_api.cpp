@@ -193,6 +193,10 @@ fm_status fm_store_build(fm_store** out, const fm_store_desc* d) {
   if (ly.plane_bytes * group_planes > kMaxGroupBytes)
     return fail(FM_ERR_UNSUPPORTED, "cap=%d: %zu bytes per layer group of map planes exceed %zu", d->cap,
                 ly.plane_bytes * group_planes, kMaxGroupBytes);
+  // ... and the prefix inverse norms of all layers with 32-bit byte offsets.
+  if (static_cast<size_t>(d->L) * static_cast<size_t>(fm::rnorm_stride(d->cap)) * 4 > kMaxGroupBytes)
+    return fail(FM_ERR_UNSUPPORTED, "cap=%d L=%d: the prefix inverse norms exceed %zu bytes", d->cap, d->L,
+                kMaxGroupBytes);
   if (d->buffer == nullptr) return fail(FM_ERR_INVALID, "buffer is NULL");
   if (reinterpret_cast<uintptr_t>(d->buffer) % fm::kAlign != 0)
     return fail(FM_ERR_INVALID, "buffer must be %zu-byte aligned", fm::kAlign);

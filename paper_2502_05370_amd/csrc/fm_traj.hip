@@ -90,6 +90,7 @@ struct ScanArgs {
   int32_t R;          // workgroups per query group
   int32_t n_blocks;   // 16-map blocks of the store (ceil(n / 16))
   int32_t grid;
+  int32_t rt_bytes;   // LDS bytes of one inverse-norm table (whole 8 KB chunks)
   Workspace ws;
   float* dbg;         // optional dense scores [B][n]
 };
@@ -322,11 +323,17 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
   constexpr int NI = NI_A + NI_Q;
   static_assert(NI < 64, "vmcnt field is 6 bits");
 
+  constexpr int SW = W * NBA * 16;            // maps per slice
+
   extern __shared__ __align__(16) unsigned char smem[];
   unsigned char* ring = smem;                                              // [NS][Q_STAGE]
-  int32_t* gperm = reinterpret_cast<int32_t*>(smem + NS * Q_STAGE);        // [QG]
+  unsigned char* rtab = smem + NS * Q_STAGE;                               // [2][rt_bytes]
+  int32_t* gperm = reinterpret_cast<int32_t*>(rtab + 2 * a.rt_bytes);      // [QG]
   int32_t* gdep = gperm + QG;                                              // [QG]
   float* grq = reinterpret_cast<float*>(gdep + QG);                        // [QG]
+  int32_t* gdi = reinterpret_cast<int32_t*>(grq + QG);                     // [QG] distinct-depth index
+  int32_t* dval = gdi + QG;                                                // [QG] distinct depths
+  uint64_t* dmask = reinterpret_cast<uint64_t*>(dval + QG);                // [QG / 64]
   uint64_t* mbuf = reinterpret_cast<uint64_t*>(smem);                      // after the loop: [W][QG][KTOP]
 
   const int tid = threadIdx.x;
@@ -342,31 +349,30 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
   const bool active = u < a.n_qg * a.R;
   const int qgrp = active ? u % a.n_qg : 0;
   const int rr = active ? u / a.n_qg : 0;
-  // this workgroup's maps: 16-map blocks [b_begin, b_end), an even share of
-  // the store, taken as slices of W * NBA blocks (the last one partial)
-  const int b_begin = active ? static_cast<int>((static_cast<int64_t>(rr) * a.n_blocks) / a.R) : 0;
-  const int b_end = active ? static_cast<int>((static_cast<int64_t>(rr + 1) * a.n_blocks) / a.R) : 0;
+  // this workgroup's maps: [y_lo, y_hi), an even share of the store to the
+  // map (so every workgroup streams the same bytes), covered by the 16-map
+  // blocks [b_begin, b_end); a block shared with a neighbour loads only this
+  // workgroup's rows.  The blocks are walked as slices of W * NBA blocks (the
+  // last one partial).
+  const int y_lo = active ? static_cast<int>((static_cast<int64_t>(rr) * a.n) / a.R) : 0;
+  const int y_hi = active ? static_cast<int>((static_cast<int64_t>(rr + 1) * a.n) / a.R) : 0;
+  const int b_begin = y_lo / 16;
+  const int b_end = y_hi > y_lo ? (y_hi + 15) / 16 : b_begin;
   const int n_slices = (b_end - b_begin + W * NBA - 1) / (W * NBA);
   const int g0 = qgrp * QG;
 
-  for (int r = tid; r < QG; r += W * kWave) {
-    const int pos = g0 + r;
-    gperm[r] = a.ws.perm[pos];
-    gdep[r] = a.ws.sdep[pos];
-    grq[r] = a.ws.rq[pos];
-  }
-  __syncthreads();
-  int tmd[TQ];
-#pragma unroll
-  for (int t = 0; t < TQ; ++t) tmd[t] = gdep[16 * t];
-  const int NLG = (tmd[0] + a.geo.lpg - 1) / a.geo.lpg;
-  const int nstages = n_slices * NLG;
-
+  // Stage 0 is (slice 0, layer group 0) whatever the group's depths (every
+  // group's first position is a real query, so a workgroup with maps has at
+  // least one stage): its loads are issued before the prologue reads the
+  // group's depths, and the two latencies overlap.  NLG and nstages are set
+  // by the prologue; the loaders see them through their captures.
+  const bool has_work = active && n_slices > 0;
   TopK<KTOP> best[TQ];
 #pragma unroll
   for (int t = 0; t < TQ; ++t) best[t].clear();
-
-  if (active && nstages > 0) {
+  int NLG = 1;
+  int nstages = has_work ? 1 : 0;
+  {
     // Lane constants.  Register element j of lane (g, c) in k-step ks holds
     // slot 32ks + 4g + j (j < 4) or 32ks + 16 + 4g + j - 4 (j >= 4) of map
     // row c of the block; each run of 4 slots is one quad of a layer of the
@@ -407,12 +413,16 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
       for (int nb = 0; nb < NBA; ++nb) {
         const int blk = b_begin + si * (W * NBA) + w * NBA + nb;
         const int y_blk = 16 * blk;
-        const bool row_ok = real && blk < b_end && y_blk + c < a.n;
+        const bool row_ok = real && blk < b_end && y_blk + c >= y_lo && y_blk + c < y_hi;
         const uint32_t blk_off = static_cast<uint32_t>(blk) * tile_bytes;
 #pragma unroll
         for (int ks = 0; ks < KSG; ++ks) {
-          const uint32_t lo = row_ok && quad_ok[ks][0] ? lane_off[ks][0] + blk_off : kOutside;
-          const uint32_t hi = row_ok && quad_ok[ks][1] ? lane_off[ks][1] + blk_off : kOutside;
+          uint32_t lo = row_ok && quad_ok[ks][0] ? lane_off[ks][0] + blk_off : kOutside;
+          uint32_t hi = row_ok && quad_ok[ks][1] ? lane_off[ks][1] + blk_off : kOutside;
+          // opaque offsets: the loads stay unconditional (the compiler would
+          // otherwise branch around them, and a branch over in-flight loads
+          // costs a wait for every outstanding load)
+          asm volatile("" : "+v"(lo), "+v"(hi));
           if constexpr (BF) {
             const uint32x2 vl = __builtin_amdgcn_raw_buffer_load_b64(rs, static_cast<int>(lo), 0, 0);
             const uint32x2 vh = __builtin_amdgcn_raw_buffer_load_b64(rs, static_cast<int>(hi), 0, 0);
@@ -442,12 +452,75 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
 #pragma unroll
       for (int t = 0; t < TQ; ++t) acc[nb][t] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    // issue order: Q0 A0 Q1 A1, then during stage j: Q(j+2) A(j+2)
+    // issue order: Q0 A0, the prologue's loads, [RT0] Q1 A1, then during
+    // stage j: [RT] Q(j+2) A(j+2)
     Raw ar0[NBA][KSG], ar1[NBA][KSG];
-    load_q(0);
-    load_a(0, ar0);
-    load_q(1);
-    load_a(1, ar1);
+    if (has_work) {
+      load_q(0);
+      load_a(0, ar0);
+    }
+    for (int r = tid; r < QG; r += W * kWave) {
+      const int pos = g0 + r;
+      gperm[r] = a.ws.perm[pos];
+      gdep[r] = a.ws.sdep[pos];
+      grq[r] = a.ws.rq[pos];
+    }
+    __syncthreads();
+    // Distinct depths of the group (the positions are sorted by depth, deepest
+    // first; padding has depth 0): dval[k] is the k-th one, gdi[r] the index of
+    // gdep[r].  The epilogue of a slice reads the store's prefix inverse norms
+    // 1/|x[y][0:p]| of the slice's maps from an LDS table with one row per
+    // distinct depth.
+    {
+      const bool is_new = tid < QG && gdep[tid] > 0 && (tid == 0 || gdep[tid - 1] != gdep[tid]);
+      const uint64_t bal = __ballot(is_new);
+      if (lane == 0 && w < QG / 64 + (QG % 64 ? 1 : 0)) dmask[w] = bal;
+      __syncthreads();
+      if (tid < QG) {
+        int before = 0;
+        for (int ww = 0; ww < w; ++ww) before += __popcll(dmask[ww]);
+        const int incl = before + __popcll(bal & ((2ull << lane) - 1ull));
+        gdi[tid] = incl > 0 ? incl - 1 : 0;
+        if (is_new) dval[incl - 1] = gdep[tid];
+      }
+      __syncthreads();
+    }
+    int nd = 0;
+    for (int ww = 0; ww < QG / 64 + (QG % 64 ? 1 : 0); ++ww) nd += __popcll(dmask[ww]);
+    int tmd[TQ];
+#pragma unroll
+    for (int t = 0; t < TQ; ++t) tmd[t] = gdep[16 * t];
+    NLG = (tmd[0] + a.geo.lpg - 1) / a.geo.lpg;
+    nstages = n_slices * NLG;
+
+    // Inverse-norm table of slice si into LDS buffer si % 2: row k holds
+    // rnorm[dval[k] - 1][y_s .. y_s + SW) (y_s = the slice's first map), read
+    // with raw buffer loads straight into LDS (offsets past the norms read as
+    // zeros).  Issued one stage ahead of the slice's last stage and before
+    // that stage's ring loads, so the counted ring waits also cover it and the
+    // next barrier publishes it.
+    const __amdgpu_buffer_rsrc_t rs_rn = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(a.rnorm), static_cast<short>(0),
+        static_cast<int>(static_cast<uint32_t>(a.L) * static_cast<uint32_t>(a.rn_stride) * 4u), kBufWord3);
+    const int rt_chunks = (nd * SW * 4 + W * 1024 - 1) / (W * 1024);   // 1 KB loads per wave
+    auto load_rt = [&](int si) {
+      unsigned char* dst = rtab + (si & 1) * a.rt_bytes;
+      const int y_s = 16 * (b_begin + si * (W * NBA));
+      for (int i = 0; i < rt_chunks; ++i) {
+        const int byte = (w + W * i) * 1024 + lane * 16;
+        const int k = byte / (SW * 4);
+        const int col = (byte - k * SW * 4) / 4;
+        const uint32_t off = k < nd ? static_cast<uint32_t>(((dval[k] - 1) * a.rn_stride + y_s + col) * 4) : kOutside;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_rn, (lds_vp)(dst + (w + W * i) * 1024), 16, static_cast<int>(off), 0,
+                                                 0, 0);
+      }
+    };
+
+    if (has_work) {
+      if (NLG == 1) load_rt(0);
+      load_q(1);
+      load_a(1, ar1);
+    }
 
     // MFMAs of one k-step for the first NT (active) query tiles, term-major so
     // that consecutive MFMAs update different accumulators.
@@ -493,8 +566,8 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
         else split2(src[nb][ks], ap[0][nb][ks], ap[1][nb][ks]);
       }
     };
+    // (callers wait for the registers' loads first: wait_vmcnt<NI>)
     auto convert = [&](Raw (&ring_regs)[NBA][KSG]) {
-      wait_vmcnt<NI>();
 #pragma unroll
       for (int nb = 0; nb < NBA; ++nb)
 #pragma unroll
@@ -513,11 +586,15 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
       const unsigned char* sq = ring + (j % NS) * Q_STAGE;
 
       raw_barrier();
+      // the inverse-norm table of the slice whose last stage is j+1
+      if (j + 1 < nstages && (j + 1) % NLG == NLG - 1) load_rt((j + 1) / NLG);
       // The query planes of stage j+2 go to slot (j+2) % 3 = (j-1) % 3,
       // which every wave finished reading before this barrier; the map rows
       // of stage j+2 go to the registers of stage j once all of its k-steps
       // are converted.
       load_q(j + 2);
+
+      const bool last = lg == NLG - 1;
 
       // Query tiles are sorted by depth (deepest first): the first na tiles
       // are those whose deepest query still has layers in this group (the
@@ -573,7 +650,13 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
         }
       }
 
-      if (lg == NLG - 1) {
+      // Stage j+1's loads (issued during stage j-1) have landed once at most
+      // this stage's NI ring loads are outstanding.  Waiting here, before the
+      // epilogue branch, also settles the registers the compiler may move
+      // where the branch joins (a move of a register whose load is still in
+      // flight would otherwise wait for every outstanding load).
+      wait_vmcnt<NI>();
+      if (last) {
         // End of a slice: cosine = dot * 1/|q[0:p]| * 1/|x[y][0:p]| with the
         // store's prefix inverse norm at the query's depth p; lane (g, c)
         // holds maps 16nb + 4g + i (i = 0..3) of query column c of each tile.
@@ -582,18 +665,17 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
           const int r = 16 * t + c;
           const int p = gdep[r];
           const float rq = grq[r];
+          if (p == 0) continue;
+          const float* rrow = reinterpret_cast<const float*>(rtab + (si & 1) * a.rt_bytes) + gdi[r] * SW;
 #pragma unroll
           for (int nb = 0; nb < NBA; ++nb) {
-            // blocks past b_end belong to the next workgroup
-            const bool blk_ok = blk_wave + nb < b_end;
             const int y0 = 16 * (blk_wave + nb) + 4 * g;
-            const float* rsp = (p > 0 && blk_ok && y0 < a.n) ? a.rnorm + static_cast<int64_t>(p - 1) * a.rn_stride + y0 : a.rnorm;
-            const floatx4 rs = *reinterpret_cast<const floatx4*>(rsp);
-            if (p == 0 || !blk_ok) continue;
+            const floatx4 rs = *reinterpret_cast<const floatx4*>(rrow + (w * NBA + nb) * 16 + 4 * g);
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const int y = y0 + i;
-              if (y >= a.n) continue;
+              // maps outside [y_lo, y_hi) belong to a neighbouring workgroup
+              if (y < y_lo || y >= y_hi) continue;
               const float dot = BF ? acc[nb][t][i] : acc[nb][t][i] * kDotUnscale;
               const float s = dot * rq * rs[i];
               if constexpr (DBG) a.dbg[static_cast<int64_t>(gperm[r]) * a.n + y] = s;
@@ -613,13 +695,16 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
     // Two-stage register rotation: stage j computes from the parts of
     // ar[j % 2], reloads it with the map rows of stage j + 2, and converts
     // ar[(j + 1) % 2] for stage j + 1.
-    convert(ar0);
-    int j = 0;
-    for (; j + 2 <= nstages; j += 2) {
-      stage(j, ar0, ar1);
-      stage(j + 1, ar1, ar0);
+    if (has_work) {
+      wait_vmcnt<NI>();
+      convert(ar0);
+      int j = 0;
+      for (; j + 2 <= nstages; j += 2) {
+        stage(j, ar0, ar1);
+        stage(j + 1, ar1, ar0);
+      }
+      if (j < nstages) stage(j, ar0, ar1);
     }
-    if (j < nstages) stage(j, ar0, ar1);
     wait_vmcnt<0>();   // drain the trailing loads
     __syncthreads();
   }
@@ -717,16 +802,29 @@ Geo geometry(int E) {
   return g;
 }
 
-// LDS of the scan: 3 ring slots of query planes (8 waves x NI_Q x 1 KB each)
-// and the group's sorted query info; the top-K merge buffer reuses the ring.
-size_t scan_lds(bool bf, int TQ, int KSG, int KTOP) {
+// One inverse-norm table: a row of the slice's 8 * NBA * 16 maps per distinct
+// depth (at most min(QG, dmax) of them), in whole 8 KB chunks (one 1 KB load
+// per wave).
+int scan_rt_bytes(int TQ, int dmax) {
+  const int QG = 16 * TQ;
+  const int nba = TQ <= 4 ? 2 : 1;
+  const int rows = QG < dmax ? QG : dmax;
+  return (rows * 8 * nba * 16 * 4 + 8 * 1024 - 1) / (8 * 1024) * (8 * 1024);
+}
+
+// LDS of the scan: 3 ring slots of query planes (8 waves x NI_Q x 1 KB each),
+// two inverse-norm tables, and the group's sorted query info (permutation,
+// depth, 1/|q|, distinct-depth index and values, distinct-depth masks); the
+// top-K merge buffer reuses the ring.
+size_t scan_lds(bool bf, int TQ, int KSG, int KTOP, int dmax) {
   const int NP = bf ? 1 : 2;
   const int QG = 16 * TQ;
   const int ni_q = (NP * QG * qrow_bytes(KSG) + 8 * 1024 - 1) / (8 * 1024);
   size_t ring = static_cast<size_t>(3) * 8 * ni_q * 1024;
   const size_t merge = static_cast<size_t>(8) * QG * KTOP * 8;
   if (merge > ring) ring = merge;
-  return ring + static_cast<size_t>(3) * QG * 4;
+  return ring + 2 * static_cast<size_t>(scan_rt_bytes(TQ, dmax)) + static_cast<size_t>(5) * QG * 4 +
+         static_cast<size_t>(8) * ((QG + 63) / 64);
 }
 
 template <bool BF, int TQ, int NBA, int KSG, int KTOP, bool DBG = false>
@@ -805,7 +903,7 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
     int TQ = 1;
     while (16 * TQ < Bc && TQ < tq_max) TQ *= 2;
     // smaller query groups when the staged planes of one would not fit the ring
-    while (TQ > 1 && scan_lds(bf, TQ, geo.ksg, KTOP) > kLds) TQ /= 2;
+    while (TQ > 1 && scan_lds(bf, TQ, geo.ksg, KTOP, max_depth) > kLds) TQ /= 2;
     const int QG = 16 * TQ;
     const int n_qg = (Bc + QG - 1) / QG;
     const int b_pad = n_qg * QG;
@@ -832,7 +930,7 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
 
     // Two 16-map blocks per wave unless the query group is large.
     const int NBA = TQ <= 4 ? 2 : 1;
-    const size_t lds = scan_lds(bf, TQ, geo.ksg, KTOP);
+    const size_t lds = scan_lds(bf, TQ, geo.ksg, KTOP, max_depth);
     if (lds > kLds) return hipErrorInvalidConfiguration;
 
     const int n_blocks = (s.n + 15) / 16;
@@ -860,6 +958,7 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
     a.R = R;
     a.n_blocks = n_blocks;
     a.grid = (n_qg * R + 7) / 8 * 8;
+    a.rt_bytes = scan_rt_bytes(TQ, max_depth);
     a.ws = ws;
     a.dbg = dbg_scores != nullptr ? dbg_scores + static_cast<int64_t>(b0) * s.n : nullptr;
     if (dbg_scores != nullptr) {
