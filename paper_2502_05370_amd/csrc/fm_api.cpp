@@ -92,12 +92,13 @@ ScanEvents& scan_events() {
   return ev;
 }
 
-// Workspace layout: [partial][perm][sdep][rq][qrows], each part 256-byte
+// Workspace layout: [partial][perm][sdep][rq][pgrp][rgrp][ngrp][qrows], each part 256-byte
 // aligned.  qrows holds the staged queries of one launch: the trajectory
 // planes, or the tiled semantic queries (1024 x d_emb bf16).
 size_t workspace_bytes_needed(int32_t L, int32_t E, int32_t d_emb, fm_dtype map_dtype) {
   size_t b = align_up(sizeof(uint64_t) * kChunkB * kMaxPartials * kMaxK, kAlign);
   b += 3 * align_up(sizeof(int32_t) * kChunkB, kAlign);
+  b += 3 * align_up(sizeof(int32_t) * (kChunkB / 16), kAlign);
   const size_t traj = traj_qrows_bytes(L, E, map_dtype, kChunkB);
   const size_t sem = static_cast<size_t>(kChunkB) * d_emb * 2;
   b += align_up(traj > sem ? traj : sem, kAlign);
@@ -115,6 +116,12 @@ Workspace carve_workspace(void* base) {
   p += align_up(sizeof(int32_t) * kChunkB, kAlign);
   w.rq = reinterpret_cast<float*>(p);
   p += align_up(sizeof(float) * kChunkB, kAlign);
+  w.pgrp = reinterpret_cast<int32_t*>(p);
+  p += align_up(sizeof(int32_t) * (kChunkB / 16), kAlign);
+  w.rgrp = reinterpret_cast<int32_t*>(p);
+  p += align_up(sizeof(int32_t) * (kChunkB / 16), kAlign);
+  w.ngrp = reinterpret_cast<int32_t*>(p);
+  p += align_up(sizeof(int32_t) * (kChunkB / 16), kAlign);
   w.qrows = p;
   return w;
 }

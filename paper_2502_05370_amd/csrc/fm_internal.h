@@ -60,6 +60,9 @@ struct Workspace {
   int32_t* perm;      // [kChunkB] query index at each depth-sorted position (-1: padding)
   int32_t* sdep;      // [kChunkB] clamped depth at each position (0: padding)
   float* rq;          // [kChunkB] 1/|query prefix| at each position
+  int32_t* pgrp;      // [kChunkB / 16] first scan workgroup of each query group (trajectory)
+  int32_t* rgrp;      // [kChunkB / 16] scan workgroups (partial lists) of each query group
+  int32_t* ngrp;      // [kChunkB / 16] layer groups each query group's scan walks
   void* qrows;        // staged query rows of every layer group (trajectory)
 };
 size_t workspace_bytes_needed(int32_t L, int32_t E, int32_t d_emb, fm_dtype map_dtype);
@@ -79,8 +82,11 @@ size_t dedup_scratch_bytes(int32_t cap, int32_t n_max);
 DedupScratch carve_dedup_scratch(void* base, int32_t cap, int32_t n_max);
 Workspace carve_workspace(void* base);
 size_t traj_qrows_bytes(int L, int E, fm_dtype dt, int b_pad);
+// partial holds R lists per position; with rgrp set, position pos merges only
+// the first rgrp[pos / qg] of them.
 hipError_t launch_finalize(const uint64_t* partial, const int32_t* perm, int32_t B, int32_t R, int32_t k, int KTOP,
-                           int32_t* idx_out, float* score_out, hipStream_t st);
+                           int32_t* idx_out, float* score_out, hipStream_t st, const int32_t* rgrp = nullptr,
+                           int32_t qg = 0);
 
 // Caller-provided events bracketing the next scan launches on this thread
 // (both null when unset); see fm_debug_scan_events.

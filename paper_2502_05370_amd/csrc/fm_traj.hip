@@ -74,6 +74,9 @@ struct PrepArgs {
   int32_t nlg;        // layer groups staged (ceil(dmax / lpg))
   int32_t b_pad;      // positions per staged layer group (multiple of the group size)
   int32_t qg;         // queries per group (16 * TQ)
+  int32_t n_qg;       // query groups
+  int32_t G;          // scan workgroups to share among the groups
+  int32_t epi16;      // a slice epilogue's cost in sixteenths of a stage's
   Workspace ws;
   uint32_t* flags;
 };
@@ -87,7 +90,7 @@ struct ScanArgs {
   Geo geo;
   int32_t B, b_pad, dmax;
   int32_t n_qg;       // query groups
-  int32_t R;          // workgroups per query group
+  int32_t R;          // partial lists per position (the workgroups of a group: ws.rgrp)
   int32_t n_blocks;   // 16-map blocks of the store (ceil(n / 16))
   int32_t grid;
   int32_t rt_bytes;   // LDS bytes of one inverse-norm table (whole 8 KB chunks)
@@ -249,9 +252,42 @@ __global__ void __launch_bounds__(256) k_traj_prep(PrepArgs a) {
     }
     return;
   }
+  const int lane = tid % kWave;
+  // Scan workgroups per query group.  Per slice of maps a group's scan takes
+  // one stage per layer group its deepest query reaches (position g * qg,
+  // the groups being depth-sorted) plus the slice epilogue (ranking every
+  // score), so the G workgroups are shared in proportion to
+  // 16 * stages + epi16, at least one each; the scan reads its group, share
+  // and stage count back.
+  if (blockIdx.x == 0 && static_cast<int>(blockIdx.y) == a.nlg && tid < kWave) {
+    int dg = 0;
+    if (lane < a.n_qg) {
+      const int P = lane * a.qg;
+      for (int l = 0; l < a.dmax; ++l) {
+        const int hi = l == 0 ? a.B : start[l - 1];
+        if (start[l] <= P && P < hi) dg = l + 1;
+      }
+    }
+    const int nlg_g = (dg + a.geo.lpg - 1) / a.geo.lpg;
+    const int wgt = lane < a.n_qg ? 16 * nlg_g + a.epi16 : 0;
+    int tot = wgt;
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) tot += __shfl_xor(tot, m, kWave);
+    const int rg = lane < a.n_qg ? 1 + static_cast<int>(static_cast<int64_t>(a.G - a.n_qg) * wgt / (tot > 0 ? tot : 1)) : 0;
+    int incl = rg;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const int o = __shfl_up(incl, off, kWave);
+      if (lane >= off) incl += o;
+    }
+    if (lane < a.n_qg) {
+      a.ws.rgrp[lane] = rg;
+      a.ws.pgrp[lane] = incl - rg;
+      a.ws.ngrp[lane] = nlg_g;
+    }
+  }
   // perm, depth and 1/|q[b][0:p]| of the 16 positions: blocks y = nlg ..
   // nlg+3 take four rows each, one wave per row
-  const int lane = tid % kWave;
   const int r = (static_cast<int>(blockIdx.y) - a.nlg) * 4 + tid / kWave;
   const int pos = p0 + r;
   const int b = s_b[r];
@@ -342,36 +378,54 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
   const int g = lane / 16;
   const int c = lane % 16;
 
-  // workgroup -> (query group, slice range); the n_qg workgroups sharing a
-  // slice range are consecutive, hence on one XCD and its L2
+  // workgroup -> (query group, share of the store): group g owns the
+  // workgroups [pgrp[g], pgrp[g] + rgrp[g]) of the XCD-aware numbering u
+  // (consecutive u run on one XCD).
   const int bid = blockIdx.x;
   const int u = (bid % 8) * (a.grid / 8) + bid / 8;
-  const bool active = u < a.n_qg * a.R;
-  const int qgrp = active ? u % a.n_qg : 0;
-  const int rr = active ? u / a.n_qg : 0;
+  // A single group owns every workgroup and walks ceil(dmax / lpg) layer
+  // groups (a bound on its deepest query; deeper staged rows are zero), so
+  // it needs no read of the allocation.
+  int pg_l = 0x7fffffff, rg_l = 0, ng_l = 0;
+  if (a.n_qg == 1) {
+    pg_l = 0;
+    rg_l = a.R;
+    ng_l = (a.dmax + a.geo.lpg - 1) / a.geo.lpg;
+  } else if (lane < a.n_qg) {
+    pg_l = a.ws.pgrp[lane];
+    rg_l = a.ws.rgrp[lane];
+    ng_l = a.ws.ngrp[lane];
+  }
+  const uint64_t gbal = __ballot(lane < a.n_qg && pg_l <= u);
+  const int qg_u = gbal != 0 ? __popcll(gbal) - 1 : 0;
+  // (read back as wave-uniform values, so everything derived from them stays
+  // in scalar registers and uniform branches)
+  const int Rg = __builtin_amdgcn_readfirstlane(__shfl(rg_l, qg_u, kWave));
+  const int Pg = __builtin_amdgcn_readfirstlane(__shfl(pg_l, qg_u, kWave));
+  const bool active = gbal != 0 && u - Pg < Rg;
+  const int qgrp = active ? qg_u : 0;
+  const int rr = active ? u - Pg : 0;
   // this workgroup's maps: [y_lo, y_hi), an even share of the store to the
   // map (so every workgroup streams the same bytes), covered by the 16-map
   // blocks [b_begin, b_end); a block shared with a neighbour loads only this
   // workgroup's rows.  The blocks are walked as slices of W * NBA blocks (the
   // last one partial).
-  const int y_lo = active ? static_cast<int>((static_cast<int64_t>(rr) * a.n) / a.R) : 0;
-  const int y_hi = active ? static_cast<int>((static_cast<int64_t>(rr + 1) * a.n) / a.R) : 0;
+  const int y_lo = active ? static_cast<int>((static_cast<int64_t>(rr) * a.n) / Rg) : 0;
+  const int y_hi = active ? static_cast<int>((static_cast<int64_t>(rr + 1) * a.n) / Rg) : 0;
   const int b_begin = y_lo / 16;
   const int b_end = y_hi > y_lo ? (y_hi + 15) / 16 : b_begin;
   const int n_slices = (b_end - b_begin + W * NBA - 1) / (W * NBA);
   const int g0 = qgrp * QG;
 
-  // Stage 0 is (slice 0, layer group 0) whatever the group's depths (every
-  // group's first position is a real query, so a workgroup with maps has at
-  // least one stage): its loads are issued before the prologue reads the
-  // group's depths, and the two latencies overlap.  NLG and nstages are set
-  // by the prologue; the loaders see them through their captures.
+  // Stages 0 and 1 load before the prologue fills LDS with the group's
+  // sorted query info, so the latencies overlap.
   const bool has_work = active && n_slices > 0;
   TopK<KTOP> best[TQ];
 #pragma unroll
   for (int t = 0; t < TQ; ++t) best[t].clear();
-  int NLG = 1;
-  int nstages = has_work ? 1 : 0;
+  const int ng_u = __builtin_amdgcn_readfirstlane(__shfl(ng_l, qg_u, kWave));
+  const int NLG = ng_u > 0 ? ng_u : 1;
+  const int nstages = has_work ? n_slices * NLG : 0;
   {
     // Lane constants.  Register element j of lane (g, c) in k-step ks holds
     // slot 32ks + 4g + j (j < 4) or 32ks + 16 + 4g + j - 4 (j >= 4) of map
@@ -452,12 +506,14 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
 #pragma unroll
       for (int t = 0; t < TQ; ++t) acc[nb][t] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    // issue order: Q0 A0, the prologue's loads, [RT0] Q1 A1, then during
+    // issue order: Q0 A0 Q1 A1, the prologue's loads, [RT0], then during
     // stage j: [RT] Q(j+2) A(j+2)
     Raw ar0[NBA][KSG], ar1[NBA][KSG];
     if (has_work) {
       load_q(0);
       load_a(0, ar0);
+      load_q(1);
+      load_a(1, ar1);
     }
     for (int r = tid; r < QG; r += W * kWave) {
       const int pos = g0 + r;
@@ -490,8 +546,6 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
     int tmd[TQ];
 #pragma unroll
     for (int t = 0; t < TQ; ++t) tmd[t] = gdep[16 * t];
-    NLG = (tmd[0] + a.geo.lpg - 1) / a.geo.lpg;
-    nstages = n_slices * NLG;
 
     // Inverse-norm table of slice si into LDS buffer si % 2: row k holds
     // rnorm[dval[k] - 1][y_s .. y_s + SW) (y_s = the slice's first map), read
@@ -516,10 +570,11 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
       }
     };
 
-    if (has_work) {
-      if (NLG == 1) load_rt(0);
-      load_q(1);
-      load_a(1, ar1);
+    // With one layer group per slice, stage 0 is slice 0's last stage: its
+    // inverse-norm table loads now and lands before the loop starts.
+    if (has_work && NLG == 1) {
+      load_rt(0);
+      wait_vmcnt<0>();
     }
 
     // MFMAs of one k-step for the first NT (active) query tiles, term-major so
@@ -749,13 +804,15 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
 template <int KTOP>
 __global__ void __launch_bounds__(256) k_finalize(const uint64_t* __restrict__ partial, const int32_t* __restrict__ perm,
                                                   int32_t B, int32_t R, int32_t k, int32_t* __restrict__ idx_out,
-                                                  float* __restrict__ score_out) {
+                                                  float* __restrict__ score_out, const int32_t* __restrict__ rgrp,
+                                                  int32_t qg) {
   const int lane = threadIdx.x % kWave;
   const int pos = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
   if (pos >= B) return;
+  const int nr = rgrp != nullptr ? rgrp[pos / qg] : R;
   TopK<KTOP> m;
   m.clear();
-  for (int r = lane; r < R; r += kWave) m.merge(partial + (static_cast<int64_t>(pos) * R + r) * KTOP);
+  for (int r = lane; r < nr; r += kWave) m.merge(partial + (static_cast<int64_t>(pos) * R + r) * KTOP);
 #pragma unroll
   for (int off = 1; off < kWave; off <<= 1) {
     uint64_t o[KTOP];
@@ -776,11 +833,14 @@ __global__ void __launch_bounds__(256) k_finalize(const uint64_t* __restrict__ p
 }
 
 hipError_t launch_finalize(const uint64_t* partial, const int32_t* perm, int32_t B, int32_t R, int32_t k, int KTOP,
-                           int32_t* idx_out, float* score_out, hipStream_t st) {
+                           int32_t* idx_out, float* score_out, hipStream_t st, const int32_t* rgrp, int32_t qg) {
   const dim3 grid((B + kWaves - 1) / kWaves);
-  if (KTOP == 1) hipLaunchKernelGGL(k_finalize<1>, grid, dim3(kThreads), 0, st, partial, perm, B, R, k, idx_out, score_out);
-  else if (KTOP == 4) hipLaunchKernelGGL(k_finalize<4>, grid, dim3(kThreads), 0, st, partial, perm, B, R, k, idx_out, score_out);
-  else hipLaunchKernelGGL(k_finalize<8>, grid, dim3(kThreads), 0, st, partial, perm, B, R, k, idx_out, score_out);
+  if (KTOP == 1)
+    hipLaunchKernelGGL(k_finalize<1>, grid, dim3(kThreads), 0, st, partial, perm, B, R, k, idx_out, score_out, rgrp, qg);
+  else if (KTOP == 4)
+    hipLaunchKernelGGL(k_finalize<4>, grid, dim3(kThreads), 0, st, partial, perm, B, R, k, idx_out, score_out, rgrp, qg);
+  else
+    hipLaunchKernelGGL(k_finalize<8>, grid, dim3(kThreads), 0, st, partial, perm, B, R, k, idx_out, score_out, rgrp, qg);
   return hipGetLastError();
 }
 
@@ -922,6 +982,17 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
     pa.qg = QG;
     pa.ws = ws;
     pa.flags = s.flags;
+    // scan workgroups: about one per CU, no more than the store's 16-map
+    // blocks per group, at least one per group
+    const int n_blocks = (s.n + 15) / 16;
+    int G = n_qg * n_blocks < 256 ? n_qg * n_blocks : 256;
+    if (G < n_qg) G = n_qg;
+    pa.n_qg = n_qg;
+    pa.G = G;
+    // slice epilogue vs stage cost, measured on the top-4 Phi-shaped batch:
+    // about 0.16 stage per score kept in a top-4 list, a third of that for
+    // top-1
+    pa.epi16 = TQ * (TQ <= 4 ? 2 : 1) * 4 * (KTOP == 1 ? 1 : 3);
     const dim3 pgrid(b_pad / 16, nlg + 4);
     if (bf) hipLaunchKernelGGL(k_traj_prep<true>, pgrid, dim3(kThreads), 0, st, pa);
     else hipLaunchKernelGGL(k_traj_prep<false>, pgrid, dim3(kThreads), 0, st, pa);
@@ -933,13 +1004,7 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
     const size_t lds = scan_lds(bf, TQ, geo.ksg, KTOP, max_depth);
     if (lds > kLds) return hipErrorInvalidConfiguration;
 
-    const int n_blocks = (s.n + 15) / 16;
-    // workgroups per query group: about one workgroup per CU in total, each
-    // with an even share of the blocks (at least one)
-    int R = 256 / n_qg;
-    if (R < 1) R = 1;
-    if (R > n_blocks) R = n_blocks > 0 ? n_blocks : 1;
-    if (R > kMaxPartials) R = kMaxPartials;
+    const int R = G;   // partial lists per position (a group's share is at most G)
 
     ScanArgs a{};
     a.planes = s.planes;
@@ -957,7 +1022,7 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
     a.n_qg = n_qg;
     a.R = R;
     a.n_blocks = n_blocks;
-    a.grid = (n_qg * R + 7) / 8 * 8;
+    a.grid = (G + 7) / 8 * 8;
     a.rt_bytes = scan_rt_bytes(TQ, max_depth);
     a.ws = ws;
     a.dbg = dbg_scores != nullptr ? dbg_scores + static_cast<int64_t>(b0) * s.n : nullptr;
@@ -976,7 +1041,7 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
     if (err != hipSuccess) return err;
     if (idx_out != nullptr) {
       err = launch_finalize(ws.partial, ws.perm, Bc, R, k, KTOP, idx_out + static_cast<int64_t>(b0) * k,
-                            score_out + static_cast<int64_t>(b0) * k, st);
+                            score_out + static_cast<int64_t>(b0) * k, st, ws.rgrp, QG);
       if (err != hipSuccess) return err;
     }
   }
