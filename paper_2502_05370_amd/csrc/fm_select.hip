@@ -46,9 +46,18 @@ __device__ __forceinline__ bool ahead(double pi, int i, double pj, int j) {
 
 }  // namespace
 
+// Ordered 64-bit key of a float64 probability: larger value -> larger key,
+// -0 and +0 equal, NaN lowest (key 0).  Ranking by (key desc, index asc) is
+// the (p desc, j asc, NaN last) order of ahead().
+__device__ __forceinline__ uint64_t ord_f64(double p) {
+  if (p != p) return 0ull;
+  const uint64_t u = static_cast<uint64_t>(__double_as_longlong(p + 0.0));
+  return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
+}
+
 __global__ void __launch_bounds__(256) k_select(SelArgs a) {
   __shared__ double sorted[4][kMaxE];
-  __shared__ double vals[4][kMaxE];
+  __shared__ uint64_t keys[4][kMaxE];
   const int lane = threadIdx.x % kWave;
   const int wv = threadIdx.x / kWave;
   const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + wv;
@@ -93,16 +102,18 @@ __global__ void __launch_bounds__(256) k_select(SelArgs a) {
     tau = static_cast<double>(a.tau);
   }
 
-  // 3. rank: every lane counts the experts ahead of its own, reading all
-  // values from LDS (broadcast reads, independent of each other)
-  if (lane < a.E) vals[wv][lane] = p;
+  // 3. rank: every lane counts the experts ahead of its own, comparing
+  // ordered integer keys read from LDS (broadcast reads, independent of
+  // each other)
+  const uint64_t key = ord_f64(p);
+  if (lane < a.E) keys[wv][lane] = key;
   __builtin_amdgcn_s_waitcnt(0);
   __builtin_amdgcn_wave_barrier();
   int rank = 0;
 #pragma unroll 8
   for (int i = 0; i < a.E; ++i) {
-    const double pi = vals[wv][i];
-    if (i != lane && ahead(pi, i, p, lane)) ++rank;
+    const uint64_t ki = keys[wv][i];
+    rank += (ki > key || (ki == key && i < lane)) ? 1 : 0;
   }
   if (lane < a.E) sorted[wv][rank] = p;
   __builtin_amdgcn_s_waitcnt(0);
