@@ -169,89 +169,93 @@ __device__ __forceinline__ void split2(const floatx8& v, u16x8& h, u16x8& l) {
 // ----------------------------------------------------------------------------- prep
 
 // grid = (b_pad / 16, nlg + 4).  Block (x, y < nlg) stages layer group y of
-// sorted positions 16x .. 16x+15; blocks (x, nlg .. nlg+3) write their perm,
-// depth and 1/|q| entries.
+// queries 16x .. 16x+15 at their sorted positions; blocks (x, nlg .. nlg+3)
+// write those queries' perm, depth and 1/|q| entries; block (0, nlg) also
+// shares the scan's workgroups among the query groups.
 template <bool BF>
 __global__ void __launch_bounds__(256) k_traj_prep(PrepArgs a) {
   using T = typename std::conditional<BF, uint16_t, float>::type;
   constexpr int esz = sizeof(T);
   __shared__ unsigned long long bits[kMaxL * 16];
   __shared__ int32_t start[kMaxL];
-  __shared__ int32_t s_b[16];
-  __shared__ int32_t s_d[16];
   const int tid = threadIdx.x;
-  if (tid < 16) {
-    s_b[tid] = -1;
-    s_d[tid] = 0;
-  }
-  depth_buckets(a.depth, a.B, a.dmax, bits, start);
-  const int p0 = blockIdx.x * 16;
-  for (int b = tid; b < a.B; b += kThreads) {
-    const int d = a.depth[b];
-    const int dc = d < 1 ? 1 : (d > a.dmax ? a.dmax : d);
-    const int pos = position_of(b, dc, bits, start);
-    if (pos >= p0 && pos < p0 + 16) {
-      s_b[pos - p0] = b;
-      s_d[pos - p0] = dc;
-    }
-    if (blockIdx.x == 0 && blockIdx.y == 0 && dc != d) atomicOr(a.flags, static_cast<uint32_t>(FM_FLAG_DEPTH_CLAMPED));
-  }
-  __syncthreads();
   const T* q = static_cast<const T*>(a.q);
+  // Blocks are indexed by query (16 per block), not by sorted position, so
+  // each thread's loads of its query's values are issued before, and land
+  // during, the depth sort that tells where the staged row goes.
   if (static_cast<int>(blockIdx.y) < a.nlg) {
-    // one thread per (row, 8-slot unit); unit 4*ksg of a row is the pad
+    // one thread per (query row, 8-slot unit); unit 4*ksg of a row is the pad
     const int lg = blockIdx.y;
     const int upr = 4 * a.geo.ksg + 1;
     const int rb = qrow_bytes(a.geo.ksg);
     constexpr int NP = BF ? 1 : 2;
     const int64_t plane_pitch = static_cast<int64_t>(a.qg) * rb;              // one plane of a group slab
-    const int grp = p0 / a.qg;
-    char* slab = static_cast<char*>(a.ws.qrows) + (static_cast<int64_t>(lg) * a.b_pad + grp * a.qg) * NP * rb;
     const int i = tid;
-    if (i < 16 * upr) {
-      const int r = i / upr;
-      const int unit = i - r * upr;
-      const int row_in_grp = p0 - grp * a.qg + r;
-      u16x8 h = u16x8{}, l = u16x8{};
-      bool big = false;
-      const int b = s_b[r];
-      if (b >= 0 && unit < 4 * a.geo.ksg) {
-        // k positions 8*unit .. 8*unit+7 hold the slot runs
-        // 32ks + 4g .. +3 and 32ks + 16 + 4g .. +3 (unit = 4ks + g), the
-        // order in which the scan loads the map quads
-        const int ks = unit / 4;
-        const int gg = unit - 4 * ks;
-        floatx8 v = floatx8{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    const bool staged = i < 16 * upr;
+    const int r = staged ? i / upr : 0;
+    const int unit = i - r * upr;
+    const int b = blockIdx.x * 16 + r;
+    const bool real = staged && b < a.B;
+    const int d = real ? a.depth[b] : 0;
+    // k positions 8*unit .. 8*unit+7 hold the slot runs 32ks + 4g .. +3 and
+    // 32ks + 16 + 4g .. +3 (unit = 4ks + g), the order in which the scan
+    // loads the map quads; layers past the query's depth are zeroed below
+    floatx8 v = floatx8{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    u16x8 h = u16x8{}, l = u16x8{};
+    int layer_of[2] = {a.L, a.L};
+    if (real && unit < 4 * a.geo.ksg) {
+      const int ks = unit / 4;
+      const int gg = unit - 4 * ks;
 #pragma unroll
-        for (int half = 0; half < 2; ++half) {
-          const int s0 = 32 * ks + 16 * half + 4 * gg;
-          const int li = s0 / a.geo.spl;
-          const int e0 = s0 - li * a.geo.spl;
-          const int layer = lg * a.geo.lpg + li;
-          if (layer < s_d[r] && e0 < a.E) {
-            const T* src = q + (static_cast<int64_t>(b) * a.L + layer) * a.E + e0;
-            const int nv = a.E - e0 < 4 ? a.E - e0 : 4;
-            for (int k = 0; k < nv; ++k) {
-              if constexpr (BF) h[4 * half + k] = src[k];
-              else v[4 * half + k] = src[k];
-            }
+      for (int half = 0; half < 2; ++half) {
+        const int s0 = 32 * ks + 16 * half + 4 * gg;
+        const int li = s0 / a.geo.spl;
+        const int e0 = s0 - li * a.geo.spl;
+        const int layer = lg * a.geo.lpg + li;
+        layer_of[half] = layer;
+        if (layer < a.dmax && e0 < a.E) {
+          const T* src = q + (static_cast<int64_t>(b) * a.L + layer) * a.E + e0;
+          const int nv = a.E - e0 < 4 ? a.E - e0 : 4;
+          for (int k = 0; k < nv; ++k) {
+            if constexpr (BF) h[4 * half + k] = src[k];
+            else v[4 * half + k] = src[k];
           }
         }
-        if constexpr (!BF) {
-#pragma unroll
-          for (int k = 0; k < 8; ++k) big = big || __builtin_fabsf(v[k]) > kRangeLimit;
-          split2(v, h, l);
-        }
-      }
-      char* dst = slab + static_cast<int64_t>(row_in_grp) * rb + 16 * unit;
-      *reinterpret_cast<u16x8*>(dst) = h;
-      if constexpr (!BF) {
-        *reinterpret_cast<u16x8*>(dst + plane_pitch) = l;
-        if (big) atomicOr(a.flags, static_cast<uint32_t>(FM_FLAG_VALUE_RANGE));
       }
     }
+    depth_buckets(a.depth, a.B, a.dmax, bits, start);
+    if (!staged) return;
+    const int dc = d < 1 ? 1 : (d > a.dmax ? a.dmax : d);
+    // padding positions B .. b_pad-1 are the padding queries' own indices
+    const int pos = real ? position_of(b, dc, bits, start) : b;
+    bool big = false;
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      if (layer_of[half] >= dc || !real) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          if constexpr (BF) h[4 * half + k] = 0;
+          else v[4 * half + k] = 0.f;
+        }
+      }
+    }
+    if constexpr (!BF) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) big = big || __builtin_fabsf(v[k]) > kRangeLimit;
+      split2(v, h, l);
+    }
+    const int grp = pos / a.qg;
+    char* slab = static_cast<char*>(a.ws.qrows) + (static_cast<int64_t>(lg) * a.b_pad + grp * a.qg) * NP * rb;
+    char* dst = slab + static_cast<int64_t>(pos - grp * a.qg) * rb + 16 * unit;
+    *reinterpret_cast<u16x8*>(dst) = h;
+    if constexpr (!BF) {
+      *reinterpret_cast<u16x8*>(dst + plane_pitch) = l;
+      if (big) atomicOr(a.flags, static_cast<uint32_t>(FM_FLAG_VALUE_RANGE));
+    }
+    if (blockIdx.y == 0 && real && unit == 0 && dc != d) atomicOr(a.flags, static_cast<uint32_t>(FM_FLAG_DEPTH_CLAMPED));
     return;
   }
+  depth_buckets(a.depth, a.B, a.dmax, bits, start);
   const int lane = tid % kWave;
   // Scan workgroups per query group.  Per slice of maps a group's scan takes
   // one stage per layer group its deepest query reaches (position g * qg,
@@ -286,16 +290,19 @@ __global__ void __launch_bounds__(256) k_traj_prep(PrepArgs a) {
       a.ws.ngrp[lane] = nlg_g;
     }
   }
-  // perm, depth and 1/|q[b][0:p]| of the 16 positions: blocks y = nlg ..
-  // nlg+3 take four rows each, one wave per row
-  const int r = (static_cast<int>(blockIdx.y) - a.nlg) * 4 + tid / kWave;
-  const int pos = p0 + r;
-  const int b = s_b[r];
+  // perm, depth and 1/|q[b][0:p]| of queries 16x .. 16x+15: blocks y = nlg ..
+  // nlg+3 take four each, one wave per query, written at the query's sorted
+  // position (padding queries b >= B fill positions b)
+  const int b = blockIdx.x * 16 + (static_cast<int>(blockIdx.y) - a.nlg) * 4 + tid / kWave;
+  const bool real = b < a.B;
+  const int d = real ? a.depth[b] : 0;
+  const int dc = d < 1 ? 1 : (d > a.dmax ? a.dmax : d);
+  const int pos = real ? position_of(b, dc, bits, start) : b;
   double acc = 0.0;
-  if (b >= 0) {
+  if (real) {
     // sixteen independent loads in flight per lane
     constexpr int U = 16;
-    const int cnt = s_d[r] * a.E;
+    const int cnt = dc * a.E;
     const T* row = q + static_cast<int64_t>(b) * a.L * a.E;
     double part[U];
 #pragma unroll
@@ -325,9 +332,9 @@ __global__ void __launch_bounds__(256) k_traj_prep(PrepArgs a) {
     if (acc != acc) rqv = __uint_as_float(0x7fc00000u);
     else if (acc == 0.0) rqv = 0.0f;
     else rqv = static_cast<float>(1.0 / sqrt(acc));
-    a.ws.rq[pos] = b >= 0 ? rqv : 0.0f;
-    a.ws.perm[pos] = b;
-    a.ws.sdep[pos] = b >= 0 ? s_d[r] : 0;
+    a.ws.rq[pos] = real ? rqv : 0.0f;
+    a.ws.perm[pos] = real ? b : -1;
+    a.ws.sdep[pos] = real ? dc : 0;
   }
 }
 
