@@ -125,6 +125,37 @@ def test_depth_clamping_sets_flag():
     assert not rep.failures, rep.failures
 
 
+def test_value_range_flag():
+    """float32 values beyond 8 in magnitude (gate probabilities are at most 1)
+    set FM_FLAG_VALUE_RANGE, from a stored map at insert and from a query
+    row at staging; values at the limit and queries past their depth do not."""
+    import paper_2502_05370_amd as fm
+    s = synth.spec(2).scaled(n=200, B_traj=5)
+    a = synth.generate(s)
+    # at the limit, in a stored map and in an observed query layer: clean
+    a["maps"][3, 2, 5] = 8.0
+    a["q_traj"][0, 0, 0] = -8.0
+    g = run_gpu(s, a)
+    assert not (g.flags & fm._lib.FM_FLAG_VALUE_RANGE)
+    # past a query's depth: never staged, clean
+    a2 = {k: (v.copy() if isinstance(v, np.ndarray) else v) for k, v in a.items()}
+    d = int(np.clip(a2["depth"][1], 1, s.L))
+    if d < s.L:
+        a2["q_traj"][1, d, 0] = 100.0
+        g = run_gpu(s, a2)
+        assert not (g.flags & fm._lib.FM_FLAG_VALUE_RANGE)
+    # inside a query's prefix: flagged
+    a3 = {k: (v.copy() if isinstance(v, np.ndarray) else v) for k, v in a.items()}
+    a3["q_traj"][2, 0, 7] = 9.0
+    g = run_gpu(s, a3)
+    assert g.flags & fm._lib.FM_FLAG_VALUE_RANGE
+    # in a stored map: flagged at insert
+    a4 = {k: (v.copy() if isinstance(v, np.ndarray) else v) for k, v in a.items()}
+    a4["maps"][7, s.L - 1, 0] = -9.5
+    g = run_gpu(s, a4)
+    assert g.flags & fm._lib.FM_FLAG_VALUE_RANGE
+
+
 @pytest.mark.parametrize("tau", [0.0, 0.1, 0.3, 0.5, 0.7, 0.9, 0.99, 1.0])
 def test_threshold_sweep_fixed(tau):
     s = synth.spec(2).scaled(n=800, B_traj=24)
