@@ -61,10 +61,11 @@ struct Geo {
   int32_t ksg;   // 32-slot k-steps per layer group
 };
 
-// Bytes of one staged query plane row: 32*ksg bf16 slots plus one 16-byte pad
-// (a 16-byte-unit stride that is odd, so 16 consecutive rows read at the same
-// column hit distinct LDS banks).
-__host__ __device__ __forceinline__ int qrow_bytes(int ksg) { return 64 * ksg + 16; }
+// Bytes of one staged query plane row: 32*ksg 16-bit slots plus, for ksg > 1,
+// one 16-byte pad (a 16-byte-unit stride that is odd, so 16 consecutive rows
+// read at the same column hit distinct LDS banks; with ksg = 1 a wave's read
+// of 16 rows is one contiguous 1 KB and needs no pad).
+__host__ __device__ __forceinline__ int qrow_bytes(int ksg) { return ksg == 1 ? 64 : 64 * ksg + 16; }
 
 struct PrepArgs {
   const void* q;
@@ -184,9 +185,9 @@ __global__ void __launch_bounds__(256) k_traj_prep(PrepArgs a) {
   // each thread's loads of its query's values are issued before, and land
   // during, the depth sort that tells where the staged row goes.
   if (static_cast<int>(blockIdx.y) < a.nlg) {
-    // one thread per (query row, 8-slot unit); unit 4*ksg of a row is the pad
+    // one thread per (query row, 8-slot unit); unit 4*ksg of a row (ksg > 1) is the pad
     const int lg = blockIdx.y;
-    const int upr = 4 * a.geo.ksg + 1;
+    const int upr = 4 * a.geo.ksg + (a.geo.ksg == 1 ? 0 : 1);
     const int rb = qrow_bytes(a.geo.ksg);
     constexpr int NP = BF ? 1 : 2;
     const int64_t plane_pitch = static_cast<int64_t>(a.qg) * rb;              // one plane of a group slab
@@ -359,7 +360,7 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
   constexpr int QG = 16 * TQ;                 // queries per group
   constexpr int MW = 16 * NBA;                // maps per wave and slice
   constexpr int NP = BF ? 1 : 2;              // MFMA parts per operand (bf16, or two float16)
-  constexpr int RB = 64 * KSG + 16;           // staged query plane row bytes
+  constexpr int RB = KSG == 1 ? 64 : 64 * KSG + 16;   // staged query plane row bytes (qrow_bytes)
   constexpr int NI_Q = (NP * QG * RB + W * 1024 - 1) / (W * 1024);  // 1 KB query loads per wave and stage
   constexpr int Q_STAGE = W * NI_Q * 1024;
   constexpr int NI_A = NBA * KSG * 2;         // map loads per wave and stage (two halves per unit)
