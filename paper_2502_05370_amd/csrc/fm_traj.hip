@@ -61,11 +61,15 @@ struct Geo {
   int32_t ksg;   // 32-slot k-steps per layer group
 };
 
-// Bytes of one staged query plane row: 32*ksg 16-bit slots plus, for ksg > 1,
-// one 16-byte pad (a 16-byte-unit stride that is odd, so 16 consecutive rows
-// read at the same column hit distinct LDS banks; with ksg = 1 a wave's read
-// of 16 rows is one contiguous 1 KB and needs no pad).
-__host__ __device__ __forceinline__ int qrow_bytes(int ksg) { return ksg == 1 ? 64 : 64 * ksg + 16; }
+// Bytes of one staged query plane row: 32*ksg 16-bit slots, in 16-byte
+// units.  With ksg > 1 unit u of row r is stored at unit u ^ (r & 7) of the
+// row, so the 16 rows a wave reads at one logical unit spread over 8 distinct
+// 16-byte bank groups (with ksg = 1 a wave's read of 16 rows is one
+// contiguous 1 KB already).
+__host__ __device__ __forceinline__ int qrow_bytes(int ksg) { return 64 * ksg; }
+__host__ __device__ __forceinline__ int qrow_unit(int ksg, int row, int unit) {
+  return ksg > 1 ? unit ^ (row & 7) : unit;
+}
 
 struct PrepArgs {
   const void* q;
@@ -185,9 +189,9 @@ __global__ void __launch_bounds__(256) k_traj_prep(PrepArgs a) {
   // each thread's loads of its query's values are issued before, and land
   // during, the depth sort that tells where the staged row goes.
   if (static_cast<int>(blockIdx.y) < a.nlg) {
-    // one thread per (query row, 8-slot unit); unit 4*ksg of a row (ksg > 1) is the pad
+    // one thread per (query row, 8-slot unit)
     const int lg = blockIdx.y;
-    const int upr = 4 * a.geo.ksg + (a.geo.ksg == 1 ? 0 : 1);
+    const int upr = 4 * a.geo.ksg;
     const int rb = qrow_bytes(a.geo.ksg);
     constexpr int NP = BF ? 1 : 2;
     const int64_t plane_pitch = static_cast<int64_t>(a.qg) * rb;              // one plane of a group slab
@@ -247,7 +251,8 @@ __global__ void __launch_bounds__(256) k_traj_prep(PrepArgs a) {
     }
     const int grp = pos / a.qg;
     char* slab = static_cast<char*>(a.ws.qrows) + (static_cast<int64_t>(lg) * a.b_pad + grp * a.qg) * NP * rb;
-    char* dst = slab + static_cast<int64_t>(pos - grp * a.qg) * rb + 16 * unit;
+    const int row_in_grp = pos - grp * a.qg;
+    char* dst = slab + static_cast<int64_t>(row_in_grp) * rb + 16 * qrow_unit(a.geo.ksg, row_in_grp, unit);
     *reinterpret_cast<u16x8*>(dst) = h;
     if constexpr (!BF) {
       *reinterpret_cast<u16x8*>(dst + plane_pitch) = l;
@@ -360,7 +365,7 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
   constexpr int QG = 16 * TQ;                 // queries per group
   constexpr int MW = 16 * NBA;                // maps per wave and slice
   constexpr int NP = BF ? 1 : 2;              // MFMA parts per operand (bf16, or two float16)
-  constexpr int RB = KSG == 1 ? 64 : 64 * KSG + 16;   // staged query plane row bytes (qrow_bytes)
+  constexpr int RB = 64 * KSG;                // staged query plane row bytes (qrow_bytes)
   constexpr int NI_Q = (NP * QG * RB + W * 1024 - 1) / (W * 1024);  // 1 KB query loads per wave and stage
   constexpr int Q_STAGE = W * NI_Q * 1024;
   constexpr int NI_A = NBA * KSG * 2;         // map loads per wave and stage (two halves per unit)
@@ -594,7 +599,8 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
       for (int t = 0; t < NT; ++t)
 #pragma unroll
         for (int pl = 0; pl < NP; ++pl)
-          bq[pl][t] = *reinterpret_cast<const u16x8*>(sq + (pl * QG + 16 * t + c) * RB + (32 * ks + 8 * g) * 2);
+          bq[pl][t] = *reinterpret_cast<const u16x8*>(sq + (pl * QG + 16 * t + c) * RB +
+                                                      16 * (KSG > 1 ? (4 * ks + g) ^ (c & 7) : 4 * ks + g));
       if constexpr (BF) {
 #pragma unroll
         for (int t = 0; t < NT; ++t)
@@ -692,7 +698,8 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
             for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
               for (int pl = 0; pl < NP; ++pl)
-                bq[pl][tt] = *reinterpret_cast<const u16x8*>(sq + (pl * QG + 16 * (tc + tt) + c) * RB + (32 * ks + 8 * g) * 2);
+                bq[pl][tt] = *reinterpret_cast<const u16x8*>(sq + (pl * QG + 16 * (tc + tt) + c) * RB +
+                                                             16 * (KSG > 1 ? (4 * ks + g) ^ (c & 7) : 4 * ks + g));
             if constexpr (BF) {
 #pragma unroll
               for (int tt = 0; tt < 4; ++tt)
