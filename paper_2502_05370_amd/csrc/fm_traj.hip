@@ -878,16 +878,17 @@ Geo geometry(int E) {
 }
 
 // 16-map blocks per wave (NBA): two, unless the query group is large; groups
-// of 8 query tiles keep two when one k-step covers a layer group (their
-// accumulators and operands still fit the registers).
-constexpr int scan_nba(int TQ, int KSG) { return (TQ <= 4 || (TQ == 8 && KSG == 1)) ? 2 : 1; }
+// of 8 query tiles keep two when one k-step covers a layer group or the store
+// is bf16 (their accumulators and operands still fit the registers).  Two
+// blocks per wave halve the LDS reads of query fragments per MFMA.
+constexpr int scan_nba(int TQ, int KSG, bool BF) { return (TQ <= 4 || (TQ == 8 && (KSG == 1 || BF))) ? 2 : 1; }
 
 // One inverse-norm table: a row of the slice's 8 * NBA * 16 maps per distinct
 // depth (at most min(QG, dmax) of them), in whole 8 KB chunks (one 1 KB load
 // per wave).
-int scan_rt_bytes(int TQ, int KSG, int dmax) {
+int scan_rt_bytes(int TQ, int KSG, int dmax, bool bf) {
   const int QG = 16 * TQ;
-  const int nba = scan_nba(TQ, KSG);
+  const int nba = scan_nba(TQ, KSG, bf);
   const int rows = QG < dmax ? QG : dmax;
   return (rows * 8 * nba * 16 * 4 + 8 * 1024 - 1) / (8 * 1024) * (8 * 1024);
 }
@@ -903,7 +904,7 @@ size_t scan_lds(bool bf, int TQ, int KSG, int KTOP, int dmax) {
   size_t ring = static_cast<size_t>(3) * 8 * ni_q * 1024;
   const size_t merge = static_cast<size_t>(8) * QG * KTOP * 8;
   if (merge > ring) ring = merge;
-  return ring + 2 * static_cast<size_t>(scan_rt_bytes(TQ, KSG, dmax)) + static_cast<size_t>(5) * QG * 4 +
+  return ring + 2 * static_cast<size_t>(scan_rt_bytes(TQ, KSG, dmax, bf)) + static_cast<size_t>(5) * QG * 4 +
          static_cast<size_t>(8) * ((QG + 63) / 64);
 }
 
@@ -927,16 +928,18 @@ hipError_t scan_launch(const ScanArgs& a, size_t lds, hipStream_t st) {
 }
 
 // Largest query-tile count per workgroup whose registers fit without spills
-// (512 threads leave 256 registers per lane).
+// (512 threads leave 256 registers per lane); for top-1 lists 8 tiles with
+// two blocks per wave beat 16 tiles with one (half the LDS fragment reads
+// per MFMA).
 constexpr int tq_limit(bool bf, int ksg, int ktop) {
-  return ktop == 1 ? (bf ? 16 : 8) : ktop == 4 ? ((bf || ksg == 1) ? 8 : 2) : (bf ? 4 : 2);
+  return ktop == 1 ? 8 : ktop == 4 ? ((bf || ksg == 1) ? 8 : 2) : (bf ? 4 : 2);
 }
 
 // NBA (16-map blocks per wave) follows from TQ and KSG (scan_nba).
 template <bool BF, int KSG, int KTOP, int TQ, bool DBG>
 hipError_t scan_tq1(const ScanArgs& a, size_t lds, hipStream_t st) {
   if constexpr (TQ <= tq_limit(BF, KSG, KTOP))
-    return scan_launch<BF, TQ, scan_nba(TQ, KSG), KSG, KTOP, DBG>(a, lds, st);
+    return scan_launch<BF, TQ, scan_nba(TQ, KSG, BF), KSG, KTOP, DBG>(a, lds, st);
   return hipErrorInvalidValue;
 }
 
@@ -1012,7 +1015,7 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
     // slice epilogue vs stage cost, measured on the top-4 Phi-shaped batch:
     // about 0.16 stage per score kept in a top-4 list, a third of that for
     // top-1
-    pa.epi16 = TQ * scan_nba(TQ, geo.ksg) * 4 * (KTOP == 1 ? 1 : 3);
+    pa.epi16 = TQ * scan_nba(TQ, geo.ksg, bf) * 4 * (KTOP == 1 ? 1 : 3);
     const dim3 pgrid(b_pad / 16, nlg + 4);
     if (bf) hipLaunchKernelGGL(k_traj_prep<true>, pgrid, dim3(kThreads), 0, st, pa);
     else hipLaunchKernelGGL(k_traj_prep<false>, pgrid, dim3(kThreads), 0, st, pa);
@@ -1041,7 +1044,7 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
     a.R = R;
     a.n_blocks = n_blocks;
     a.grid = (G + 7) / 8 * 8;
-    a.rt_bytes = scan_rt_bytes(TQ, geo.ksg, max_depth);
+    a.rt_bytes = scan_rt_bytes(TQ, geo.ksg, max_depth, bf);
     a.ws = ws;
     a.dbg = dbg_scores != nullptr ? dbg_scores + static_cast<int64_t>(b0) * s.n : nullptr;
     if (dbg_scores != nullptr) {
