@@ -9,28 +9,30 @@
 //                   1/|q[b][0:p_b]| (float64 sum) and, for every "layer
 //                   group", the sorted query rows as MFMA-ready planes (two
 //                   float16 parts of each float32 value, one bf16 plane for
-//                   bf16 stores), zero beyond each query's depth and padded,
-//                   so the scan copies them verbatim.
+//                   bf16 stores), zero beyond each query's depth, so the scan
+//                   copies them verbatim; it also shares the scan's
+//                   workgroups among the query groups by their cost.
 //  k_traj_scan      workgroup = one group of 16*TQ sorted queries x an even
-//                   share of the store's 16-map blocks, walked as slices of
-//                   8 waves x NBA blocks.  The map quads of a stage two stages
-//                   ahead load into registers (raw buffer loads), the query
-//                   planes into a three-slot LDS ring (direct global->LDS
-//                   loads); one barrier per stage.  A query tile (16 queries)
-//                   stops at the layer group of its deepest member.  float32
+//                   share of the store (to the map) among the group's
+//                   workgroups, walked as slices of 8 waves x NBA 16-map
+//                   blocks.  The map quads of a stage two stages ahead load
+//                   into registers (raw buffer loads), the query planes into
+//                   a three-slot LDS ring (direct global->LDS loads); one
+//                   barrier per stage.  A query tile (16 queries) stops at
+//                   the layer group of its deepest member.  float32
 //                   operands are scaled by 2^12 and split into two float16
 //                   parts, A = 2^12 a = a1 + a2 + r with |r| <= 2^-22 |A|
 //                   (absolute 2^-25 where a2 falls below the float16 normal
 //                   range), and a.b = 2^-24 (a1b2 + a1b1 + a2b1) accumulates
 //                   on v_mfma_f32_16x16x32_f16 (dropped a2b2 and residuals
 //                   < 3 * 2^-22 |ab| + 2^-37 (|a| + |b|), for |a|, |b| <= 8);
-//                   bf16 stores take one bf16 MFMA.  The slice
-//                   epilogue divides by the query's and the store's prefix
-//                   norms (the latter precomputed at insert), keeps a per-lane
-//                   top-K of packed (score, index) keys, merges it across the
-//                   workgroup and stores it (plain stores) as this workgroup's
-//                   partial list per query.
-//  k_finalize       merges the partial lists of each query into idx/score.
+//                   bf16 stores take one bf16 MFMA.  The slice epilogue
+//                   divides by the query's and the store's prefix norms (the
+//                   latter precomputed at insert and staged per slice in an
+//                   LDS table), keeps a per-lane top-K of packed (score,
+//                   index) keys, merges it across the workgroup and stores it
+//                   (plain stores) as this workgroup's partial list per query.
+//  k_finalize       merges each query's group's partial lists into idx/score.
 //
 // "Slots": each layer's E experts padded to a multiple of 32, or LPG = 32/E
 // layers per 32 slots when E (>= 8) divides 32.  MFMA k position 8g + j of a
