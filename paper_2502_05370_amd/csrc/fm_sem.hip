@@ -112,7 +112,7 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
   uint64_t* mbuf = reinterpret_cast<uint64_t*>(smem);              // after the loop: [W][QG][KTOP]
 
   const int tid = threadIdx.x;
-  const int w = tid / kWave;
+  const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int lane = tid % kWave;
   const int g = lane / 16;
   const int c = lane % 16;
@@ -256,16 +256,21 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
 #pragma unroll
         for (int t = 0; t < TQ; ++t) asm volatile("" : "+v"(bq[ks][t]));
       };
+      // A wave whose blocks all lie past the range (the short last slice of
+      // a workgroup) skips the query reads and MFMAs; it still takes part in
+      // the barriers and issues its share of the loads.
+      if (blk_wave < b_end) {
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) read_q(ks);
+        for (int ks = 0; ks < KS; ++ks) read_q(ks);
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) pin_q(ks);
+        for (int ks = 0; ks < KS; ++ks) pin_q(ks);
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
+        for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-        for (int t = 0; t < TQ; ++t)
+          for (int t = 0; t < TQ; ++t)
 #pragma unroll
-          for (int nb = 0; nb < NBA; ++nb) acc[nb][t] = mfma_bf16(cur[nb][ks], bq[ks][t], acc[nb][t]);
+            for (int nb = 0; nb < NBA; ++nb) acc[nb][t] = mfma_bf16(cur[nb][ks], bq[ks][t], acc[nb][t]);
+      }
       load_a(j + 3, ring_regs, ring_xn);
 
       if (kc == NKC - 1) {
