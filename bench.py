@@ -126,6 +126,9 @@ def parse():
     p.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cold-reps", type=int, default=10,
+                   help="untimed steps after the timed region, each after a 512 MiB read that flushes the "
+                        "256 MB memory-side cache, whose scan events give the cold scan time (0: skip)")
     p.add_argument("--path", default="match", choices=["match", "dedup", "step", "order", "capacity"],
                    help="match: search + selection (default); dedup: deduplicating inserts (Section 4.4); "
                         "step: incremental per-layer trajectory re-search passes (Section 4.2.2); "
@@ -723,15 +726,15 @@ def main():
     timers = {"k_sem_scan": ScanTimer(hip, lib, args.steps) if s.B_sem else None,
               "k_traj_scan": ScanTimer(hip, lib, args.steps) if s.B_traj else None}
 
-    def match(i=None):
+    def match(i=None, tm=timers):
         if s.B_sem:
             if i is not None:
-                timers["k_sem_scan"].arm(i)
+                tm["k_sem_scan"].arm(i)
             fm.match_semantic(store, q_sem, s.k, out=(idx[:s.B_sem], score[:s.B_sem]), workspace=ws_sem,
                               stream=stream)
         if s.B_traj:
             if i is not None:
-                timers["k_traj_scan"].arm(i)
+                tm["k_traj_scan"].arm(i)
             fm.match_trajectory(store, q_traj, depth, s.k, max_depth=max_depth,
                                 out=(idx[s.B_sem:], score[s.B_sem:]), workspace=ws_traj, stream=stream)
         if i is not None:
@@ -763,6 +766,24 @@ def main():
     match_ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
     scan_ms = {k: t.mean_ms(args.steps) for k, t in timers.items() if t is not None}
 
+    # Cold scans (outside the timed region): before each of these steps a
+    # read of 512 MiB, twice the 256 MB memory-side cache, evicts the store's
+    # lines (with clean ones, so no write-back competes with the scan), and
+    # the scan events time reads that come from HBM.
+    cold_ms = {}
+    if args.cold_reps > 0:
+        flush = torch.ones(128 << 20, dtype=torch.int32, device=dev)
+        cold = {k: ScanTimer(hip, lib, args.cold_reps) if t is not None else None for k, t in timers.items()}
+        sink = torch.zeros((), dtype=torch.int32, device=dev)
+        torch.cuda.synchronize()
+        for i in range(args.cold_reps):
+            torch.amax(flush, dim=0, out=sink)
+            match(i, cold)
+            select()
+        torch.cuda.synchronize()
+        cold_ms = {k: t.mean_ms(args.cold_reps) for k, t in cold.items() if t is not None}
+        del flush
+
     # Dominant kernel and its binding roofline: the larger of its algorithmic
     # bytes at the HBM peak and its algorithmic flops at the MFMA peak of the
     # arithmetic it implements (float32 products for float32 maps, bf16
@@ -791,6 +812,13 @@ def main():
     roof["algorithmic_flops"] = flops
     roof["scan_us"] = {k: v * 1e3 for k, v in scan_ms.items()}
     roof["match_call_us"] = match_ms * 1e3
+    if cold_ms:
+        # the same kernel's cold average and the fraction it reaches
+        cold_s = cold_ms[kernel] * 1e-3
+        roof["cold_duration_us"] = cold_ms[kernel] * 1e3
+        roof["cold_frac"] = ((flops / cold_s / 1e12) / fpeak if roof["bound"] == "mfma"
+                             else (byts / cold_s / 1e9) / HBM_PEAK_GBS)
+        roof["cold_scan_us"] = {k: v * 1e3 for k, v in cold_ms.items()}
 
     value = s.B * args.steps / elapsed
     gpu_idx = idx.cpu().numpy()
