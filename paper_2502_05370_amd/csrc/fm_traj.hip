@@ -171,6 +171,21 @@ __device__ __forceinline__ void split2(const floatx8& v, u16x8& h, u16x8& l) {
 
 
 
+// Position of stage j of the scan: slice j / NLG, layer group j % NLG and
+// query ring slot j % NS, stepped from stage to stage without divisions.
+struct StagePos {
+  int j, si, lg, slot;
+};
+__device__ __forceinline__ StagePos next_pos(const StagePos& p, int nlg, int ns) {
+  StagePos q;
+  q.j = p.j + 1;
+  const bool wrap = p.lg + 1 == nlg;
+  q.lg = wrap ? 0 : p.lg + 1;
+  q.si = wrap ? p.si + 1 : p.si;
+  q.slot = p.slot + 1 == ns ? 0 : p.slot + 1;
+  return q;
+}
+
 }  // namespace
 
 // ----------------------------------------------------------------------------- prep
@@ -469,10 +484,10 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
     // group.  Rows past the store, padding quads and layers at or past L use
     // offsets beyond the descriptor's range and read as zeros without
     // touching memory (the row padding itself is stored as zeros).
-    auto load_a = [&](int j, Raw (&dst)[NBA][KSG]) {
-      const bool real = j < nstages;
-      const int si = real ? j / NLG : 0;
-      const int lg = real ? j % NLG : 0;
+    auto load_a = [&](const StagePos& p, Raw (&dst)[NBA][KSG]) {
+      const bool real = p.j < nstages;
+      const int si = real ? p.si : 0;
+      const int lg = real ? p.lg : 0;
       const int l0 = lg * a.geo.lpg;
       const int nl = a.L - l0 < a.geo.lpg ? a.L - l0 : a.geo.lpg;
       const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
@@ -506,10 +521,10 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
         }
       }
     };
-    auto load_q = [&](int j) {
-      const bool real = j < nstages;
-      const int lg = real ? j % NLG : 0;
-      unsigned char* st = ring + (j % NS) * Q_STAGE;
+    auto load_q = [&](const StagePos& p) {
+      const bool real = p.j < nstages;
+      const int lg = real ? p.lg : 0;
+      unsigned char* st = ring + p.slot * Q_STAGE;
       const char* qsl = qrows + (static_cast<int64_t>(lg) * a.b_pad + g0) * NP * RB;
 #pragma unroll
       for (int i = 0; i < NI_Q; ++i) dma16(qsl + (w * NI_Q + i) * 1024 + lane * 16, st + (w * NI_Q + i) * 1024);
@@ -524,11 +539,14 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
     // issue order: Q0 A0 Q1 A1, the prologue's loads, [RT0], then during
     // stage j: [RT] Q(j+2) A(j+2)
     Raw ar0[NBA][KSG], ar1[NBA][KSG];
+    // Stage positions advance incrementally (no division per stage).
+    const StagePos p_first{0, 0, 0, 0};
     if (has_work) {
-      load_q(0);
-      load_a(0, ar0);
-      load_q(1);
-      load_a(1, ar1);
+      load_q(p_first);
+      load_a(p_first, ar0);
+      const StagePos p_second = next_pos(p_first, NLG, NS);
+      load_q(p_second);
+      load_a(p_second, ar1);
     }
     for (int r = tid; r < QG; r += W * kWave) {
       const int pos = g0 + r;
@@ -650,20 +668,21 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
     // wave that may then wait at the barrier while the other wave of its SIMD
     // finishes its MFMAs); after the barrier every wave's query planes of
     // stage j are in LDS.
-    auto stage = [&](int j, Raw (&ring_regs)[NBA][KSG], Raw (&next_regs)[NBA][KSG]) {
-      const int si = j / NLG;
-      const int lg = j % NLG;
+    auto stage = [&](const StagePos& p0, const StagePos& p1, const StagePos& p2, Raw (&ring_regs)[NBA][KSG],
+                     Raw (&next_regs)[NBA][KSG]) {
+      const int si = p0.si;
+      const int lg = p0.lg;
       const int blk_wave = b_begin + si * (W * NBA) + w * NBA;
-      const unsigned char* sq = ring + (j % NS) * Q_STAGE;
+      const unsigned char* sq = ring + p0.slot * Q_STAGE;
 
       raw_barrier();
       // the inverse-norm table of the slice whose last stage is j+1
-      if (j + 1 < nstages && (j + 1) % NLG == NLG - 1) load_rt((j + 1) / NLG);
+      if (p1.j < nstages && p1.lg == NLG - 1) load_rt(p1.si);
       // The query planes of stage j+2 go to slot (j+2) % 3 = (j-1) % 3,
       // which every wave finished reading before this barrier; the map rows
       // of stage j+2 go to the registers of stage j once all of its k-steps
       // are converted.
-      load_q(j + 2);
+      load_q(p2);
 
       const bool last = lg == NLG - 1;
 
@@ -678,7 +697,7 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
 #pragma unroll
       for (int ks = 0; ks < KSG; ++ks) {
         if (ks > 0) convert_ks(ring_regs, ks);
-        if (ks == KSG - 1) load_a(j + 2, ring_regs);
+        if (ks == KSG - 1) load_a(p2, ring_regs);
         if constexpr (TQ == 1) {
           mfma_tiles(std::integral_constant<int, 1>{}, ks, sq, ap);
         } else if constexpr (TQ == 2) {
@@ -770,12 +789,20 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
     if (has_work) {
       wait_vmcnt<NI>();
       convert(ar0);
-      int j = 0;
-      for (; j + 2 <= nstages; j += 2) {
-        stage(j, ar0, ar1);
-        stage(j + 1, ar1, ar0);
+      StagePos p0 = p_first;
+      StagePos p1 = next_pos(p0, NLG, NS);
+      StagePos p2 = next_pos(p1, NLG, NS);
+      for (; p0.j + 2 <= nstages;) {
+        stage(p0, p1, p2, ar0, ar1);
+        p0 = p1;
+        p1 = p2;
+        p2 = next_pos(p2, NLG, NS);
+        stage(p0, p1, p2, ar1, ar0);
+        p0 = p1;
+        p1 = p2;
+        p2 = next_pos(p2, NLG, NS);
       }
-      if (j < nstages) stage(j, ar0, ar1);
+      if (p0.j < nstages) stage(p0, p1, p2, ar0, ar1);
     }
     wait_vmcnt<0>();   // drain the trailing loads
     __syncthreads();
