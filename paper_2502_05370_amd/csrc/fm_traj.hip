@@ -484,15 +484,15 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
     // group.  Rows past the store, padding quads and layers at or past L use
     // offsets beyond the descriptor's range and read as zeros without
     // touching memory (the row padding itself is stored as zeros).
-    auto load_a = [&](const StagePos& p, Raw (&dst)[NBA][KSG]) {
-      const bool real = p.j < nstages;
-      const int si = real ? p.si : 0;
-      const int lg = real ? p.lg : 0;
-      const int l0 = lg * a.geo.lpg;
-      const int nl = a.L - l0 < a.geo.lpg ? a.L - l0 : a.geo.lpg;
-      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-          const_cast<char*>(planes + l0 * a.plane_bytes), static_cast<short>(0),
-          static_cast<int>(static_cast<uint32_t>(nl) * static_cast<uint32_t>(a.plane_bytes)), kBufWord3);
+    // The quad offsets of a slice's map rows are the same in all its layer
+    // groups (only the descriptor's base moves), so they are computed when a
+    // slice's first layer group loads (and for every load past the last
+    // stage, whose offsets are all out of range).  The empty asm makes them
+    // opaque: the loads stay unconditional (the compiler would otherwise
+    // branch around them, and a branch over in-flight loads costs a wait for
+    // every outstanding load).
+    uint32_t offs[NBA][KSG][2];
+    auto set_offsets = [&](bool real, int si) {
 #pragma unroll
       for (int nb = 0; nb < NBA; ++nb) {
         const int blk = b_begin + si * (W * NBA) + w * NBA + nb;
@@ -501,12 +501,29 @@ __global__ void __launch_bounds__(512) k_traj_scan(ScanArgs a) {
         const uint32_t blk_off = static_cast<uint32_t>(blk) * tile_bytes;
 #pragma unroll
         for (int ks = 0; ks < KSG; ++ks) {
-          uint32_t lo = row_ok && quad_ok[ks][0] ? lane_off[ks][0] + blk_off : kOutside;
-          uint32_t hi = row_ok && quad_ok[ks][1] ? lane_off[ks][1] + blk_off : kOutside;
-          // opaque offsets: the loads stay unconditional (the compiler would
-          // otherwise branch around them, and a branch over in-flight loads
-          // costs a wait for every outstanding load)
-          asm volatile("" : "+v"(lo), "+v"(hi));
+#pragma unroll
+          for (int half = 0; half < 2; ++half) {
+            offs[nb][ks][half] = row_ok && quad_ok[ks][half] ? lane_off[ks][half] + blk_off : kOutside;
+            asm volatile("" : "+v"(offs[nb][ks][half]));
+          }
+        }
+      }
+    };
+    auto load_a = [&](const StagePos& p, Raw (&dst)[NBA][KSG]) {
+      const bool real = p.j < nstages;
+      const int lg = real ? p.lg : 0;
+      const int l0 = lg * a.geo.lpg;
+      const int nl = a.L - l0 < a.geo.lpg ? a.L - l0 : a.geo.lpg;
+      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<char*>(planes + l0 * a.plane_bytes), static_cast<short>(0),
+          static_cast<int>(static_cast<uint32_t>(nl) * static_cast<uint32_t>(a.plane_bytes)), kBufWord3);
+      if (!real || p.lg == 0) set_offsets(real, p.si);
+#pragma unroll
+      for (int nb = 0; nb < NBA; ++nb) {
+#pragma unroll
+        for (int ks = 0; ks < KSG; ++ks) {
+          const uint32_t lo = offs[nb][ks][0];
+          const uint32_t hi = offs[nb][ks][1];
           if constexpr (BF) {
             const uint32x2 vl = __builtin_amdgcn_raw_buffer_load_b64(rs, static_cast<int>(lo), 0, 0);
             const uint32x2 vh = __builtin_amdgcn_raw_buffer_load_b64(rs, static_cast<int>(hi), 0, 0);
