@@ -58,10 +58,10 @@ COPY_BYTES_KIB = 262144.0
 COPY_COUNTERS_KIB = {"FETCH_SIZE": 131083.5, "WRITE_SIZE": 262144.0}
 COUNTERS_KIB = {
     # workload: (kernel, FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch
-    "mixtral_traj_n1k": ("k_traj_scan", 611.6, 10.9),
-    "qwen_traj_n50k_b64": ("k_traj_scan", 138794.9, 128.0),
+    "mixtral_traj_n1k": ("k_traj_scan", 610.1, 10.9),
+    "qwen_traj_n50k_b64": ("k_traj_scan", 138797.4, 128.0),
     "semantic_d4096_n100k_b256": ("k_sem_scan", 433391.7, 432.0),
-    "phi_traj_top4_n200k_b512": ("k_traj_scan", 333123.2, 1012.0),
+    "phi_traj_top4_n200k_b512": ("k_traj_scan", 333131.3, 1012.0),
     "qwen_mixed_bf16_n1m_b1024": ("k_sem_scan", 2508757.0, 434.9),
 }
 
