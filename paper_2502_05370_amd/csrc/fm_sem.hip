@@ -51,6 +51,21 @@ struct SemArgs {
   double w_self, w_mix;
 };
 
+// Position of stage j of the semantic scan: slice j / NKC, k-step pair
+// j % NKC and query ring slot j % NS, stepped without divisions.
+struct SemPos {
+  int j, si, kc, slot;
+};
+__device__ __forceinline__ SemPos next_sem_pos(const SemPos& p, int nkc, int ns) {
+  SemPos q;
+  q.j = p.j + 1;
+  const bool wrap = p.kc + 1 == nkc;
+  q.kc = wrap ? 0 : p.kc + 1;
+  q.si = wrap ? p.si + 1 : p.si;
+  q.slot = p.slot + 1 == ns ? 0 : p.slot + 1;
+  return q;
+}
+
 }  // namespace
 
 // One wave per query position: the row is copied 8 dimensions (16 bytes) at a
@@ -152,25 +167,37 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
     // load out of range.
     const __amdgpu_buffer_rsrc_t rs_norm = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<float*>(a.xnorm), static_cast<short>(0), static_cast<int>(static_cast<uint32_t>(a.n) * 4u), kBufWord3);
-    auto load_a = [&](int j, u16x8 (&dst)[NBA][KS], float& dxn) {
-      const bool real = j < nstages;
-      const int si = real ? j / NKC : 0;
-      const int kc = real ? j % NKC : 0;
+    // The descriptor is based at the stage's first k-step in the slice's
+    // first block, so a lane's offsets are the same in every stage of a
+    // slice: they are computed when a slice's first stage loads (and for
+    // every load past the last stage, all out of range) and kept opaque, so
+    // the loads stay unconditional.
+    uint32_t soff[NBA];
+    auto load_a = [&](const SemPos& p, u16x8 (&dst)[NBA][KS], float& dxn) {
+      const bool real = p.j < nstages;
+      const int si = real ? p.si : 0;
+      const int kc = real ? p.kc : 0;
       const int blk0 = b_begin + si * (W * NBA);
-      const int64_t base = static_cast<int64_t>(blk0) * blk_bytes;
+      const int64_t base = static_cast<int64_t>(blk0) * blk_bytes + kc * KS * 1024;
       int64_t rem = a.x_bytes - base;
       if (rem > static_cast<int64_t>(kOutside)) rem = kOutside;
       if (rem < 0) rem = 0;
       const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
           const_cast<char*>(xb + base), static_cast<short>(0), static_cast<int>(static_cast<uint32_t>(rem)), kBufWord3);
+      if (!real || kc == 0) {
+#pragma unroll
+        for (int nb = 0; nb < NBA; ++nb) {
+          const int blk = blk0 + w * NBA + nb;
+          const bool ok = real && blk < b_end && 16 * blk + c < a.n;
+          soff[nb] = ok ? static_cast<uint32_t>((w * NBA + nb) * ksteps * 1024 + lane * 16) : kOutside;
+          asm volatile("" : "+v"(soff[nb]));
+        }
+      }
 #pragma unroll
       for (int nb = 0; nb < NBA; ++nb) {
-        const int blk = blk0 + w * NBA + nb;
-        const bool ok = real && blk < b_end && 16 * blk + c < a.n;
-        const uint32_t base_off = static_cast<uint32_t>(((w * NBA + nb) * ksteps + kc * KS) * 1024 + lane * 16);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          const uint32_t off = ok ? base_off + static_cast<uint32_t>(ks * 1024) : kOutside;
+          const uint32_t off = soff[nb] + static_cast<uint32_t>(ks * 1024);
           dst[nb][ks] = __builtin_bit_cast(u16x8, __builtin_amdgcn_raw_buffer_load_b128(rs, static_cast<int>(off), 0, 0));
         }
       }
@@ -182,10 +209,10 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
     // Query tiles of stage j: tile (t, ks) is 1 KB at slot offset (t*KS+ks) KB;
     // wave w loads tiles w, w+8, ... (wrapping: a repeated tile rewrites
     // identical bytes).
-    auto load_q = [&](int j) {
-      const bool real = j < nstages;
-      const int kc = real ? j % NKC : 0;
-      unsigned char* st = ring + (j % NS) * Q_STAGE;
+    auto load_q = [&](const SemPos& p) {
+      const bool real = p.j < nstages;
+      const int kc = real ? p.kc : 0;
+      unsigned char* st = ring + p.slot * Q_STAGE;
 #pragma unroll
       for (int i = 0; i < NI_Q; ++i) {
         const int tile = (w + W * i) % NQ;
@@ -205,12 +232,17 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
     // issue order: Q0 A0 Q1 A1 Q2 A2, then during stage j: Q(j+3) A(j+3)
     u16x8 ar0[NBA][KS], ar1[NBA][KS], ar2[NBA][KS];
     float xr0, xr1, xr2;
-    load_q(0);
-    load_a(0, ar0, xr0);
-    load_q(1);
-    load_a(1, ar1, xr1);
-    load_q(2);
-    load_a(2, ar2, xr2);
+    // stage positions advance incrementally (no division per stage)
+    SemPos p0{0, 0, 0, 0};
+    SemPos p1 = next_sem_pos(p0, NKC, NS);
+    SemPos p2 = next_sem_pos(p1, NKC, NS);
+    SemPos p3 = next_sem_pos(p2, NKC, NS);
+    load_q(p0);
+    load_a(p0, ar0, xr0);
+    load_q(p1);
+    load_a(p1, ar1, xr1);
+    load_q(p2);
+    load_a(p2, ar2, xr2);
 
     // The map registers of a stage pass through an empty asm placed after
     // the wait for them, so no use of them is scheduled above it (the
@@ -218,7 +250,7 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
     // the prefetch).
     u16x8 cur[NBA][KS];
     float xn_slice = 0.0f;
-    auto take = [&](int j, u16x8 (&ring_regs)[NBA][KS], float& ring_xn) {
+    auto take = [&](const SemPos& p, u16x8 (&ring_regs)[NBA][KS], float& ring_xn) {
       wait_vmcnt<2 * NI>();
 #pragma unroll
       for (int nb = 0; nb < NBA; ++nb) {
@@ -228,21 +260,21 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
           asm volatile("" : "+v"(cur[nb][ks]));
         }
       }
-      if (j % NKC == 0) {
+      if (p.kc == 0) {
         xn_slice = ring_xn;
         asm volatile("" : "+v"(xn_slice));
       }
     };
 
-    auto stage = [&](int j, u16x8 (&ring_regs)[NBA][KS], float& ring_xn, u16x8 (&next_regs)[NBA][KS],
-                     float& next_xn) {
-      const int si = j / NKC;
-      const int kc = j % NKC;
+    auto stage = [&](const SemPos& q0, const SemPos& q1, const SemPos& q3, u16x8 (&ring_regs)[NBA][KS],
+                     float& ring_xn, u16x8 (&next_regs)[NBA][KS], float& next_xn) {
+      const int si = q0.si;
+      const int kc = q0.kc;
       const int blk_wave = b_begin + si * (W * NBA) + w * NBA;
-      const unsigned char* sq = ring + (j % NS) * Q_STAGE;
+      const unsigned char* sq = ring + q0.slot * Q_STAGE;
 
       raw_barrier();
-      load_q(j + 3);
+      load_q(q3);
       // The query tiles of a k-step land in registers of their own before
       // its MFMAs (the empty asm keeps the compiler from reusing one register
       // set per tile, which would serialise one LDS round trip per tile);
@@ -271,7 +303,7 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
 #pragma unroll
             for (int nb = 0; nb < NBA; ++nb) acc[nb][t] = mfma_bf16(cur[nb][ks], bq[ks][t], acc[nb][t]);
       }
-      load_a(j + 3, ring_regs, ring_xn);
+      load_a(q3, ring_regs, ring_xn);
 
       if (kc == NKC - 1) {
         // End of a slice: cosine = dot * 1/|q| * 1/|x|; lane (g, c) holds maps
@@ -313,18 +345,29 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
 #pragma unroll
           for (int t = 0; t < TQ; ++t) acc[nb][t] = floatx4{0.f, 0.f, 0.f, 0.f};
       }
-      take(j + 1, next_regs, next_xn);
+      take(q1, next_regs, next_xn);
+    };
+    auto advance = [&]() {
+      p0 = p1;
+      p1 = p2;
+      p2 = p3;
+      p3 = next_sem_pos(p3, NKC, NS);
     };
 
-    take(0, ar0, xr0);
-    int j = 0;
-    for (; j + 3 <= nstages; j += 3) {
-      stage(j, ar0, xr0, ar1, xr1);
-      stage(j + 1, ar1, xr1, ar2, xr2);
-      stage(j + 2, ar2, xr2, ar0, xr0);
+    take(p0, ar0, xr0);
+    while (p0.j + 3 <= nstages) {
+      stage(p0, p1, p3, ar0, xr0, ar1, xr1);
+      advance();
+      stage(p0, p1, p3, ar1, xr1, ar2, xr2);
+      advance();
+      stage(p0, p1, p3, ar2, xr2, ar0, xr0);
+      advance();
     }
-    if (j < nstages) stage(j, ar0, xr0, ar1, xr1);
-    if (j + 1 < nstages) stage(j + 1, ar1, xr1, ar2, xr2);
+    if (p0.j < nstages) {
+      stage(p0, p1, p3, ar0, xr0, ar1, xr1);
+      advance();
+      if (p0.j < nstages) stage(p0, p1, p3, ar1, xr1, ar2, xr2);
+    }
     wait_vmcnt<0>();   // drain the trailing loads
     __syncthreads();
   }
