@@ -167,24 +167,26 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
     // load out of range.
     const __amdgpu_buffer_rsrc_t rs_norm = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<float*>(a.xnorm), static_cast<short>(0), static_cast<int>(static_cast<uint32_t>(a.n) * 4u), kBufWord3);
-    // The descriptor is based at the stage's first k-step in the slice's
-    // first block, so a lane's offsets are the same in every stage of a
-    // slice: they are computed when a slice's first stage loads (and for
-    // every load past the last stage, all out of range) and kept opaque, so
-    // the loads stay unconditional.
+    // The descriptor (based at the slice's first block) and a lane's offsets
+    // are the same in every stage of a slice: they are set when a slice's
+    // first stage loads (and for every load past the last stage, whose
+    // offsets are all out of range), the offsets kept opaque so the loads
+    // stay unconditional; a stage's k-step pair goes in as the loads' scalar
+    // offset.
     uint32_t soff[NBA];
+    __amdgpu_buffer_rsrc_t rs_slice = rs_norm;
     auto load_a = [&](const SemPos& p, u16x8 (&dst)[NBA][KS], float& dxn) {
       const bool real = p.j < nstages;
       const int si = real ? p.si : 0;
       const int kc = real ? p.kc : 0;
       const int blk0 = b_begin + si * (W * NBA);
-      const int64_t base = static_cast<int64_t>(blk0) * blk_bytes + kc * KS * 1024;
-      int64_t rem = a.x_bytes - base;
-      if (rem > static_cast<int64_t>(kOutside)) rem = kOutside;
-      if (rem < 0) rem = 0;
-      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-          const_cast<char*>(xb + base), static_cast<short>(0), static_cast<int>(static_cast<uint32_t>(rem)), kBufWord3);
       if (!real || kc == 0) {
+        const int64_t base = static_cast<int64_t>(blk0) * blk_bytes;
+        int64_t rem = a.x_bytes - base;
+        if (rem > static_cast<int64_t>(kOutside)) rem = kOutside;
+        if (rem < 0) rem = 0;
+        rs_slice = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(xb + base), static_cast<short>(0),
+                                                     static_cast<int>(static_cast<uint32_t>(rem)), kBufWord3);
 #pragma unroll
         for (int nb = 0; nb < NBA; ++nb) {
           const int blk = blk0 + w * NBA + nb;
@@ -198,7 +200,8 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
           const uint32_t off = soff[nb] + static_cast<uint32_t>(ks * 1024);
-          dst[nb][ks] = __builtin_bit_cast(u16x8, __builtin_amdgcn_raw_buffer_load_b128(rs, static_cast<int>(off), 0, 0));
+          dst[nb][ks] = __builtin_bit_cast(
+              u16x8, __builtin_amdgcn_raw_buffer_load_b128(rs_slice, static_cast<int>(off), kc * KS * 1024, 0));
         }
       }
       // lane l: the norm of map l % 16 of the wave's block (l / 16) % NBA
@@ -209,18 +212,21 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
     // Query tiles of stage j: tile (t, ks) is 1 KB at slot offset (t*KS+ks) KB;
     // wave w loads tiles w, w+8, ... (wrapping: a repeated tile rewrites
     // identical bytes).
+    // this lane's source of each query tile it loads, at the first k-step pair
+    const char* qsrc[NI_Q];
+#pragma unroll
+    for (int i = 0; i < NI_Q; ++i) {
+      const int tile = (w + W * i) % NQ;
+      const int t = tile / KS;
+      const int ks = tile - t * KS;
+      qsrc[i] = qst + ((static_cast<int64_t>(g0 / 16 + t) * ksteps + ks) * 1024) + lane * 16;
+    }
     auto load_q = [&](const SemPos& p) {
       const bool real = p.j < nstages;
       const int kc = real ? p.kc : 0;
       unsigned char* st = ring + p.slot * Q_STAGE;
 #pragma unroll
-      for (int i = 0; i < NI_Q; ++i) {
-        const int tile = (w + W * i) % NQ;
-        const int t = tile / KS;
-        const int ks = tile - t * KS;
-        const char* src = qst + ((static_cast<int64_t>(g0 / 16 + t) * ksteps + kc * KS + ks) * 1024) + lane * 16;
-        dma16(src, st + tile * 1024);
-      }
+      for (int i = 0; i < NI_Q; ++i) dma16(qsrc[i] + kc * KS * 1024, st + ((w + W * i) % NQ) * 1024);
     };
 
     floatx4 acc[NBA][TQ];
