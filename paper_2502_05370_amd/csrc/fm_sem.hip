@@ -172,7 +172,11 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
     // first stage loads (and for every load past the last stage, whose
     // offsets are all out of range), the offsets kept opaque so the loads
     // stay unconditional; a stage's k-step pair goes in as the loads' scalar
-    // offset.
+    // offset.  The descriptor's range ends with the slice's blocks, and lanes
+    // with no row use an offset of 2^31 - 4 KB, which with any scalar offset
+    // of the slice stays past that range without wrapping, so they read
+    // zeros.
+    constexpr uint32_t kNoRow = 0x7FFFF000u;
     uint32_t soff[NBA];
     __amdgpu_buffer_rsrc_t rs_slice = rs_norm;
     auto load_a = [&](const SemPos& p, u16x8 (&dst)[NBA][KS], float& dxn) {
@@ -183,7 +187,7 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
       if (!real || kc == 0) {
         const int64_t base = static_cast<int64_t>(blk0) * blk_bytes;
         int64_t rem = a.x_bytes - base;
-        if (rem > static_cast<int64_t>(kOutside)) rem = kOutside;
+        if (rem > static_cast<int64_t>(W * NBA) * blk_bytes) rem = static_cast<int64_t>(W * NBA) * blk_bytes;
         if (rem < 0) rem = 0;
         rs_slice = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(xb + base), static_cast<short>(0),
                                                      static_cast<int>(static_cast<uint32_t>(rem)), kBufWord3);
@@ -191,7 +195,7 @@ __global__ void __launch_bounds__(512) k_sem_scan(SemArgs a) {
         for (int nb = 0; nb < NBA; ++nb) {
           const int blk = blk0 + w * NBA + nb;
           const bool ok = real && blk < b_end && 16 * blk + c < a.n;
-          soff[nb] = ok ? static_cast<uint32_t>((w * NBA + nb) * ksteps * 1024 + lane * 16) : kOutside;
+          soff[nb] = ok ? static_cast<uint32_t>((w * NBA + nb) * ksteps * 1024 + lane * 16) : kNoRow;
           asm volatile("" : "+v"(soff[nb]));
         }
       }
