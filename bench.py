@@ -60,9 +60,9 @@ COUNTERS_KIB = {
     # workload: (kernel, FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch
     "mixtral_traj_n1k": ("k_traj_scan", 610.1, 10.9),
     "qwen_traj_n50k_b64": ("k_traj_scan", 138797.4, 128.0),
-    "semantic_d4096_n100k_b256": ("k_sem_scan", 433198.1, 432.0),
+    "semantic_d4096_n100k_b256": ("k_sem_scan", 433244.2, 431.9),
     "phi_traj_top4_n200k_b512": ("k_traj_scan", 333131.3, 1012.0),
-    "qwen_mixed_bf16_n1m_b1024": ("k_sem_scan", 2508687.9, 386.0),
+    "qwen_mixed_bf16_n1m_b1024": ("k_sem_scan", 2508540.4, 390.8),
 }
 
 
