@@ -19,7 +19,11 @@ It is a plain, slow, obviously correct restatement of what the paper defines:
   tiny inputs.
 
 Every function is pinned by the ``-m "not gpu"`` tests against closed forms,
-invariants and brute force; none is "parity unpinned".
+invariants and brute force, including the similarity-weighted blend with
+missing matches and NaN weights (against a correctly rounded blend) and the
+searches and redundancy scores over several store chunks (with the chunk size
+made small, against brute force over the whole store).  Each pin is chosen so
+that a planted mistake in the function it covers makes it fail.
 """
 from . import finemoe, brute  # noqa: F401
 from .finemoe import (  # noqa: F401

@@ -138,3 +138,25 @@ def misses_by_enumeration(p: Sequence[float], K: int, chosen: int) -> int:
         if best_key is None or key < best_key:
             best, best_key = S, key
     return sum(1 for j in best if not (chosen >> j) & 1)
+
+
+def blend_fsum(rows: Sequence[Sequence[float]], scores: Sequence[float]) -> List[float]:
+    """Similarity-weighted mean of the given rows with correctly rounded sums:
+    weight max(score, 0), a NaN score weighing 0, and equal weights when every
+    weight is 0 (the blend extension used with several matches)."""
+    w = [0.0 if math.isnan(s) or s <= 0.0 else float(s) for s in scores]
+    if math.fsum(w) == 0.0:
+        w = [1.0] * len(w)
+    den = math.fsum(w)
+    E = len(rows[0])
+    return [math.fsum(w[i] * rows[i][j] for i in range(len(rows))) / den for j in range(E)]
+
+
+def guide_fsum(maps, idx_row: Sequence[int], score_row: Sequence[float], blend: bool, l: int) -> List[float]:
+    """Guiding probabilities of layer l for one query, from a list of stored
+    maps (maps[y][l][j] as Python floats): the best match's row, or with
+    ``blend`` the weighted mean over the matches whose index is not -1."""
+    if not blend:
+        return [float(v) for v in maps[idx_row[0]][l]]
+    keep = [i for i, y in enumerate(idx_row) if y >= 0]
+    return blend_fsum([[float(v) for v in maps[idx_row[i]][l]] for i in keep], [score_row[i] for i in keep])

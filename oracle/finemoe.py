@@ -73,6 +73,20 @@ def _cosine_many(V: np.ndarray, u: np.ndarray) -> np.ndarray:
     return s
 
 
+def _cosine_cols(V: np.ndarray, U: np.ndarray) -> np.ndarray:
+    """Cosine of every row of V [n][m] with every column of U [m][c] (float64),
+    as a [n][c] array, with the conventions of cosine()."""
+    dots = V @ U
+    nv = np.sqrt(np.einsum("ij,ij->i", V, V))[:, None]
+    nu = np.sqrt(np.einsum("ij,ij->j", U, U))[None, :]
+    with np.errstate(invalid="ignore", divide="ignore"):
+        s = dots / (nv * nu)
+    zero = (nv == 0.0) | (nu == 0.0)
+    s[zero & ~np.isnan(dots) & ~np.isnan(nv) & ~np.isnan(nu)] = 0.0
+    s[:, np.isnan(nu[0])] = np.nan
+    return s
+
+
 def trajectory_scores(maps64: np.ndarray, q64: np.ndarray, p: int) -> np.ndarray:
     """Eq. 5: cosine between the observed trajectory of the first ``p`` layers of
     query ``q64`` [L][E] and the same ``p`` layers of every stored map
@@ -81,6 +95,17 @@ def trajectory_scores(maps64: np.ndarray, q64: np.ndarray, p: int) -> np.ndarray
     V = maps64[:, :p, :].reshape(n, p * E)
     u = q64[:p, :].reshape(p * E)
     return _cosine_many(V, u)
+
+
+def trajectory_scores_many(maps64: np.ndarray, Q64: np.ndarray, p: int) -> np.ndarray:
+    """Eq. 5 for several queries observed to the same depth ``p``: [n][c] cosines
+    between the first ``p`` layers of every stored map (maps64 [n][L][E]) and of
+    every query (Q64 [c][L][E]), flattened over (layer, expert).  In a map
+    flattened layer by layer, its first p layers are its first p * E values."""
+    n, L, E = maps64.shape
+    V = np.ascontiguousarray(maps64).reshape(n, L * E)[:, :p * E]
+    U = np.ascontiguousarray(Q64).reshape(Q64.shape[0], L * E)[:, :p * E].T
+    return _cosine_cols(V, U)
 
 
 def semantic_scores(embs64: np.ndarray, qs64: np.ndarray) -> np.ndarray:
@@ -133,9 +158,12 @@ def match_trajectory(maps: np.ndarray, dtype: str, Q: np.ndarray, depth: np.ndar
         b = min(a + _CHUNK, n)
         M = widen(maps[a:b], dtype)
         ids = np.arange(a, b, dtype=np.int64)
+        S = np.empty((b - a, B), dtype=np.float64)
+        for p in np.unique(depth):
+            qs = np.flatnonzero(depth == p)
+            S[:, qs] = trajectory_scores_many(M, Q64[qs], int(p))
         for q in range(B):
-            s = trajectory_scores(M, Q64[q], int(depth[q]))
-            out_i[q], out_s[q] = _merge(out_i[q], out_s[q], ids, s, k)
+            out_i[q], out_s[q] = _merge(out_i[q], out_s[q], ids, S[:, q], k)
     return out_i, out_s
 
 
@@ -151,9 +179,9 @@ def match_semantic(embs: np.ndarray, Qs: np.ndarray, k: int, n: int = None) -> T
         b = min(a + _CHUNK, n)
         X = widen(embs[a:b], "bf16")
         ids = np.arange(a, b, dtype=np.int64)
+        S = _cosine_cols(X, Q64.T)
         for q in range(B):
-            s = semantic_scores(X, Q64[q])
-            out_i[q], out_s[q] = _merge(out_i[q], out_s[q], ids, s, k)
+            out_i[q], out_s[q] = _merge(out_i[q], out_s[q], ids, S[:, q], k)
     return out_i, out_s
 
 

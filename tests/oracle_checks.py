@@ -552,6 +552,134 @@ def check_misses_vs_enumeration(seed=19):
         assert got == ref, (p, K, chosen, got, ref)
 
 
+# ------------------------------------------------------------------ blend glue and chunked search
+
+def _maps_as_lists(maps):
+    return F.widen(maps, "f32").tolist()
+
+
+def check_guide_row_blend(seed=20):
+    """BLEND_SCORE guiding rows against the fsum blend: each weight goes with
+    its own match's row, missing matches (index -1) are skipped even when
+    their score is finite, a NaN score weighs 0, and all-zero weights give
+    the plain mean of the valid rows."""
+    rng = np.random.default_rng(seed)
+    n, L, E = 12, 4, 5
+    maps = _rand_maps(rng, n, L, E)
+    ml = _maps_as_lists(maps)
+    cases = [
+        ([3, 7, 1, 9], [0.9, 0.6, 0.3, 0.05]),        # distinct weights per match
+        ([5, 2, -1, -1], [0.8, 0.4, -np.inf, -np.inf]),  # missing matches
+        ([4, -1, -1, -1], [-0.2, -np.inf, -np.inf, -np.inf]),  # no positive weight: mean of the valid row
+        ([6, 8, -1], [-0.1, 0.0, 0.7]),               # missing match with a finite score is not used
+        ([0, 11, 2], [np.nan, 0.5, 0.25]),            # NaN weighs 0
+        ([1, 10], [np.nan, np.nan]),                  # every weight 0: plain mean
+        ([9, 3, 0], [0.7, -0.3, 0.2]),                # a negative weight is dropped
+    ]
+    for idx_row, sc_row in cases:
+        idx_row = np.array(idx_row)
+        sc_row = np.array(sc_row, dtype=np.float64)
+        for l in range(L):
+            got = F.guide_row(maps, "f32", idx_row, sc_row, F.BLEND_SCORE, l)
+            ref = brute.guide_fsum(ml, idx_row.tolist(), sc_row.tolist(), True, l)
+            assert not np.any(np.isnan(got)), (idx_row, sc_row)
+            assert np.max(np.abs(got - np.array(ref))) <= 4e-16, (idx_row, sc_row, l, got, ref)
+            best = F.guide_row(maps, "f32", idx_row, sc_row, F.BLEND_NONE, l)
+            assert np.array_equal(best, np.array(ml[idx_row[0]][l]))
+    # a single valid match reproduces its row whatever its score (w * x / w
+    # within one rounding of x)
+    for sc in (0.9, 0.0, -0.5, np.nan):
+        got = F.guide_row(maps, "f32", np.array([7, -1]), np.array([sc, -np.inf]), F.BLEND_SCORE, 2)
+        ref = F.widen(maps[7, 2], "f32")
+        assert np.all(np.abs(got - ref) <= 2.0 ** -52 * ref), (sc, got, ref)
+
+
+def check_select_prefetch_blend(seed=21):
+    """select_prefetch with BLEND_SCORE against the fsum blend and subset
+    enumeration of Eq. 6-8, over ragged match lists."""
+    rng = np.random.default_rng(seed)
+    n, L, E, k = 15, 5, 6, 4
+    maps = _rand_maps(rng, n, L, E, zero_frac=0.2)
+    ml = _maps_as_lists(maps)
+    B = 6
+    idx = np.full((B, k), -1, dtype=np.int64)
+    score = np.full((B, k), -np.inf)
+    for b in range(B):
+        m = int(rng.integers(1, k + 1))
+        idx[b, :m] = rng.permutation(n)[:m]
+        score[b, :m] = np.sort(rng.uniform(-0.3, 1.0, m))[::-1]
+    score[2, 1] = np.nan
+    lb = rng.integers(0, L, size=B)
+    le = np.full(B, L)
+    for tau in (0.3, 0.6, 0.85):
+        mask, cnt = F.select_prefetch(maps, "f32", idx, score, lb, le, F.TAU_FIXED, tau, 1, E, F.BLEND_SCORE)
+        t = float(np.float32(tau))
+        for b in range(B):
+            for l in range(L):
+                if l < lb[b]:
+                    assert mask[b, l] == 0 and cnt[b, l] == 0
+                    continue
+                p = brute.guide_fsum(ml, idx[b].tolist(), score[b].tolist(), True, l)
+                kk, S = brute.prefetch_set(p, t, 1, E)
+                assert cnt[b, l] == kk, (tau, b, l)
+                assert int(mask[b, l]) == sum(1 << j for j in S), (tau, b, l)
+
+
+def check_chunked_search(seed=22):
+    """Searches over several store chunks (chunk size set to 7 for 60 stored
+    iterations) against brute force over the whole store; duplicates planted
+    across chunk boundaries keep the lowest index."""
+    rng = np.random.default_rng(seed)
+    old = F._CHUNK
+    F._CHUNK = 7
+    try:
+        n, L, E = 60, 4, 5
+        maps = _rand_maps(rng, n, L, E)
+        maps[45] = maps[3]
+        maps[59] = maps[3]
+        Q = _rand_maps(rng, 5, L, E)
+        Q[0] = maps[3]
+        Q[1] = maps[58]
+        depth = np.array([4, 2, 1, 3, 4])
+        idx, sc = F.match_trajectory(maps, "f32", Q, depth, 3)
+        m64 = F.widen(maps, "f32")
+        q64 = F.widen(Q, "f32")
+        for b in range(5):
+            p = int(depth[b])
+            ref = [brute.cosine_fsum(list(q64[b, :p].ravel()), list(m64[y, :p].ravel())) for y in range(n)]
+            best = brute.best_matches(ref, 3)
+            assert list(idx[b]) == best, (b, list(idx[b]), best)
+            assert all(abs(sc[b, j] - ref[best[j]]) <= 1e-14 for j in range(3))
+        assert list(idx[0]) == [3, 45, 59] and idx[1, 0] == 58
+        X = _bf16(rng.standard_normal((n, 16)))
+        X[33] = X[8]
+        Qs = _bf16(rng.standard_normal((3, 16)))
+        Qs[2] = X[8]
+        idx, sc = F.match_semantic(X, Qs, 4)
+        X64 = F.widen(X, "bf16")
+        Q64 = F.widen(Qs, "bf16")
+        for b in range(3):
+            ref = [brute.cosine_fsum(list(Q64[b]), list(X64[y])) for y in range(n)]
+            assert list(idx[b]) == brute.best_matches(ref, 4), b
+        assert list(idx[2, :2]) == [8, 33]
+        # fewer stored iterations than k across chunks: -1 / -inf fill
+        idx, sc = F.match_trajectory(maps[:9], "f32", Q[:1], depth[:1], 12)
+        assert list(idx[0, 9:]) == [-1, -1, -1] and np.all(np.isneginf(sc[0, 9:]))
+        assert sorted(idx[0, :9].tolist()) == list(range(9))
+        # redundancy over several chunks against the fsum pair formula
+        old_maps, old_embs = maps[:20], _bf16(rng.standard_normal((20, 8)))
+        new_maps, new_embs = maps[40:43], _bf16(rng.standard_normal((3, 8)))
+        r = F.redundancy(old_maps, old_embs, new_maps, new_embs, "f32", 2)
+        om, nm = F.widen(old_maps, "f32"), F.widen(new_maps, "f32")
+        oe, ne = F.widen(old_embs, "bf16"), F.widen(new_embs, "bf16")
+        for x in range(3):
+            for y in range(20):
+                ref = brute.redundancy_fsum(om[y].tolist(), oe[y].tolist(), nm[x].tolist(), ne[x].tolist(), 2)
+                assert abs(r[x, y] - ref) <= 1e-14, (x, y)
+    finally:
+        F._CHUNK = old
+
+
 ALL_CHECKS = [
     check_cosine_vs_fsum, check_cosine_vs_torch, check_self_match, check_disjoint_support,
     check_depth_special_cases, check_unobserved_layers_ignored, check_semantic_vs_fsum,
@@ -562,4 +690,5 @@ ALL_CHECKS = [
     check_research_schedule_depths, check_research_schedule_vs_fsum,
     check_priority_closed_forms, check_priority_vs_brute,
     check_misses_closed_forms, check_misses_vs_enumeration,
+    check_guide_row_blend, check_select_prefetch_blend, check_chunked_search,
 ]

@@ -240,6 +240,76 @@ def activated_one_short(p, K):
     return _orig_activated(p, max(K - 1, 0))
 
 
+_orig_guide_row = F.guide_row
+_orig_blend_rows = F.blend_rows
+
+
+def guide_keeps_missing(maps, dtype, idx_row, score_row, blend, l):
+    if blend != F.BLEND_SCORE:
+        return _orig_guide_row(maps, dtype, idx_row, score_row, blend, l)
+    rows = np.stack([F.widen(maps[idx_row[i]], dtype)[l] for i in range(len(idx_row))])   # -1 reads maps[-1]
+    return F.blend_rows(rows, list(score_row))
+
+
+def guide_top1_weight_for_all(maps, dtype, idx_row, score_row, blend, l):
+    if blend != F.BLEND_SCORE:
+        return _orig_guide_row(maps, dtype, idx_row, score_row, blend, l)
+    valid = [i for i in range(len(idx_row)) if idx_row[i] >= 0]
+    rows = np.stack([F.widen(maps[idx_row[i], l], dtype) for i in valid])
+    return F.blend_rows(rows, [score_row[0]] * len(valid))      # every row weighted by the best score
+
+
+def blend_nan_weight_kept(rows, scores):
+    rows = np.asarray(rows, dtype=np.float64)
+    w = [0.0 if float(s) <= 0.0 else float(s) for s in scores]  # NaN is not <= 0: kept as a NaN weight
+    if sum(w) == 0.0:
+        w = [1.0] * len(w)
+    num = np.zeros(rows.shape[1])
+    den = 0.0
+    for i in range(rows.shape[0]):
+        num = num + w[i] * rows[i]
+        den = den + w[i]
+    return num / den
+
+
+def merge_forgets_earlier_chunks(best_i, best_s, new_i, new_s, k):
+    return F.rank(new_s, k, new_i)
+
+
+_orig_traj_many = F.trajectory_scores_many
+
+
+def cols_missing_sqrt(V, U):
+    dots = V @ U
+    nv = np.einsum("ij,ij->i", V, V)[:, None]          # squared norm used as the norm
+    nu = np.sqrt(np.einsum("ij,ij->j", U, U))[None, :]
+    with np.errstate(invalid="ignore", divide="ignore"):
+        s = dots / (nv * nu)
+    s[((nv == 0) | (nu == 0)) & ~np.isnan(dots)] = 0.0
+    return s
+
+
+def cols_query_norm_of_first(V, U):
+    dots = V @ U
+    nv = np.sqrt(np.einsum("ij,ij->i", V, V))[:, None]
+    nu = math.sqrt(float(U[:, 0] @ U[:, 0]))             # every column divided by the first one's norm
+    with np.errstate(invalid="ignore", divide="ignore"):
+        s = dots / (nv * nu)
+    s[(nv[:, 0] == 0) | (nu == 0)] = 0.0
+    return s
+
+
+def traj_many_prefix_off_by_one(maps64, Q64, p):
+    return _orig_traj_many(maps64, Q64, min(p + 1, maps64.shape[1]))
+
+
+def traj_many_layers_transposed(maps64, Q64, p):
+    n, L, E = maps64.shape
+    V = np.ascontiguousarray(maps64.transpose(0, 2, 1)).reshape(n, L * E)[:, :p * E]   # expert-major flattening
+    U = np.ascontiguousarray(Q64).reshape(Q64.shape[0], L * E)[:, :p * E].T
+    return F._cosine_cols(V, U)
+
+
 MUTANTS = [
     ("select_row", strict_threshold_select),
     ("select_row", high_index_first_select),
@@ -268,6 +338,14 @@ MUTANTS = [
     ("priority_order", evict_by_ratio),
     ("activated", activated_high_index_first),
     ("activated", activated_one_short),
+    ("guide_row", guide_keeps_missing),
+    ("guide_row", guide_top1_weight_for_all),
+    ("blend_rows", blend_nan_weight_kept),
+    ("_merge", merge_forgets_earlier_chunks),
+    ("_cosine_cols", cols_missing_sqrt),
+    ("_cosine_cols", cols_query_norm_of_first),
+    ("trajectory_scores_many", traj_many_prefix_off_by_one),
+    ("trajectory_scores_many", traj_many_layers_transposed),
 ]
 
 
