@@ -37,7 +37,7 @@ def widen(arr: np.ndarray, dtype: str) -> np.ndarray:
     """Exact float64 values of a float32 array or of bf16 bit patterns."""
     if dtype == "bf16":
         a = np.ascontiguousarray(arr, dtype=np.uint16)
-        return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+        return np.left_shift(a, 16, dtype=np.uint32).view(np.float32).astype(np.float64)
     if dtype == "f32":
         return np.asarray(arr, dtype=np.float32).astype(np.float64)
     raise ValueError(dtype)

@@ -45,6 +45,31 @@ def _ptr(t: Optional[torch.Tensor]):
     return None if t is None else C.c_void_p(t.data_ptr())
 
 
+def _need(t, name: str, dtype, shape, device) -> torch.Tensor:
+    """Check a tensor handed to the library: on the store's device,
+    contiguous, of the expected dtype and shape (None in ``shape`` matches any
+    size).  The kernels read and write through raw pointers, so a wrong
+    layout would be read out of bounds instead of failing; raise instead."""
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor, got {type(t).__name__}")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, the store is on {device}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.dim() != len(shape) or any(w is not None and g != w for g, w in zip(t.shape, shape)):
+        want = "x".join("*" if w is None else str(w) for w in shape)
+        raise ValueError(f"{name} must have shape [{want}], got {list(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _dev(store: "Store") -> torch.device:
+    return store.device
+
+
 def _stream(stream) -> C.c_void_p:
     if stream is None:
         stream = torch.cuda.current_stream()
@@ -99,6 +124,8 @@ class Store:
         self.map_dtype = map_dtype
         self.dtype_code = _DTYPES[map_dtype]
         self.device = torch.device(device)
+        if self.device.type == "cuda" and self.device.index is None:
+            self.device = torch.device("cuda", torch.cuda.current_device())
         nbytes = store_bytes(cap, L, E, d_emb, map_dtype)
         if nbytes == 0:
             raise ValueError(f"invalid store shape cap={cap} L={L} E={E} d_emb={d_emb}")
@@ -127,16 +154,12 @@ class Store:
     def insert(self, maps: torch.Tensor, embs: Optional[torch.Tensor] = None, stream=None,
                return_slots: bool = False):
         """Append maps [n][L][E] (and embeddings [n][d_emb] bf16) already on the device."""
-        maps = maps.contiguous()
-        if maps.dtype != _TORCH[self.dtype_code] or maps.dim() != 3 or tuple(maps.shape[1:]) != (self.L, self.E):
-            raise ValueError(f"maps must be [n][{self.L}][{self.E}] {_TORCH[self.dtype_code]}, got "
-                             f"{tuple(maps.shape)} {maps.dtype}")
+        dev = _dev(self)
+        maps = _need(maps.contiguous(), "maps", _TORCH[self.dtype_code], (None, self.L, self.E), dev)
         n = maps.shape[0]
         if embs is not None:
-            embs = embs.contiguous()
-            if embs.dtype != torch.bfloat16 or tuple(embs.shape) != (n, self.d_emb):
-                raise ValueError(f"embs must be [{n}][{self.d_emb}] bfloat16")
-        slots = torch.empty(n, dtype=torch.int32, device=self.device) if return_slots else None
+            embs = _need(embs.contiguous(), "embs", torch.bfloat16, (n, self.d_emb), dev)
+        slots = torch.empty(n, dtype=torch.int32, device=dev) if return_slots else None
         _lib.check(_lib.load().fm_store_insert(self.handle, _ptr(maps), _ptr(embs), n, _ptr(slots),
                                                _stream(stream)), "fm_store_insert")
         return slots
@@ -148,15 +171,11 @@ class Store:
         then replace the most redundant stored iterations (RDY with prefetch
         distance d).  Returns the slot of each new iteration (int32, -1 if
         dropped) on the device."""
-        maps = maps.contiguous()
-        if maps.dtype != _TORCH[self.dtype_code] or maps.dim() != 3 or tuple(maps.shape[1:]) != (self.L, self.E):
-            raise ValueError(f"maps must be [n][{self.L}][{self.E}] {_TORCH[self.dtype_code]}, got "
-                             f"{tuple(maps.shape)} {maps.dtype}")
+        dev = _dev(self)
+        maps = _need(maps.contiguous(), "maps", _TORCH[self.dtype_code], (None, self.L, self.E), dev)
         n = maps.shape[0]
         if embs is not None:
-            embs = embs.contiguous()
-            if embs.dtype != torch.bfloat16 or tuple(embs.shape) != (n, self.d_emb):
-                raise ValueError(f"embs must be [{n}][{self.d_emb}] bfloat16")
+            embs = _need(embs.contiguous(), "embs", torch.bfloat16, (n, self.d_emb), dev)
         ws = workspace if workspace is not None else self.ensure_workspace()
         if scratch is None:
             need = dedup_scratch_bytes(self.cap, max(n, 1))
@@ -204,13 +223,14 @@ class TrajPass:
              out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None, workspace: Optional[Workspace] = None,
              stream=None):
         """q_layer [B][E] (store dtype): every query's gate probabilities at ``layer``."""
-        q_layer = q_layer.contiguous()
-        if tuple(q_layer.shape) != (self.B, self.store.E) or q_layer.dtype != _TORCH[self.store.dtype_code]:
-            raise ValueError(f"q_layer must be [{self.B}][{self.store.E}] {_TORCH[self.store.dtype_code]}")
+        dev = _dev(self.store)
+        _need(q_layer, "q_layer", _TORCH[self.store.dtype_code], (self.B, self.store.E), dev)
         if out is None:
-            out = (torch.empty((self.B, k), dtype=torch.int32, device=self.store.device),
-                   torch.empty((self.B, k), dtype=torch.float32, device=self.store.device))
+            out = (torch.empty((self.B, k), dtype=torch.int32, device=dev),
+                   torch.empty((self.B, k), dtype=torch.float32, device=dev))
         idx, score = out
+        _need(idx, "out[0] (idx)", torch.int32, (self.B, k), dev)
+        _need(score, "out[1] (score)", torch.float32, (self.B, k), dev)
         ws = _ws(self.store, workspace)
         _lib.check(_lib.load().fm_traj_step(self.store.handle, C.c_void_p(self.buf.data_ptr()), self.nbytes,
                                             _ptr(q_layer), int(layer), self.B, k, _ptr(idx), _ptr(score), ws.ptr,
@@ -226,13 +246,18 @@ def match_trajectory(store: Store, q: torch.Tensor, depth: torch.Tensor, k: int 
                      max_depth: Optional[int] = None, out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None,
                      workspace: Optional[Workspace] = None, stream=None):
     """Eq. 5 search: q [B][L][E] (store dtype), depth [B] int32 -> idx [B][k] int32, score [B][k] float32."""
+    dev = _dev(store)
+    _need(q, "q", _TORCH[store.dtype_code], (None, store.L, store.E), dev)
     B = q.shape[0]
+    _need(depth, "depth", torch.int32, (B,), dev)
     if max_depth is None:
         max_depth = store.L
     if out is None:
-        out = (torch.empty((B, k), dtype=torch.int32, device=store.device),
-               torch.empty((B, k), dtype=torch.float32, device=store.device))
+        out = (torch.empty((B, k), dtype=torch.int32, device=dev),
+               torch.empty((B, k), dtype=torch.float32, device=dev))
     idx, score = out
+    _need(idx, "out[0] (idx)", torch.int32, (B, k), dev)
+    _need(score, "out[1] (score)", torch.float32, (B, k), dev)
     ws = _ws(store, workspace)
     _lib.check(_lib.load().fm_match_trajectory(store.handle, _ptr(q), _ptr(depth), max_depth, B, k,
                                                _ptr(idx), _ptr(score), ws.ptr, ws.nbytes, _stream(stream)),
@@ -244,11 +269,15 @@ def match_semantic(store: Store, q: torch.Tensor, k: int = 1,
                    out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None,
                    workspace: Optional[Workspace] = None, stream=None):
     """Eq. 4 search: q [B][d_emb] bfloat16 -> idx [B][k] int32, score [B][k] float32."""
+    dev = _dev(store)
+    _need(q, "q", torch.bfloat16, (None, store.d_emb), dev)
     B = q.shape[0]
     if out is None:
-        out = (torch.empty((B, k), dtype=torch.int32, device=store.device),
-               torch.empty((B, k), dtype=torch.float32, device=store.device))
+        out = (torch.empty((B, k), dtype=torch.int32, device=dev),
+               torch.empty((B, k), dtype=torch.float32, device=dev))
     idx, score = out
+    _need(idx, "out[0] (idx)", torch.int32, (B, k), dev)
+    _need(score, "out[1] (score)", torch.float32, (B, k), dev)
     ws = _ws(store, workspace)
     _lib.check(_lib.load().fm_match_semantic(store.handle, _ptr(q), B, k, _ptr(idx), _ptr(score), ws.ptr,
                                              ws.nbytes, _stream(stream)), "fm_match_semantic")
@@ -260,13 +289,20 @@ def select_prefetch(store: Store, idx: torch.Tensor, score: torch.Tensor, layer_
                     mode: int = FM_TAU_FIXED, blend: int = FM_BLEND_NONE,
                     out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None, stream=None):
     """Eq. 6-8 prefetch sets -> mask [B][L] (int64 holding uint64 bits), count [B][L] uint8."""
+    dev = _dev(store)
+    _need(idx, "idx", torch.int32, (None, None), dev)
     B, k = idx.shape
+    _need(score, "score", torch.float32, (B, k), dev)
+    _need(layer_begin, "layer_begin", torch.int32, (B,), dev)
+    _need(layer_end, "layer_end", torch.int32, (B,), dev)
     if k_max is None:
         k_max = store.E
     if out is None:
-        out = (torch.empty((B, store.L), dtype=torch.int64, device=store.device),
-               torch.empty((B, store.L), dtype=torch.uint8, device=store.device))
+        out = (torch.empty((B, store.L), dtype=torch.int64, device=dev),
+               torch.empty((B, store.L), dtype=torch.uint8, device=dev))
     mask, count = out
+    _need(mask, "out[0] (mask)", torch.int64, (B, store.L), dev)
+    _need(count, "out[1] (count)", torch.uint8, (B, store.L), dev)
     p = SelectParams(mode, tau, k_min, k_max, blend)
     _lib.check(_lib.load().fm_select_prefetch(store.handle, _ptr(idx), _ptr(score), B, k, _ptr(layer_begin),
                                               _ptr(layer_end), C.byref(p), _ptr(mask), _ptr(count),
@@ -281,15 +317,26 @@ def priority_order(store: Store, idx: torch.Tensor, score: torch.Tensor, masks: 
     """Section 4.5 priorities -> order [B][cap] int32 (l * E + j), pri [B][cap] float32, count [B] int32.
     PREFETCH: masks [B][L] (int64 holding uint64 bits) from select_prefetch, l_now [B] int32.
     EVICT: masks [L] (cached experts), freq [L][E] float32."""
+    dev = _dev(store)
+    _need(idx, "idx", torch.int32, (None, None), dev)
     B, k = idx.shape
+    _need(score, "score", torch.float32, (B, k), dev)
+    _need(masks, "masks", torch.int64, (B, store.L) if kind == FM_PRI_PREFETCH else (store.L,), dev)
+    if kind == FM_PRI_PREFETCH:
+        _need(l_now, "l_now", torch.int32, (B,), dev)
+    else:
+        _need(freq, "freq", torch.float32, (store.L, store.E), dev)
     cap = store.L * store.E if cap is None else int(cap)
     if out is None:
-        out = (torch.empty((B, cap), dtype=torch.int32, device=store.device),
-               torch.empty((B, cap), dtype=torch.float32, device=store.device),
-               torch.empty((B,), dtype=torch.int32, device=store.device))
+        out = (torch.empty((B, cap), dtype=torch.int32, device=dev),
+               torch.empty((B, cap), dtype=torch.float32, device=dev),
+               torch.empty((B,), dtype=torch.int32, device=dev))
     order, pri, count = out
+    _need(order, "out[0] (order)", torch.int32, (B, cap), dev)
+    _need(pri, "out[1] (pri)", torch.float32, (B, cap), dev)
+    _need(count, "out[2] (count)", torch.int32, (B,), dev)
     _lib.check(_lib.load().fm_priority_order(store.handle, _ptr(idx), _ptr(score), B, k, blend, kind,
-                                             _ptr(masks.contiguous()), _ptr(l_now), _ptr(freq), cap, _ptr(order),
+                                             _ptr(masks), _ptr(l_now), _ptr(freq), cap, _ptr(order),
                                              _ptr(pri), _ptr(count), _stream(stream)), "fm_priority_order")
     return order, pri, count
 
@@ -298,10 +345,15 @@ def miss_count(store: Store, q: torch.Tensor, masks: torch.Tensor, K: int, layer
                layer_end: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     """Section 3 misses: activated experts (top-K of q [B][L][E], store dtype) outside the sets
     masks [B][L] -> [B][L] uint8 for layers in [layer_begin, layer_end)."""
+    dev = _dev(store)
+    _need(q, "q", _TORCH[store.dtype_code], (None, store.L, store.E), dev)
     B = q.shape[0]
+    _need(masks, "masks", torch.int64, (B, store.L), dev)
+    _need(layer_begin, "layer_begin", torch.int32, (B,), dev)
+    _need(layer_end, "layer_end", torch.int32, (B,), dev)
     if out is None:
-        out = torch.empty((B, store.L), dtype=torch.uint8, device=store.device)
-    q = q.contiguous()
+        out = torch.empty((B, store.L), dtype=torch.uint8, device=dev)
+    _need(out, "out", torch.uint8, (B, store.L), dev)
     _lib.check(_lib.load().fm_miss_count(store.handle, _ptr(q), B, int(K), _ptr(masks), _ptr(layer_begin),
                                          _ptr(layer_end), _ptr(out), _stream(stream)), "fm_miss_count")
     return out
@@ -311,9 +363,15 @@ def debug_scores(store: Store, q: Optional[torch.Tensor] = None, depth: Optional
                  q_sem: Optional[torch.Tensor] = None, max_depth: Optional[int] = None,
                  workspace: Optional[Workspace] = None, stream=None) -> torch.Tensor:
     """Dense float32 scores [B][size] from the same kernels as the match calls (test support)."""
+    dev = _dev(store)
+    if q is not None:
+        _need(q, "q", _TORCH[store.dtype_code], (None, store.L, store.E), dev)
+        _need(depth, "depth", torch.int32, (q.shape[0],), dev)
+    if q_sem is not None:
+        _need(q_sem, "q_sem", torch.bfloat16, (None, store.d_emb), dev)
     B = (q if q is not None else q_sem).shape[0]
     n = store.size
-    out = torch.full((B, max(n, 1)), float("nan"), dtype=torch.float32, device=store.device)
+    out = torch.full((B, max(n, 1)), float("nan"), dtype=torch.float32, device=dev)
     ws = _ws(store, workspace)
     _lib.check(_lib.load().fm_debug_scores(store.handle, _ptr(q), _ptr(depth),
                                            max_depth if max_depth is not None else store.L, _ptr(q_sem), B,
