@@ -224,6 +224,8 @@ class TrajPass:
              stream=None):
         """q_layer [B][E] (store dtype): every query's gate probabilities at ``layer``."""
         dev = _dev(self.store)
+        if isinstance(q_layer, torch.Tensor):
+            q_layer = q_layer.contiguous()
         _need(q_layer, "q_layer", _TORCH[self.store.dtype_code], (self.B, self.store.E), dev)
         if out is None:
             out = (torch.empty((self.B, k), dtype=torch.int32, device=dev),
@@ -321,6 +323,8 @@ def priority_order(store: Store, idx: torch.Tensor, score: torch.Tensor, masks: 
     _need(idx, "idx", torch.int32, (None, None), dev)
     B, k = idx.shape
     _need(score, "score", torch.float32, (B, k), dev)
+    if isinstance(masks, torch.Tensor):
+        masks = masks.contiguous()
     _need(masks, "masks", torch.int64, (B, store.L) if kind == FM_PRI_PREFETCH else (store.L,), dev)
     if kind == FM_PRI_PREFETCH:
         _need(l_now, "l_now", torch.int32, (B,), dev)
@@ -346,6 +350,8 @@ def miss_count(store: Store, q: torch.Tensor, masks: torch.Tensor, K: int, layer
     """Section 3 misses: activated experts (top-K of q [B][L][E], store dtype) outside the sets
     masks [B][L] -> [B][L] uint8 for layers in [layer_begin, layer_end)."""
     dev = _dev(store)
+    if isinstance(q, torch.Tensor):
+        q = q.contiguous()
     _need(q, "q", _TORCH[store.dtype_code], (None, store.L, store.E), dev)
     B = q.shape[0]
     _need(masks, "masks", torch.int64, (B, store.L), dev)
