@@ -215,6 +215,25 @@ fm_status fm_match_trajectory(const fm_store* store, const void* q, const int32_
                               int32_t* idx_out, float* score_out,
                               void* workspace, size_t workspace_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * fm_match_trajectory without a workspace argument.  Its workspace is a
+ * device array of the library of FM_NOALLOC_SCRATCH_BYTES, one per GPU,
+ * which every GPU the call runs on holds until the process ends; its address
+ * is looked up on the first call on each device.  The call allocates and
+ * frees nothing.  Arguments, results, limits and errors as for
+ * fm_match_trajectory, plus FM_ERR_UNSUPPORTED when a trajectory search of
+ * the store's L x E needs more workspace than the array holds (no shape with
+ * L, E <= 64 does) and FM_ERR_HIP when the array's address cannot be
+ * obtained.  All calls on one GPU share the array: calls that overlap in time
+ * on one GPU (other streams, or host threads without ordering) race, and
+ * their results are unspecified.  Nothing in it needs to start at zero
+ * (every call rewrites what it reads). */
+#define FM_NOALLOC_SCRATCH_BYTES (40u << 20)
+fm_status fm_match_trajectory_noalloc(const fm_store* store, const void* q, const int32_t* depth,
+                                      int32_t max_depth, int32_t B, int32_t k, int32_t* idx_out,
+                                      float* score_out, void* stream);
+
 /* Prefetch sets, Section 4.3 (Eq. 6-8): for query b and every layer l in
  * [layer_begin[b], layer_end[b]) (device [B] int32 each, clamped to [0, L]),
  * take the guiding probabilities (fm_blend), the threshold (fm_tau_mode) from

@@ -31,7 +31,7 @@ from ._lib import (FM_BF16, FM_BLEND_NONE, FM_BLEND_SCORE, FM_F32, FM_FLAG_DEPTH
 
 _lib.load()
 
-__all__ = ["Store", "Workspace", "match_semantic", "match_trajectory", "select_prefetch", "priority_order",
+__all__ = ["Store", "Workspace", "match_semantic", "match_trajectory", "match_trajectory_noalloc", "select_prefetch", "priority_order",
            "miss_count",
            "debug_scores",
            "map_bytes", "store_bytes", "workspace_bytes", "dedup_scratch_bytes", "traj_state_bytes", "TrajPass",
@@ -264,6 +264,30 @@ def match_trajectory(store: Store, q: torch.Tensor, depth: torch.Tensor, k: int 
     _lib.check(_lib.load().fm_match_trajectory(store.handle, _ptr(q), _ptr(depth), max_depth, B, k,
                                                _ptr(idx), _ptr(score), ws.ptr, ws.nbytes, _stream(stream)),
                "fm_match_trajectory")
+    return idx, score
+
+
+def match_trajectory_noalloc(store: Store, q: torch.Tensor, depth: torch.Tensor, k: int = 1,
+                             max_depth: Optional[int] = None, out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None,
+                             stream=None):
+    """match_trajectory through the entry point that takes no workspace (the
+    library's own device scratch serves as one); ``out`` must be given by
+    callers that cannot allocate."""
+    dev = _dev(store)
+    _need(q, "q", _TORCH[store.dtype_code], (None, store.L, store.E), dev)
+    B = q.shape[0]
+    _need(depth, "depth", torch.int32, (B,), dev)
+    if max_depth is None:
+        max_depth = store.L
+    if out is None:
+        out = (torch.empty((B, k), dtype=torch.int32, device=dev),
+               torch.empty((B, k), dtype=torch.float32, device=dev))
+    idx, score = out
+    _need(idx, "out[0] (idx)", torch.int32, (B, k), dev)
+    _need(score, "out[1] (score)", torch.float32, (B, k), dev)
+    _lib.check(_lib.load().fm_match_trajectory_noalloc(store.handle, _ptr(q), _ptr(depth), max_depth, B, k,
+                                                       _ptr(idx), _ptr(score), _stream(stream)),
+               "fm_match_trajectory_noalloc")
     return idx, score
 
 

@@ -6,6 +6,7 @@
 
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <new>
 #include <string>
 
@@ -95,14 +96,24 @@ ScanEvents& scan_events() {
 // Workspace layout: [partial][perm][sdep][rq][pgrp][rgrp][ngrp][qrows], each part 256-byte
 // aligned.  qrows holds the staged queries of one launch: the trajectory
 // planes, or the tiled semantic queries (1024 x d_emb bf16).
-size_t workspace_bytes_needed(int32_t L, int32_t E, int32_t d_emb, fm_dtype map_dtype) {
+
+// Parts before the staged queries (partial lists, positions, groups).
+static size_t workspace_fixed_bytes() {
   size_t b = align_up(sizeof(uint64_t) * kChunkB * kMaxPartials * kMaxK, kAlign);
   b += 3 * align_up(sizeof(int32_t) * kChunkB, kAlign);
   b += 3 * align_up(sizeof(int32_t) * (kChunkB / 16), kAlign);
+  return b;
+}
+
+size_t workspace_bytes_needed(int32_t L, int32_t E, int32_t d_emb, fm_dtype map_dtype) {
   const size_t traj = traj_qrows_bytes(L, E, map_dtype, kChunkB);
   const size_t sem = static_cast<size_t>(kChunkB) * d_emb * 2;
-  b += align_up(traj > sem ? traj : sem, kAlign);
-  return b;
+  return workspace_fixed_bytes() + align_up(traj > sem ? traj : sem, kAlign);
+}
+
+// What a trajectory search alone reads and writes of a workspace.
+size_t workspace_bytes_trajectory(int32_t L, int32_t E, fm_dtype map_dtype) {
+  return workspace_fixed_bytes() + align_up(traj_qrows_bytes(L, E, map_dtype, kChunkB), kAlign);
 }
 
 Workspace carve_workspace(void* base) {
@@ -475,6 +486,67 @@ fm_status fm_debug_scores(const fm_store* s, const void* q, const int32_t* depth
     e = fm::launch_match_semantic(s->v, q_sem, B, 1, nullptr, nullptr, scores_out, w, st);
   }
   if (e != hipSuccess) return hip_fail(e, "debug scores launch");
+  return ok();
+}
+
+// ---------------------------------------------------------------- allocation-free trajectory search
+
+}  // extern "C"
+
+namespace {
+
+// Workspace of fm_match_trajectory_noalloc: a device array of the library.
+// Each GPU it runs on holds its own copy until the process ends.  Host code
+// never passes the array's name to a kernel or a copy (on the host it only
+// stands in for the symbol); it uses the device address looked up once per
+// device by scratch_address().
+constexpr size_t kScratchBytes = FM_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on device dev, which must be current.
+fm_status scratch_address(int dev, void** out) {
+  if (dev < 0 || dev >= kMaxDevices) return fail(FM_ERR_UNSUPPORTED, "device %d beyond %d devices", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (ptr == nullptr || reinterpret_cast<uintptr_t>(ptr) % fm::kAlign != 0)
+      return fail(FM_ERR_HIP, "device scratch at %p is not %zu-byte aligned", ptr, fm::kAlign);
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return FM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+fm_status fm_match_trajectory_noalloc(const fm_store* s, const void* q, const int32_t* depth, int32_t max_depth,
+                                      int32_t B, int32_t k, int32_t* idx_out, float* score_out, void* stream) {
+  if (fm_status st = check_store(s)) return st;
+  if (B < 1 || B > 65536) return fail(FM_ERR_INVALID, "B=%d outside [1, 65536]", B);
+  if (k < 1 || k > fm::kMaxK) return fail(FM_ERR_INVALID, "k=%d outside [1, %d]", k, fm::kMaxK);
+  if (idx_out == nullptr || score_out == nullptr) return fail(FM_ERR_INVALID, "idx_out and score_out must be non-NULL");
+  if (q == nullptr || depth == nullptr) return fail(FM_ERR_INVALID, "q and depth must be non-NULL");
+  if (max_depth < 1 || max_depth > s->v.L)
+    return fail(FM_ERR_INVALID, "max_depth=%d outside [1, L=%d]", max_depth, s->v.L);
+  const size_t need = fm::workspace_bytes_trajectory(s->v.L, s->v.E, s->v.map_dtype);
+  if (need > kScratchBytes)
+    return fail(FM_ERR_UNSUPPORTED, "a trajectory search of L=%d x E=%d needs %zu bytes of workspace, beyond the %zu "
+                "bytes of the library's device scratch", s->v.L, s->v.E, need, kScratchBytes);
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(FM_ERR_HIP, "cannot select the store's device %d", s->device);
+  void* ws = nullptr;
+  if (fm_status st = scratch_address(s->device, &ws)) return st;
+  hipError_t e = fm::launch_match_trajectory(s->v, q, depth, max_depth, B, k, idx_out, score_out, nullptr,
+                                             fm::carve_workspace(ws), static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "trajectory match launch");
   return ok();
 }
 

@@ -66,6 +66,7 @@ struct Workspace {
   void* qrows;        // staged query rows of every layer group (trajectory)
 };
 size_t workspace_bytes_needed(int32_t L, int32_t E, int32_t d_emb, fm_dtype map_dtype);
+size_t workspace_bytes_trajectory(int32_t L, int32_t E, fm_dtype map_dtype);
 
 // Scratch of a deduplicating insert: [depth][slots][cand][cand_score] sized
 // for kChunkB new iterations, then the two dense score matrices of n_max x
