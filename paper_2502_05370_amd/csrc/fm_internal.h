@@ -112,6 +112,13 @@ hipError_t launch_match_semantic(const StoreView& s, const void* q, int32_t B, i
                                  int32_t* idx_out, float* score_out, float* dbg_scores,
                                  const Workspace& ws, hipStream_t st, const float* mix = nullptr,
                                  double w_self = 1.0, double w_mix = 0.0);
+// Top-1 semantic scan (fm_sem_mm.hip): queries per group for a chunk of Bc
+// queries, and the scan itself on queries already staged by k_sem_prep
+// (b_pad = groups * queries per group); *R_out receives the partial lists per
+// query for k_finalize.
+int sem_mm_group(int32_t Bc);
+hipError_t launch_sem_mm(const StoreView& s, int32_t Bc, int32_t b_pad, const Workspace& ws, float* dbg, int32_t* R_out,
+                         hipStream_t st);
 hipError_t launch_miss(const StoreView& s, const void* q, int32_t B, int32_t K, const uint64_t* masks,
                        const int32_t* lb, const int32_t* le, uint8_t* miss_out, hipStream_t st);
 hipError_t launch_priority(const StoreView& s, const int32_t* idx, const float* score, int32_t B, int32_t k,

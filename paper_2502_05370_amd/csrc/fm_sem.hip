@@ -472,10 +472,13 @@ hipError_t launch_match_semantic(const StoreView& s, const void* q, int32_t B, i
   // the dense-output form keeps top-1 lists (k = 1)
   const int tq_max = sem_tq_limit(dbg_scores != nullptr ? 1 : KTOP);
   const int n_blocks = (s.n + 15) / 16;
+  // top-1 searches run on the 128 x 128 wave-tile scan (fm_sem_mm.hip)
+  const bool mm = mix == nullptr && (dbg_scores != nullptr || KTOP == 1);
   for (int b0 = 0; b0 < B; b0 += kChunkB) {
     const int Bc = (B - b0) < kChunkB ? (B - b0) : kChunkB;
     int TQ = 1;
     while (16 * TQ < Bc && TQ < tq_max) TQ *= 2;
+    if (mm) TQ = sem_mm_group(Bc) / 16;
     const int QG = 16 * TQ;
     const int n_qg = (Bc + QG - 1) / QG;
     const int b_pad = n_qg * QG;
@@ -490,6 +493,19 @@ hipError_t launch_match_semantic(const StoreView& s, const void* q, int32_t B, i
     hipLaunchKernelGGL(k_sem_prep, dim3((b_pad + 3) / 4), dim3(256), 0, st, pa);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
+
+    if (mm) {
+      int R = 1;
+      err = launch_sem_mm(s, Bc, b_pad, ws, dbg_scores != nullptr ? dbg_scores + static_cast<int64_t>(b0) * s.n : nullptr,
+                          &R, st);
+      if (err != hipSuccess) return err;
+      if (idx_out != nullptr) {
+        err = launch_finalize(ws.partial, nullptr, Bc, R, k, 1, idx_out + static_cast<int64_t>(b0) * k,
+                              score_out + static_cast<int64_t>(b0) * k, st);
+        if (err != hipSuccess) return err;
+      }
+      continue;
+    }
 
     // workgroups per query group: about one workgroup per CU in total, each
     // with an even share of the blocks (at least one)
