@@ -9,28 +9,29 @@
 // insert.  k_sem_prep stages the queries in the embedding tile layout and
 // writes 1/|q| before it runs; k_finalize merges its partial lists after.
 //
-// Workgroup: 4 waves, one per SIMD, arranged GQ x GM over (queries, maps).
-// Wave (wq, wm) holds 128 x 128 float32 accumulators: the group's query
-// tiles 8 wq .. 8 wq + 7 (16 queries each) against the map blocks wm,
-// wm + GM, ... of a slice (16 maps each, interleaved so that a short last
-// slice still splits evenly over the waves).  Per k-step of 32 dimensions a
-// wave reads 16 operand fragments (16 KB) from LDS for 64 MFMAs, i.e. 64
-// bytes per clock per CU at the MFMA rate, half of what a 128 x 32 wave tile
-// needs.
+// Workgroup: 8 waves, two per SIMD (two waves on a SIMD let one issue its
+// LDS reads and copies while the other's MFMAs run), arranged GQ x GM over
+// (queries, maps).  Wave (wq, wm) holds 128 x 64 float32 accumulators: the
+// group's query tiles 8 wq .. 8 wq + 7 (16 queries each) against the map
+// blocks wm, wm + GM, wm + 2 GM, wm + 3 GM of a slice (16 maps each).  Per
+// k-step of 32 dimensions a wave reads 12 operand fragments (12 KB) from LDS
+// for 32 MFMAs.
 //
-// Pipeline: a stage is one k-step of one slice (8 GM blocks of the
+// Pipeline: a stage is one k-step of one slice (4 GM blocks of the
 // workgroup's block range).  Its map tiles and the group's query tiles are
 // 1 KB MFMA operand tiles in HBM (emb_offset), copied global -> LDS by
 // buffer loads straight into ring slot j % NS.  At the start of stage j,
 // once its own copies of stage j+1 have landed, each wave passes the one
 // barrier of the stage; ring slot j % NS, whose fragments every wave already
 // holds in registers, then receives the copies of stage j + NS, and the
-// fragments of stage j+1 are read from LDS while the MFMAs of stage j run.
-// Every stage issues the same number of copies per wave (copies past the
-// last stage use offsets past every descriptor: zeros, no memory traffic),
-// so "stage j+1 has landed" is a fixed vmcnt bound.  The map norms of a
-// slice are copied with its first stage into one of two buffers.
-//
+// fragments of stage j+1 are read from LDS while the MFMAs of stage j run
+// (the map fragments into a second register set, each query fragment into
+// its register as soon as the MFMAs of its tile have read it).  Every stage
+// issues the same copies per wave (copies past the last stage use offsets
+// past every descriptor: zeros, no memory traffic), so "stage j+1 has
+// landed" is a fixed vmcnt bound.  The map norms of a slice are copied with
+// its first stage into one of two buffers.
+
 // Epilogue of a slice: lane (g, c) holds, for block i and query tile t, the
 // dots of maps 4g .. 4g+3 of the block with query c of the tile; the cosine
 // is (dot * 1/|q|) * 1/|x| and the lane keeps the best (score, index) per
@@ -81,36 +82,38 @@ __device__ __forceinline__ MmPos mm_next(const MmPos& p, int ksteps) {
 
 template <int GQ>
 struct MmShape {
-  static constexpr int GM = 4 / GQ;
+  static constexpr int W = 8;                   // waves per workgroup (two per SIMD)
+  static constexpr int GM = W / GQ;
   static constexpr int NT = 8;                  // query tiles per wave
-  static constexpr int NB = 6;                  // map blocks per wave and slice
+  static constexpr int NB = 4;                  // map blocks per wave and slice
   static constexpr int QG = 16 * NT * GQ;       // queries per group
   static constexpr int SB = NB * GM;            // map blocks per slice
-  static constexpr int NS = 4;                  // ring slots
+  static constexpr int NS = GQ == 2 ? 4 : 3;    // ring slots
   static constexpr int TILES = SB + QG / 16;    // 1 KB tiles per stage
-  static constexpr int MPW = SB / 4;            // map tile copies per wave and stage
-  static constexpr int QPW = QG / 64;           // query tile copies per wave and stage
-  static constexpr int NI = MPW + QPW;          // tile copies per wave and stage
+  static constexpr int MPW = SB / W;            // map tile copies per wave and stage
+  static constexpr int QPW = QG / 16 / W;       // query tile copies per wave and stage
+  static constexpr int NI = MPW + QPW + 1;      // copies per wave and stage (tiles, norms)
   static constexpr int SLOT = TILES * 1024;
   static constexpr int NNORM = (SB * 16 * 4 + 1023) / 1024;   // 1 KB copies of one slice's map norms
   static constexpr int NSTRIDE = NNORM * 256;   // floats per norm buffer
-  static constexpr int LDS = NS * SLOT + 2 * NNORM * 1024;
+  static constexpr int LDS = NS * SLOT + 2 * NNORM * 1024 + 1024;   // + a scratch kilobyte
 };
 
 }  // namespace
 
 template <int GQ, bool DBG>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) k_sem_mm(SemMmArgs a) {
+__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) k_sem_mm(SemMmArgs a) {
   using S = MmShape<GQ>;
-  constexpr int GM = S::GM, NT = S::NT, NB = S::NB, QG = S::QG, SB = S::SB, NS = S::NS, NI = S::NI;
+  constexpr int W = S::W, GM = S::GM, NT = S::NT, NB = S::NB, QG = S::QG, SB = S::SB, NS = S::NS, NI = S::NI;
   constexpr int MPW = S::MPW, QPW = S::QPW;
   constexpr int SLOT = S::SLOT, NNORM = S::NNORM, NSTRIDE = S::NSTRIDE;
-  static_assert(SB % 4 == 0 && QG % 64 == 0 && (NS - 1) * NI < 64, "tile copies per stage");
+  static_assert(SB % W == 0 && (QG / 16) % W == 0 && (NS - 1) * NI < 64, "copies per stage");
   static_assert(S::LDS <= 160 * 1024, "LDS");
 
   extern __shared__ __align__(16) unsigned char smem[];
   unsigned char* ring = smem;                                    // [NS][SLOT]
   float* xnb = reinterpret_cast<float*>(smem + NS * SLOT);       // [2][NSTRIDE] map norms
+  float* junk = xnb + 2 * NSTRIDE;                               // [256] target of unneeded norm copies
   uint64_t* mbuf = reinterpret_cast<uint64_t*>(smem);            // after the loop: [GM][QG]
 
   const int tid = threadIdx.x;
@@ -135,7 +138,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))
   const int g0 = qgrp * QG;
   const int ksteps = a.ksteps;
   const int nstages = n_slices * ksteps;
-  const int64_t blk_bytes = static_cast<int64_t>(ksteps) * 1024;
+  const uint32_t blk32 = static_cast<uint32_t>(ksteps) * 1024u;   // bytes of one 16-row block (d < 2^21)
 
   float rqv[NT];
 #pragma unroll
@@ -150,53 +153,51 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))
 
   if (nstages > 0) {
     const char* xb = reinterpret_cast<const char*>(a.x);
-    const char* qbase = reinterpret_cast<const char*>(a.qst) + static_cast<int64_t>(g0 / 16) * blk_bytes;
+    const char* qbase = reinterpret_cast<const char*>(a.qst) + static_cast<uint64_t>(g0 / 16) * blk32;
     const __amdgpu_buffer_rsrc_t rs_q = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<char*>(qbase), static_cast<short>(0),
-        static_cast<int>(static_cast<uint32_t>(QG / 16) * static_cast<uint32_t>(blk_bytes)), kBufWord3);
+        const_cast<char*>(qbase), static_cast<short>(0), static_cast<int>(static_cast<uint32_t>(QG / 16) * blk32),
+        kBufWord3);
     const __amdgpu_buffer_rsrc_t rs_norm = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<float*>(a.xnorm), static_cast<short>(0), static_cast<int>(static_cast<uint32_t>(a.n) * 4u),
         kBufWord3);
 
-    // Copies of the stage at position p into its ring slot.  Map tiles go
-    // through a descriptor based at the slice's first block whose range ends
-    // with the workgroup's blocks (rebuilt at each slice's first stage), so
-    // blocks past the range read as zeros; positions past the last stage use
-    // offsets past every descriptor.
-    __amdgpu_buffer_rsrc_t rs_slice = rs_norm;
+    // Copies of the stage at position p into its ring slot, branch-free so
+    // that they can be placed between the MFMAs: the map tiles through a
+    // descriptor based at the slice's first block whose range ends with the
+    // workgroup's blocks (blocks past it read as zeros), the query tiles
+    // through rs_q, positions past the last stage with offsets past every
+    // descriptor; every stage also issues the norm copy, into a scratch
+    // kilobyte of LDS except at a slice's first stage.
     auto load_stage = [&](const MmPos& p) __attribute__((always_inline)) {
       const bool real = p.j < nstages;
-      if (!real || p.ks == 0) {
-        const int blk0 = b_begin + (real ? p.si : 0) * SB;
-        int64_t rem = real ? static_cast<int64_t>(b_end - blk0) * blk_bytes : 0;
-        if (rem > static_cast<int64_t>(SB) * blk_bytes) rem = static_cast<int64_t>(SB) * blk_bytes;
-        rs_slice = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(xb + static_cast<int64_t>(blk0) * blk_bytes),
-                                                     static_cast<short>(0),
-                                                     static_cast<int>(static_cast<uint32_t>(rem)), kBufWord3);
-      }
+      const int blk0 = b_begin + p.si * SB;
+      int nbk = b_end - blk0;
+      nbk = nbk < 0 ? 0 : (nbk > SB ? SB : nbk);
+      nbk = __builtin_amdgcn_readfirstlane(real ? nbk : 0);   // wave-uniform: a scalar descriptor
+      const __amdgpu_buffer_rsrc_t rs_slice = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<char*>(xb + static_cast<uint64_t>(static_cast<uint32_t>(blk0)) * blk32), static_cast<short>(0),
+          static_cast<int>(static_cast<uint32_t>(nbk) * blk32), kBufWord3);
       unsigned char* slot = ring + p.slot * SLOT;
-      const uint32_t kofs = real ? static_cast<uint32_t>(p.ks * 1024 + lane * 16) : kOutside;
-      // wave w copies map tiles w * MPW .. and query tiles w * QPW ..
+      const uint32_t kofs = static_cast<uint32_t>(p.ks * 1024 + lane * 16);
 #pragma unroll
       for (int i = 0; i < MPW; ++i) {
         const int tile = w * MPW + i;
-        const uint32_t off = real ? static_cast<uint32_t>(tile) * static_cast<uint32_t>(blk_bytes) + kofs : kOutside;
+        const uint32_t off = real ? static_cast<uint32_t>(tile) * blk32 + kofs : kOutside;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_slice, (lds_vp)(slot + tile * 1024), 16, static_cast<int>(off), 0, 0,
                                                  0);
       }
 #pragma unroll
       for (int i = 0; i < QPW; ++i) {
         const int tile = w * QPW + i;
-        const uint32_t off = real ? static_cast<uint32_t>(tile) * static_cast<uint32_t>(blk_bytes) + kofs : kOutside;
+        const uint32_t off = real ? static_cast<uint32_t>(tile) * blk32 + kofs : kOutside;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_q, (lds_vp)(slot + (SB + tile) * 1024), 16, static_cast<int>(off), 0,
                                                  0, 0);
       }
-      // the slice's map norms, with its first stage
-      if (real && p.ks == 0 && w < NNORM) {
-        const uint32_t off = static_cast<uint32_t>(((b_begin + p.si * SB) * 16 + w * 256 + lane * 4) * 4);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_norm, (lds_vp)(xnb + (p.si & 1) * NSTRIDE + w * 256), 16,
-                                                 static_cast<int>(off), 0, 0, 0);
-      }
+      const bool norm = real && p.ks == 0 && w < NNORM;
+      const uint32_t noff =
+          norm ? static_cast<uint32_t>(((b_begin + p.si * SB) * 16 + w * 256 + lane * 4) * 4) : kOutside;
+      float* ndst = norm ? xnb + (p.si & 1) * NSTRIDE + w * 256 : junk;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_norm, (lds_vp)(ndst), 16, static_cast<int>(noff), 0, 0, 0);
     };
 
     floatx4 acc[NB][NT];
@@ -205,12 +206,11 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))
 #pragma unroll
       for (int t = 0; t < NT; ++t) acc[i][t] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    auto read_frags = [&](int slot, u16x8 (&fa)[NB], u16x8 (&fb)[NT]) __attribute__((always_inline)) {
-      const unsigned char* sp = ring + slot * SLOT + lane * 16;
-#pragma unroll
-      for (int i = 0; i < NB; ++i) fa[i] = *reinterpret_cast<const u16x8*>(sp + (wm + GM * i) * 1024);
-#pragma unroll
-      for (int t = 0; t < NT; ++t) fb[t] = *reinterpret_cast<const u16x8*>(sp + (SB + NT * wq + t) * 1024);
+    auto read_mfrag = [&](int slot, int i) __attribute__((always_inline)) {
+      return *reinterpret_cast<const u16x8*>(ring + slot * SLOT + lane * 16 + (wm + GM * i) * 1024);
+    };
+    auto read_qfrag = [&](int slot, int t) __attribute__((always_inline)) {
+      return *reinterpret_cast<const u16x8*>(ring + slot * SLOT + lane * 16 + (SB + NT * wq + t) * 1024);
     };
 
     // Slice epilogue: scores of this wave's blocks of slice si, best per query.
@@ -221,10 +221,18 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))
       for (int i = 0; i < NB; ++i) {
         const int blk = blk_s + wm + GM * i;
         if (blk >= b_end) break;
-        const floatx4 xn = *reinterpret_cast<const floatx4*>(xn_s + (wm + GM * i) * 16 + 4 * g);
+        // The norms were copied into LDS with the slice's first stage, and
+        // the stage waits have covered that copy; a plain LDS read here would
+        // make the compiler wait for every copy still in flight, so the read
+        // is written out, with its own wait that the value depends on.
+        floatx4 xn;
+        const uint32_t xaddr = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(xn_s + (wm + GM * i) * 16 + 4 * g));
+        asm volatile("ds_read_b128 %0, %1" : "=v"(xn) : "v"(xaddr));
+        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(xn));
+        // 1/|x| (within one unit in the last place; 0 for a zero norm, NaN for NaN)
         float rx[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) rx[r] = xn[r] > 0.0f ? 1.0f / xn[r] : (xn[r] != xn[r] ? xn[r] : 0.0f);
+        for (int r = 0; r < 4; ++r) rx[r] = xn[r] > 0.0f ? __builtin_amdgcn_rcpf(xn[r]) : (xn[r] != xn[r] ? xn[r] : 0.0f);
         const int y0 = 16 * blk + 4 * g;
         const bool full = 16 * blk + 16 <= a.n;
 #pragma unroll
@@ -248,15 +256,10 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))
         // one block's accumulators at a time
         __builtin_amdgcn_sched_barrier(0);
       }
-      // the next slice accumulates from zero; the empty asm keeps the
-      // compiler from treating the accumulators as known zeros (it would
-      // then build the first MFMAs of a slice from a shared zero register)
 #pragma unroll
       for (int i = 0; i < NB; ++i)
 #pragma unroll
-        for (int t = 0; t < NT; ++t) {
-          acc[i][t] = floatx4{0.f, 0.f, 0.f, 0.f};
-        }
+        for (int t = 0; t < NT; ++t) acc[i][t] = floatx4{0.f, 0.f, 0.f, 0.f};
     };
 
     // prologue: the copies of stages 0 .. NS-1, then stage 0's fragments
@@ -266,80 +269,60 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))
       load_stage(pl);
       pl = mm_next<NS>(pl, ksteps);
     }
-    u16x8 fa0[NB], fb0[NT], fa1[NB], fb1[NT];
+    u16x8 fa0[NB], fa1[NB], fb[NT];
     wait_vmcnt<(NS - 1) * NI>();
     raw_barrier();
-    read_frags(0, fa0, fb0);
+#pragma unroll
+    for (int i = 0; i < NB; ++i) fa0[i] = read_mfrag(0, i);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) fb[t] = read_qfrag(0, t);
     wait_lgkm0();
 
-    // One stage: MFMAs of the first NBV blocks from fragments (fa, fb),
-    // copies of stage j + NS, fragments of stage j+1 into (na, nb).  The
-    // accumulators of blocks NBV.. are left alone (zero in a short slice).
+    // One stage j: the copies of stage j + NS into slot j % NS (every wave
+    // holds stage j's fragments, read during stage j-1, before this stage's
+    // barrier); stage j+1's map fragments into na; per query tile the MFMAs
+    // of stage j, then that tile's fragment of stage j+1 into the register
+    // its MFMAs have just read. Blocks past the workgroup's range read as
+    // zeros and their scores are never looked at, so a short last slice runs
+    // the same code.
     int slot_next = 1 % NS;
-    int nbv_rt = NB;   // blocks of this wave in a short slice
-    auto stage = [&](auto nbv_const, u16x8 (&fa)[NB], u16x8 (&fb)[NT], u16x8 (&na)[NB], u16x8 (&nb)[NT])
-                     __attribute__((always_inline)) {
-      constexpr int NBV = decltype(nbv_const)::value;
-      // stage j+1's copies have landed (this wave's, then everyone's), and
-      // every wave holds stage j's fragments: slot j % NS is free
+    auto stage = [&](u16x8 (&fa)[NB], u16x8 (&na)[NB]) __attribute__((always_inline)) {
+      // stage j+1's copies have landed (this wave's, then everyone's)
       wait_vmcnt<(NS - 2) * NI>();
       raw_barrier();
       load_stage(pl);
       pl = mm_next<NS>(pl, ksteps);
-      read_frags(slot_next, na, nb);
+      const int sn = slot_next;
       slot_next = slot_next + 1 == NS ? 0 : slot_next + 1;
-      if constexpr (NBV == NB) {
 #pragma unroll
-        for (int i = 0; i < NB; ++i)
+      for (int i = 0; i < NB; ++i) na[i] = read_mfrag(sn, i);
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-          for (int t = 0; t < NT; ++t) acc[i][t] = mfma_bf16(fa[i], fb[t], acc[i][t]);
-        // issue order: the copies and the fragment reads spread between the
-        // stage's MFMAs, then the wait for the reads
-        constexpr int NR = NB + NT;                    // fragment reads
-        constexpr int NM = NB * NT;                    // MFMAs
-        constexpr int PER = NM / (NI + NR) > 0 ? NM / (NI + NR) : 1;
+      for (int t = 0; t < NT; ++t) {
 #pragma unroll
-        for (int k = 0; k < NI; ++k) {
-          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // one copy
-          __builtin_amdgcn_sched_group_barrier(0x008, PER, 0); // MFMAs
-        }
-#pragma unroll
-        for (int k = 0; k < NR; ++k) {
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one fragment read
-          __builtin_amdgcn_sched_group_barrier(0x008, PER, 0); // MFMAs
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);    // the remaining MFMAs
-      } else {
-        // the short last slice: only the blocks below b_end (nbv_rt of them)
-#pragma unroll
-        for (int i = 0; i < NB; ++i) {
-          if (i < nbv_rt) {
-#pragma unroll
-            for (int t = 0; t < NT; ++t) acc[i][t] = mfma_bf16(fa[i], fb[t], acc[i][t]);
-          }
-        }
+        for (int i = 0; i < NB; ++i) acc[i][t] = mfma_bf16(fa[i], fb[t], acc[i][t]);
+        fb[t] = read_qfrag(sn, t);
       }
+      // issue order: the copies, the map fragment reads, then per query
+      // tile its MFMAs and its next fragment
+      __builtin_amdgcn_sched_group_barrier(0x020, NI, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, NB, 0);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        __builtin_amdgcn_sched_group_barrier(0x008, NB, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_s_setprio(0);
       __builtin_amdgcn_sched_barrier(0);
       wait_lgkm0();
     };
-    // all k-steps of one slice (ksteps is a multiple of 4)
-    auto slice = [&](auto nbv_const) __attribute__((always_inline)) {
+    for (int si = 0; si < n_slices; ++si) {
+      // all k-steps of one slice (ksteps is even)
       for (int ks = 0; ks < ksteps; ks += 2) {
-        stage(nbv_const, fa0, fb0, fa1, fb1);
-        stage(nbv_const, fa1, fb1, fa0, fb0);
+        stage(fa0, fa1);
+        stage(fa1, fa0);
       }
-    };
-    const int n_full = (b_end - b_begin) / SB;
-    for (int si = 0; si < n_full; ++si) {
-      slice(std::integral_constant<int, NB>{});
       epilogue(si);
-    }
-    if (n_full < n_slices) {
-      // the short last slice: this wave's blocks wm, wm + GM, ... below b_end
-      const int rem = b_end - (b_begin + n_full * SB) - wm;
-      nbv_rt = rem <= 0 ? 0 : (rem + GM - 1) / GM;
-      slice(std::integral_constant<int, 0>{});
-      epilogue(n_full);
     }
     wait_vmcnt<0>();   // the trailing copies
   }
@@ -362,7 +345,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))
   }
   __syncthreads();
   if (active) {
-    for (int r = tid; r < QG; r += 4 * kWave) {
+    for (int r = tid; r < QG; r += W * kWave) {
       uint64_t m = 0;
 #pragma unroll
       for (int ww = 0; ww < GM; ++ww) m = mbuf[ww * QG + r] > m ? mbuf[ww * QG + r] : m;
@@ -385,7 +368,7 @@ hipError_t sem_mm_launch(const SemMmArgs& a, hipStream_t st) {
     err = hipEventRecord(ev.start, st);
     if (err != hipSuccess) return err;
   }
-  hipLaunchKernelGGL(kern, dim3(a.grid), dim3(256), lds, st, a);
+  hipLaunchKernelGGL(kern, dim3(a.grid), dim3(MmShape<GQ>::W * kWave), lds, st, a);
   err = hipGetLastError();
   if (err != hipSuccess || ev.stop == nullptr) return err;
   return hipEventRecord(ev.stop, st);
