@@ -23,7 +23,7 @@ OUT = os.path.join(HERE, "libfinemoe_map.so")
 BUILD_DIR = os.path.join(HERE, "_build")
 ARCH = "gfx950"
 
-SOURCES = ["fm_api.cpp", "fm_store.hip", "fm_traj.hip", "fm_sem.hip", "fm_sem_mm.hip", "fm_select.hip", "fm_dedup.hip", "fm_step.hip", "fm_priority.hip"]
+SOURCES = ["fm_api.cpp", "fm_store.hip", "fm_traj.hip", "fm_sem.hip", "fm_sem_mm.hip", "fm_traj_mm.hip", "fm_select.hip", "fm_dedup.hip", "fm_step.hip", "fm_priority.hip"]
 
 # Packed float32 instructions are kept out of every kernel; hipcc's host pass
 # warns that it does not know the feature, which is harmless.

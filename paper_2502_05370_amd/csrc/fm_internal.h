@@ -119,6 +119,14 @@ hipError_t launch_match_semantic(const StoreView& s, const void* q, int32_t B, i
 int sem_mm_group(int32_t Bc);
 hipError_t launch_sem_mm(const StoreView& s, int32_t Bc, int32_t b_pad, const Workspace& ws, float* dbg, int32_t* R_out,
                          hipStream_t st);
+// Top-1 trajectory scan of bf16 stores (fm_traj_mm.hip): whether a chunk of
+// Bc queries takes it, its queries per group, and the scan itself on queries
+// staged by k_traj_prep in its tiled layout (b_pad = groups * queries per
+// group); *R_out receives the partial lists per query for k_finalize.
+bool traj_mm_fits(bool bf, int KTOP, int32_t Bc, int32_t max_depth, int nlg, int ksg);
+int traj_mm_group();
+hipError_t launch_traj_mm(const StoreView& s, int spl, int lpg, int ksg, int nlg, int32_t max_depth, int32_t b_pad,
+                          const Workspace& ws, float* dbg, int32_t* R_out, hipStream_t st);
 hipError_t launch_miss(const StoreView& s, const void* q, int32_t B, int32_t K, const uint64_t* masks,
                        const int32_t* lb, const int32_t* le, uint8_t* miss_out, hipStream_t st);
 hipError_t launch_priority(const StoreView& s, const int32_t* idx, const float* score, int32_t B, int32_t k,

@@ -84,6 +84,7 @@ struct PrepArgs {
   int32_t n_qg;       // query groups
   int32_t G;          // scan workgroups to share among the groups
   int32_t epi16;      // a slice epilogue's cost in sixteenths of a stage's
+  int32_t tiled;      // bf16 only: stage for k_traj_mm (MFMA operand tiles, groups interleaved)
   Workspace ws;
   uint32_t* flags;
 };
@@ -265,6 +266,22 @@ __global__ void __launch_bounds__(256) k_traj_prep(PrepArgs a) {
 #pragma unroll
       for (int k = 0; k < 8; ++k) big = big || __builtin_fabsf(v[k]) > kRangeLimit;
       split2(v, h, l);
+    }
+    if (BF && a.tiled) {
+      // k_traj_mm layout: sorted tile T = pos / 16 is local tile T / n_qg of
+      // group T % n_qg; the 1 KB operand tile of (layer group, k-step, group,
+      // local tile) holds this unit at lane slot 16 g + c
+      const int T = pos / 16;
+      const int tg = T % a.n_qg;
+      const int tl = T / a.n_qg;
+      const int ks = unit / 4;
+      const int gg = unit - 4 * ks;
+      char* dst = static_cast<char*>(a.ws.qrows) +
+                  ((((static_cast<int64_t>(lg) * a.geo.ksg + ks) * a.n_qg + tg) * 16 + tl) * 1024) +
+                  (gg * 16 + pos % 16) * 16;
+      *reinterpret_cast<u16x8*>(dst) = h;
+      if (blockIdx.y == 0 && real && unit == 0 && dc != d) atomicOr(a.flags, static_cast<uint32_t>(FM_FLAG_DEPTH_CLAMPED));
+      return;
     }
     const int grp = pos / a.qg;
     char* slab = static_cast<char*>(a.ws.qrows) + (static_cast<int64_t>(lg) * a.b_pad + grp * a.qg) * NP * rb;
@@ -1027,8 +1044,45 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
   const int tq_max = tq_limit(bf, geo.ksg, KTOP);
   constexpr size_t kLds = 160 * 1024;
 
+  const int nlg = (max_depth + geo.lpg - 1) / geo.lpg;
   for (int b0 = 0; b0 < B; b0 += kChunkB) {
     const int Bc = (B - b0) < kChunkB ? (B - b0) : kChunkB;
+    if (traj_mm_fits(bf, KTOP, Bc, max_depth, nlg, geo.ksg)) {
+      // bf16 top-1 (or dense) batches of more than 128 queries: k_traj_mm
+      const int QG = traj_mm_group();
+      const int n_qg = (Bc + QG - 1) / QG;
+      const int b_pad = n_qg * QG;
+      PrepArgs pa{};
+      pa.q = static_cast<const char*>(q) + static_cast<int64_t>(b0) * s.L * s.E * esz;
+      pa.depth = depth + b0;
+      pa.B = Bc;
+      pa.L = s.L;
+      pa.E = s.E;
+      pa.dmax = max_depth;
+      pa.geo = geo;
+      pa.nlg = nlg;
+      pa.b_pad = b_pad;
+      pa.qg = QG;
+      pa.n_qg = n_qg;
+      pa.G = n_qg;
+      pa.epi16 = 0;
+      pa.tiled = 1;
+      pa.ws = ws;
+      pa.flags = s.flags;
+      hipLaunchKernelGGL(k_traj_prep<true>, dim3(b_pad / 16, nlg + 4), dim3(kThreads), 0, st, pa);
+      hipError_t err = hipGetLastError();
+      if (err != hipSuccess) return err;
+      int32_t R = 0;
+      err = launch_traj_mm(s, geo.spl, geo.lpg, geo.ksg, nlg, max_depth, b_pad, ws,
+                           dbg_scores != nullptr ? dbg_scores + static_cast<int64_t>(b0) * s.n : nullptr, &R, st);
+      if (err != hipSuccess) return err;
+      if (idx_out != nullptr) {
+        err = launch_finalize(ws.partial, ws.perm, Bc, R, k, 1, idx_out + static_cast<int64_t>(b0) * k,
+                              score_out + static_cast<int64_t>(b0) * k, st);
+        if (err != hipSuccess) return err;
+      }
+      continue;
+    }
     int TQ = 1;
     while (16 * TQ < Bc && TQ < tq_max) TQ *= 2;
     // smaller query groups when the staged planes of one would not fit the ring
@@ -1036,7 +1090,6 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
     const int QG = 16 * TQ;
     const int n_qg = (Bc + QG - 1) / QG;
     const int b_pad = n_qg * QG;
-    const int nlg = (max_depth + geo.lpg - 1) / geo.lpg;
 
     PrepArgs pa{};
     pa.q = static_cast<const char*>(q) + static_cast<int64_t>(b0) * s.L * s.E * esz;

@@ -1,0 +1,490 @@
+// Trajectory-based expert map search (Section 4.2.2, Eq. 5), top-1 form for
+// bfloat16 stores and batches of more than 128 queries.
+//
+// The batch is the contraction of the depth-sorted query prefixes with the
+// stored maps' prefixes, layer group by layer group, on
+// v_mfma_f32_16x16x32_bf16, followed by the division by the query's and the
+// stored map's prefix norms (the latter precomputed at insert) and the best
+// stored index per query.  k_traj_prep (fm_traj.hip) sorts and stages the
+// queries before it runs; k_finalize merges its partial lists after.
+//
+// Query groups.  The sorted queries form tiles of 16 (deepest first); tile T
+// belongs to group T % n_qg as its local tile T / n_qg, so every group holds
+// the same mix of depths and needs the same work per map.  The workgroups of
+// one map range (one per group) are consecutive in the XCD-aware numbering,
+// run on one XCD at about the same pace, and read the same plane bytes: the
+// store streams from HBM about once, the other groups' reads hit that XCD's
+// L2.  Within a group a query tile takes part in the layer groups its
+// deepest query reaches; shallower queries of the tile contribute their
+// staged zeros.
+//
+// Workgroup: 8 waves, two per SIMD, arranged 2 x 4 over (queries, maps).
+// Wave (wq, wm) holds 128 x 64 float32 accumulators: local query tiles
+// wq, wq + 2, ..., wq + 14 (so the two query rows of waves stay equally
+// deep) against the map blocks wm, wm + 4, wm + 8, wm + 12 of a slice (16
+// blocks of 16 maps).
+//
+// Pipeline: a stage is one k-step of one layer group of one slice.  Its map
+// tiles (1 KB of a plane tile: 8 expert quads of 16 maps) and the group's
+// query tiles (1 KB MFMA operand tiles staged by the prep) are copied
+// global -> LDS by buffer loads straight into ring slot j % 3; tiles of
+// queries that are all shallower than the layer group read as zeros without
+// memory traffic.  At the start of stage j, once its own copies of stage
+// j+1 have landed, each wave passes the one barrier of the stage; slot j % 3
+// then receives the copies of stage j + 3 and the fragments of stage j+1
+// are read while the MFMAs of stage j run.  The copies of a slice's last
+// stage also bring the slice's prefix inverse norms: one 1 KB row per depth
+// (rnorm[p-1] of the slice's 256 maps) into one of two tables.
+//
+// Epilogue of a slice: lane (g, c) holds, for block i and query tile t, the
+// dots of maps 4g .. 4g+3 of the block with query c of the tile; the cosine
+// is (dot * 1/|q[0:p]|) * 1/|x[y][0:p]| at the query's depth p, and the lane
+// keeps the best (score, index) per query tile (strictly better replaces,
+// maps in increasing order: equal scores keep the lower index; a NaN score
+// is taken as -2).  The lists are merged over lane groups and waves and
+// stored as the workgroup's partial list.
+#include "fm_device.h"
+#include "fm_internal.h"
+
+namespace fm {
+
+namespace {
+
+struct TrajMmArgs {
+  const char* planes;     // [L] tiled bf16 planes
+  uint32_t plane_bytes;   // bytes per plane
+  uint32_t tile_bytes;    // bytes of one 16-map tile of a plane (32 * row)
+  const float* rnorm;     // [L][rn_stride] prefix inverse norms
+  int32_t rn_stride;
+  const char* qst;        // staged queries: [lg][ks][group][local tile][1 KB]
+  uint32_t qst_bytes;
+  const float* rq;        // [b_pad] 1/|q[0:p]| at each sorted position
+  const int32_t* sdep;    // [b_pad] depth at each sorted position (0: padding)
+  const int32_t* perm;    // [b_pad] query index at each sorted position
+  uint64_t* partial;      // [b_pad][R] one packed key per (position, workgroup of its group)
+  float* dbg;             // optional dense scores [B][n]
+  int32_t n, L, row, spl, lpg, ksg, nlg, dmax;
+  int32_t n_qg;           // query groups (256 queries each)
+  int32_t R;              // workgroups per query group
+  int32_t n_blocks;       // 16-map blocks of the store
+  int32_t grid;
+};
+
+constexpr int kW = 8;          // waves per workgroup (two per SIMD)
+constexpr int kGM = 4;         // wave columns over the maps
+constexpr int kNT = 8;         // query tiles per wave
+constexpr int kNB = 4;         // map blocks per wave and slice
+constexpr int kQG = 256;       // queries per group
+constexpr int kSB = 16;        // map blocks per slice
+constexpr int kNS = 3;         // ring slots
+constexpr int kMPW = 2;        // map tile copies per wave and stage
+constexpr int kQPW = 2;        // query tile copies per wave and stage
+constexpr int kNI = kMPW + kQPW;
+constexpr int kNTAB = 4;       // inverse-norm rows per wave (slice-last stages only)
+constexpr int kRows = kW * kNTAB;   // table rows: depths 1 .. 32
+constexpr int kSlot = (kSB + kQG / 16) * 1024;
+constexpr int kTab = kRows * 1024;
+constexpr int kLds = kNS * kSlot + 2 * kTab;
+static_assert(kSB == kW * kMPW && kQG / 16 == kW * kQPW, "copies per stage");
+static_assert(kLds <= 160 * 1024, "LDS");
+
+// Position of stage j: slice si, layer group lg, k-step ks and ring slot.
+struct TmPos {
+  int j, si, lg, ks, slot;
+};
+
+__device__ __forceinline__ TmPos tm_next(const TmPos& p, int ksg, int nlg) {
+  TmPos q;
+  q.j = p.j + 1;
+  const bool kwrap = p.ks + 1 == ksg;
+  const bool lwrap = kwrap && p.lg + 1 == nlg;
+  q.ks = kwrap ? 0 : p.ks + 1;
+  q.lg = lwrap ? 0 : (kwrap ? p.lg + 1 : p.lg);
+  q.si = lwrap ? p.si + 1 : p.si;
+  q.slot = p.slot + 1 == kNS ? 0 : p.slot + 1;
+  return q;
+}
+
+}  // namespace
+
+template <bool DBG>
+__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) k_traj_mm(TrajMmArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  unsigned char* ring = smem;                    // [kNS][kSlot]
+  unsigned char* tab = smem + kNS * kSlot;       // [2][kRows][256] float
+  uint64_t* mbuf = reinterpret_cast<uint64_t*>(smem);   // after the loop: [kGM][kQG]
+
+  const int tid = threadIdx.x;
+  const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int wq = w / kGM;
+  const int wm = w - wq * kGM;
+  const int lane = tid % kWave;
+  const int g = lane / 16;
+  const int c = lane % 16;
+
+  const int bid = blockIdx.x;
+  const int u = (bid % 8) * (a.grid / 8) + bid / 8;
+  const bool active = u < a.n_qg * a.R;
+  const int grp = active ? u % a.n_qg : 0;
+  const int rr = active ? u / a.n_qg : 0;
+  const int b_begin = active ? static_cast<int>((static_cast<int64_t>(rr) * a.n_blocks) / a.R) : 0;
+  const int b_end = active ? static_cast<int>((static_cast<int64_t>(rr + 1) * a.n_blocks) / a.R) : 0;
+  const int n_slices = (b_end - b_begin + kSB - 1) / kSB;
+  const int ksg = a.ksg;
+  const int nlg = a.nlg;
+  const int nst = nlg * ksg;   // stages per slice (at least 2)
+  const int nstages = n_slices * nst;
+
+  // sorted position of query c of this wave's tile t
+  auto pos_of = [&](int t) __attribute__((always_inline)) { return ((wq + 2 * t) * a.n_qg + grp) * 16 + c; };
+  float rqv[kNT];
+  uint32_t rows4[kNT / 4];   // the query's inverse-norm table row (depth - 1), a byte per tile
+  int tmd[kNT];              // depth of the tile's deepest query (wave-uniform)
+#pragma unroll
+  for (int t = 0; t < kNT / 4; ++t) rows4[t] = 0;
+#pragma unroll
+  for (int t = 0; t < kNT; ++t) {
+    const int p = pos_of(t);
+    rqv[t] = a.rq[p];
+    const int d = a.sdep[p];
+    rows4[t / 4] |= static_cast<uint32_t>(d > 0 ? d - 1 : 0) << (8 * (t % 4));
+    tmd[t] = __builtin_amdgcn_readfirstlane(d);   // lane 0 holds row 0 of the tile, its deepest query
+  }
+  float best_s[kNT];
+  int best_i[kNT];
+#pragma unroll
+  for (int t = 0; t < kNT; ++t) {
+    best_s[t] = kEmptyScore;
+    best_i[t] = -1;
+  }
+
+  if (nstages > 0) {
+    // Lane L of a map tile copy takes 16 bytes of quad L / 8 (maps 2m, 2m+1,
+    // m = L % 8) of k-step ks: slots 32 ks + 4 (L / 8) .. +3 lie in layer li
+    // of the layer group at expert e0; quads past the row read as zeros.
+    uint32_t loff[2];
+    bool qv[2];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const int s0 = 32 * ks + 4 * (lane / 8);
+      const int li = s0 / a.spl;
+      const int e0 = s0 - li * a.spl;
+      qv[ks] = ks < ksg && e0 < a.row;
+      loff[ks] = static_cast<uint32_t>(li) * a.plane_bytes + static_cast<uint32_t>((e0 / 4) * 128 + (lane % 8) * 16);
+    }
+    // depths of the two local tiles this wave copies
+    int qdep[kQPW];
+#pragma unroll
+    for (int i = 0; i < kQPW; ++i) qdep[i] = a.sdep[((w * kQPW + i) * a.n_qg + grp) * 16];
+#pragma unroll
+    for (int i = 0; i < kQPW; ++i) qdep[i] = __builtin_amdgcn_readfirstlane(qdep[i]);
+
+    const __amdgpu_buffer_rsrc_t rs_q = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<char*>(a.qst), static_cast<short>(0), static_cast<int>(a.qst_bytes), kBufWord3);
+    const __amdgpu_buffer_rsrc_t rs_rn = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(a.rnorm), static_cast<short>(0),
+        static_cast<int>(static_cast<uint32_t>(a.L) * static_cast<uint32_t>(a.rn_stride) * 4u), kBufWord3);
+
+    // Copy `part` of the stage at position p into its ring slot: parts 0 and
+    // 1 a map tile each, 2 and 3 a query tile each, and part 4, at a slice's
+    // last k-step only, kNTAB table rows (whether or not p is past the last
+    // stage, so that the counts depend on the position only).  Positions past
+    // the last stage use offsets past every descriptor.
+    auto load_part = [&](const TmPos& p, int part) __attribute__((always_inline)) {
+      const bool real = p.j < nstages;
+      const int lg = real ? p.lg : 0;
+      const int ks = real ? p.ks : 0;
+      const int l0 = lg * a.lpg;
+      unsigned char* slot = ring + p.slot * kSlot;
+      const int blk0 = b_begin + p.si * kSB;
+      if (part < kMPW) {
+        const int nl = a.L - l0 < a.lpg ? a.L - l0 : a.lpg;
+        const __amdgpu_buffer_rsrc_t rs_map = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<char*>(a.planes + static_cast<uint64_t>(l0) * a.plane_bytes), static_cast<short>(0),
+            static_cast<int>(static_cast<uint32_t>(nl) * a.plane_bytes), kBufWord3);
+        const uint32_t lo = ks ? loff[1] : loff[0];
+        const bool lv = ks ? qv[1] : qv[0];
+        const int tile = w * kMPW + part;
+        const int blk = blk0 + tile;
+        uint32_t off = lv ? lo + static_cast<uint32_t>(blk) * a.tile_bytes : kOutside;
+        off = (real && blk < b_end) ? off : kOutside;
+        // (opaque, so that the copy stays unconditional rather than becoming
+        // a branch on the lanes' quad validity)
+        asm volatile("" : "+v"(off));
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_map, (lds_vp)(slot + tile * 1024), 16, static_cast<int>(off), 0, 0,
+                                                 0);
+      } else if (part < kNI) {
+        const int i = part - kMPW;
+        const uint32_t qbase = static_cast<uint32_t>(((lg * ksg + ks) * a.n_qg + grp) * 16) * 1024u;
+        const int tl = w * kQPW + i;
+        const uint32_t off = (real && qdep[i] > l0) ? qbase + static_cast<uint32_t>(tl * 1024 + lane * 16) : kOutside;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_q, (lds_vp)(slot + (kSB + tl) * 1024), 16, static_cast<int>(off),
+                                                 0, 0, 0);
+      } else if (p.lg == nlg - 1 && p.ks == ksg - 1) {
+        const uint32_t ys = static_cast<uint32_t>(16 * blk0);
+        unsigned char* tb = tab + (p.si & 1) * kTab;
+#pragma unroll
+        for (int i = 0; i < kNTAB; ++i) {
+          const int r = w * kNTAB + i;
+          const uint32_t off =
+              (real && r < a.dmax) ? (static_cast<uint32_t>(r) * static_cast<uint32_t>(a.rn_stride) + ys) * 4u +
+                                         static_cast<uint32_t>(lane * 16)
+                                   : kOutside;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_rn, (lds_vp)(tb + r * 1024), 16, static_cast<int>(off), 0, 0, 0);
+        }
+      }
+    };
+    auto load_stage = [&](const TmPos& p) __attribute__((always_inline)) {
+#pragma unroll
+      for (int part = 0; part <= kNI; ++part) load_part(p, part);
+    };
+    auto has_tab = [&](const TmPos& p) __attribute__((always_inline)) {
+      return p.lg == nlg - 1 && p.ks == ksg - 1;
+    };
+
+    floatx4 acc[kNB][kNT];
+#pragma unroll
+    for (int i = 0; i < kNB; ++i)
+#pragma unroll
+      for (int t = 0; t < kNT; ++t) acc[i][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    // map fragment of block i: quads g and 4 + g of map c (two 8-byte reads
+    // 512 bytes apart); query fragment of local tile wq + 2t
+    auto read_mfrag = [&](int slot, int i) __attribute__((always_inline)) {
+      const unsigned char* p = ring + slot * kSlot + (wm + kGM * i) * 1024 + g * 128 + c * 8;
+      const uint32x2 lo = *reinterpret_cast<const uint32x2*>(p);
+      const uint32x2 hi = *reinterpret_cast<const uint32x2*>(p + 512);
+      return __builtin_bit_cast(u16x8, uint32x4{lo[0], lo[1], hi[0], hi[1]});
+    };
+    auto read_qfrag = [&](int slot, int t) __attribute__((always_inline)) {
+      return *reinterpret_cast<const u16x8*>(ring + slot * kSlot + (kSB + wq + 2 * t) * 1024 + lane * 16);
+    };
+
+    // Slice epilogue: scores of this wave's blocks of slice si, best per query.
+    auto epilogue = [&](int si) __attribute__((always_inline)) {
+      const int blk_s = b_begin + si * kSB;
+      const unsigned char* tb = tab + (si & 1) * kTab;
+#pragma unroll
+      for (int i = 0; i < kNB; ++i) {
+        const int blk = blk_s + wm + kGM * i;
+        if (blk >= b_end) break;
+        // The table was copied with the slice's last stage and the stage
+        // waits have covered it; the reads are written out (with one wait the
+        // values depend on) so that the compiler does not wait for every copy
+        // still in flight.
+        const int y0 = 16 * blk + 4 * g;
+        const bool full = 16 * blk + 16 <= a.n;
+        floatx4 xr[4];   // the rows of four tiles at a time
+#pragma unroll
+        for (int t = 0; t < kNT; ++t) {
+          if (t % 4 == 0) {
+#pragma unroll
+            for (int h = 0; h < 4; ++h) {
+              const int row = (rows4[t / 4] >> (8 * h)) & 0xFF;
+              const uint32_t addr =
+                  static_cast<uint32_t>(reinterpret_cast<uintptr_t>(tb + row * 1024 + (wm + kGM * i) * 64 + 16 * g));
+              asm volatile("ds_read_b128 %0, %1" : "=v"(xr[h]) : "v"(addr));
+            }
+            asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(xr[0]), "+v"(xr[1]), "+v"(xr[2]), "+v"(xr[3]));
+          }
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int y = y0 + r;
+            const float s = acc[i][t][r] * rqv[t] * xr[t % 4][r];
+            if constexpr (DBG) {
+              const int p = pos_of(t);
+              const int b = a.perm[p];
+              if (b >= 0 && y < a.n) a.dbg[static_cast<int64_t>(b) * a.n + y] = s;
+            }
+            const float sv = __builtin_fmaxf(s, kNanScore);
+            if ((full || y < a.n) && sv > best_s[t]) {
+              best_s[t] = sv;
+              best_i[t] = y;
+            }
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      // (the zeros are hidden from the compiler: known-zero accumulators
+      // would otherwise be folded into the next MFMAs and no longer share
+      // registers with the other paths)
+#pragma unroll
+      for (int i = 0; i < kNB; ++i)
+#pragma unroll
+        for (int t = 0; t < kNT; ++t) {
+          acc[i][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+          asm volatile("" : "+v"(acc[i][t]));
+        }
+    };
+
+    // prologue: the copies of stages 0 .. 2, then stage 0's fragments
+    TmPos pl{0, 0, 0, 0, 0};
+    bool tab_last = false;   // the latest copies issued include a table
+#pragma unroll
+    for (int s = 0; s < kNS; ++s) {
+      tab_last = has_tab(pl);
+      load_stage(pl);
+      pl = tm_next(pl, ksg, nlg);
+    }
+    u16x8 fa0[kNB], fa1[kNB], fb[kNT];
+    wait_vmcnt<0>();
+    raw_barrier();
+#pragma unroll
+    for (int i = 0; i < kNB; ++i) fa0[i] = read_mfrag(0, i);
+#pragma unroll
+    for (int t = 0; t < kNT; ++t) fb[t] = read_qfrag(0, t);
+    wait_lgkm0();
+
+    TmPos cur{0, 0, 0, 0, 0};
+    auto stage = [&](u16x8 (&fa)[kNB], u16x8 (&na)[kNB]) __attribute__((always_inline)) {
+      // stage j+1's copies have landed once only the latest ones (those of
+      // stage j+2) are outstanding
+      if (tab_last) wait_vmcnt<kNI + kNTAB>();
+      else wait_vmcnt<kNI>();
+      raw_barrier();
+      const TmPos pc = pl;   // the stage whose copies this one issues
+      tab_last = has_tab(pc);
+      pl = tm_next(pl, ksg, nlg);
+      const TmPos nxt = tm_next(cur, ksg, nlg);
+      const int sn = nxt.slot;
+#pragma unroll
+      for (int i = 0; i < kNB; ++i) na[i] = read_mfrag(sn, i);
+      // active tiles: those whose deepest query reaches the layer group
+      const int l_first = cur.lg * a.lpg;
+      int nact = 0;   // (the depths fall with t)
+#pragma unroll
+      for (int t = 0; t < kNT; ++t) nact = tmd[t] > l_first ? t + 1 : nact;
+      __builtin_amdgcn_s_setprio(1);
+      // per tile a uniform branch: its MFMAs, then its fragment of the next
+      // stage into the register they have just read; copy part t of stage
+      // j+3 after tile t (a copy can hold up this wave's issue while the
+      // vector memory unit is busy; the MFMAs already issued keep running)
+#pragma unroll
+      for (int t = 0; t < kNT; ++t) {
+        if (t < nact) {
+#pragma unroll
+          for (int i = 0; i < kNB; ++i) acc[i][t] = mfma_bf16(fa[i], fb[t], acc[i][t]);
+          fb[t] = read_qfrag(sn, t);
+        }
+        if (t <= kNI) load_part(pc, t);
+      }
+      __builtin_amdgcn_s_setprio(0);
+      // the next stage starts a slice: every tile's fragment
+      if (nxt.lg == 0 && nxt.ks == 0) {
+#pragma unroll
+        for (int t = 0; t < kNT; ++t) fb[t] = read_qfrag(sn, t);
+      }
+      wait_lgkm0();
+      cur = nxt;
+    };
+    // per slice: its stages (pairs, then one more when nst is odd, after
+    // which the next slice's map fragments sit in fa1 and are moved to fa0),
+    // then the epilogue
+    for (int si = 0; si < n_slices; ++si) {
+      for (int s2 = 0; s2 + 1 < nst; s2 += 2) {
+        stage(fa0, fa1);
+        stage(fa1, fa0);
+      }
+      if (nst & 1) {
+        stage(fa0, fa1);
+#pragma unroll
+        for (int i = 0; i < kNB; ++i) fa0[i] = fa1[i];
+      }
+      epilogue(si);
+    }
+    wait_vmcnt<0>();   // the trailing copies
+  }
+  __syncthreads();
+
+  // merge: the four lane groups of a query, then the kGM waves of its tile row
+  uint64_t key[kNT];
+#pragma unroll
+  for (int t = 0; t < kNT; ++t) {
+    key[t] = best_i[t] < 0 ? 0ull : make_key(best_s[t], best_i[t]);
+#pragma unroll
+    for (int m = 16; m <= 32; m <<= 1) {
+      const uint64_t o = shfl_xor_u64(key[t], m);
+      key[t] = o > key[t] ? o : key[t];
+    }
+  }
+  if (g == 0) {
+#pragma unroll
+    for (int t = 0; t < kNT; ++t) mbuf[wm * kQG + (wq + 2 * t) * 16 + c] = key[t];
+  }
+  __syncthreads();
+  if (active) {
+    for (int r = tid; r < kQG; r += kW * kWave) {
+      uint64_t m = 0;
+#pragma unroll
+      for (int ww = 0; ww < kGM; ++ww) m = mbuf[ww * kQG + r] > m ? mbuf[ww * kQG + r] : m;
+      const int p = ((r / 16) * a.n_qg + grp) * 16 + r % 16;
+      a.partial[static_cast<int64_t>(p) * a.R + rr] = m;
+    }
+  }
+}
+
+namespace {
+
+template <bool DBG>
+hipError_t traj_mm_launch(const TrajMmArgs& a, hipStream_t st) {
+  auto kern = k_traj_mm<DBG>;
+  hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       kLds);
+  if (err != hipSuccess) return err;
+  const ScanEvents& ev = scan_events();
+  if (ev.start != nullptr) {
+    err = hipEventRecord(ev.start, st);
+    if (err != hipSuccess) return err;
+  }
+  hipLaunchKernelGGL(kern, dim3(a.grid), dim3(kW * kWave), kLds, st, a);
+  err = hipGetLastError();
+  if (err != hipSuccess || ev.stop == nullptr) return err;
+  return hipEventRecord(ev.stop, st);
+}
+
+}  // namespace
+
+bool traj_mm_fits(bool bf, int KTOP, int32_t Bc, int32_t max_depth, int nlg, int ksg) {
+  return bf && KTOP == 1 && Bc > 128 && max_depth <= kRows && nlg * ksg >= 2;
+}
+
+int traj_mm_group() { return kQG; }
+
+hipError_t launch_traj_mm(const StoreView& s, int spl, int lpg, int ksg, int nlg, int32_t max_depth, int32_t b_pad,
+                          const Workspace& ws, float* dbg, int32_t* R_out, hipStream_t st) {
+  const int n_qg = b_pad / kQG;
+  const int n_blocks = (s.n + 15) / 16;
+  int R = 256 / n_qg;
+  if (R < 1) R = 1;
+  if (R > n_blocks) R = n_blocks > 0 ? n_blocks : 1;
+  if (R > kMaxPartials) R = kMaxPartials;
+  TrajMmArgs a;
+  a.planes = static_cast<const char*>(s.planes);
+  a.plane_bytes = static_cast<uint32_t>(s.plane_elems * 2);
+  a.tile_bytes = static_cast<uint32_t>(16 * s.row * 2);
+  a.rnorm = s.rnorm;
+  a.rn_stride = static_cast<int32_t>(s.rn_stride);
+  a.qst = static_cast<const char*>(ws.qrows);
+  a.qst_bytes = static_cast<uint32_t>(static_cast<int64_t>(nlg) * ksg * b_pad * 64);
+  a.rq = ws.rq;
+  a.sdep = ws.sdep;
+  a.perm = ws.perm;
+  a.partial = ws.partial;
+  a.dbg = dbg;
+  a.n = s.n;
+  a.L = s.L;
+  a.row = s.row;
+  a.spl = spl;
+  a.lpg = lpg;
+  a.ksg = ksg;
+  a.nlg = nlg;
+  a.dmax = max_depth;
+  a.n_qg = n_qg;
+  a.R = R;
+  a.n_blocks = n_blocks;
+  a.grid = (n_qg * R + 7) / 8 * 8;
+  *R_out = R;
+  return dbg != nullptr ? traj_mm_launch<true>(a, st) : traj_mm_launch<false>(a, st);
+}
+
+}  // namespace fm
