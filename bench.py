@@ -61,22 +61,35 @@ FP32_MFMA_PEAK_TFS = 157.3     # dense fp32 MFMA
 COPY_BYTES_KIB = 262144.0
 COPY_COUNTERS_KIB = {"FETCH_SIZE": 131083.5, "WRITE_SIZE": 262144.0}
 COUNTERS_KIB = {
-    # workload: (kernel, FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch
-    "mixtral_traj_n1k": ("k_traj_scan", 610.1, 10.9),
-    "qwen_traj_n50k_b64": ("k_traj_scan", 138797.4, 128.0),
-    "semantic_d4096_n100k_b256": ("k_sem_scan", 433244.2, 431.9),
-    "phi_traj_top4_n200k_b512": ("k_traj_scan", 333131.3, 1012.0),
-    "qwen_mixed_bf16_n1m_b1024": ("k_sem_scan", 2508540.4, 390.8),
+    # workload: {kernel: (FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch}
+    "mixtral_traj_n1k": {"k_traj_scan": (610.1, 10.9)},
+    "qwen_traj_n50k_b64": {"k_traj_scan": (138797.4, 128.0)},
+    "phi_traj_top4_n200k_b512": {"k_traj_scan": (333131.3, 1012.0)},
+    "qwen_mixed_bf16_n1m_b1024": {"k_sem_mm": (2265213.7, 512.0), "k_traj_mm": (1828695.5, 512.0)},
 }
 
 
-def counter_traffic(workload):
-    if workload not in COUNTERS_KIB:
+def counter_traffic(workload, kernel):
+    fw = COUNTERS_KIB.get(workload, {}).get(kernel)
+    if fw is None:
         return None
-    _, fetch, write = COUNTERS_KIB[workload]
+    fetch, write = fw
     kib = (fetch * COPY_BYTES_KIB / COPY_COUNTERS_KIB["FETCH_SIZE"]
            + write * COPY_BYTES_KIB / COPY_COUNTERS_KIB["WRITE_SIZE"])
     return kib * 1024.0
+
+
+def scan_kernels(s):
+    """The scan kernel the library launches for each half of workload s's
+    batch (the same rules as the library's dispatch): the semantic top-1
+    scan k_sem_mm for k = 1, else k_sem_scan; the bf16 top-1 trajectory scan
+    k_traj_mm for bf16 stores, k = 1 and more than 128 queries per launch,
+    else k_traj_scan."""
+    sem = ("k_sem_mm" if s.k == 1 else "k_sem_scan") if s.B_sem else None
+    traj = None
+    if s.B_traj:
+        traj = "k_traj_mm" if (s.map_dtype == "bf16" and s.k == 1 and min(s.B_traj, 1024) > 128) else "k_traj_scan"
+    return sem, traj
 
 
 def hip_runtime():
@@ -654,7 +667,7 @@ def bench_capacity(args):
         achieved = sem_bytes / dur_s / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": achieved / HBM_PEAK_GBS}
-    roof.update({"traffic": None, "kernel": "k_sem_scan", "mfma_dtype": "bf16", "duration_us": last["sem_scan_us"],
+    roof.update({"traffic": None, "kernel": "k_sem_mm", "mfma_dtype": "bf16", "duration_us": last["sem_scan_us"],
                  "algorithmic_bytes": sem_bytes, "algorithmic_flops": sem_flops})
     cpu = None
     if not args.no_cpu_baseline:
@@ -748,18 +761,22 @@ def main():
 
     hip = hip_runtime()
     lib = fm._lib.load()
-    timers = {"k_sem_scan": ScanTimer(hip, lib, args.steps) if s.B_sem else None,
-              "k_traj_scan": ScanTimer(hip, lib, args.steps) if s.B_traj else None}
+    sem_k, traj_k = scan_kernels(s)
+    timers = {}
+    if sem_k:
+        timers[sem_k] = ScanTimer(hip, lib, args.steps)
+    if traj_k:
+        timers[traj_k] = ScanTimer(hip, lib, args.steps)
 
     def match(i=None, tm=timers):
         if s.B_sem:
             if i is not None:
-                tm["k_sem_scan"].arm(i)
+                tm[sem_k].arm(i)
             fm.match_semantic(store, q_sem, s.k, out=(idx[:s.B_sem], score[:s.B_sem]), workspace=ws_sem,
                               stream=stream)
         if s.B_traj:
             if i is not None:
-                tm["k_traj_scan"].arm(i)
+                tm[traj_k].arm(i)
             fm.match_trajectory(store, q_traj, depth, s.k, max_depth=max_depth,
                                 out=(idx[s.B_sem:], score[s.B_sem:]), workspace=ws_traj, stream=stream)
         if i is not None:
@@ -815,7 +832,7 @@ def main():
     # otherwise).
     cost = algorithmic_cost(s, a)
     kernel = max(scan_ms, key=scan_ms.get)
-    if kernel == "k_traj_scan":
+    if kernel == traj_k:
         byts, flops = cost["traj_bytes"], cost["traj_flops"]
         fpeak, fdt = (FP32_MFMA_PEAK_TFS, "f32") if s.map_dtype == "f32" else (BF16_MFMA_PEAK_TFS, "bf16")
     else:
@@ -829,7 +846,7 @@ def main():
         achieved = byts / dur_s / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": achieved / HBM_PEAK_GBS}
-    roof["traffic"] = counter_traffic(s.name) if COUNTERS_KIB.get(s.name, ("",))[0] == kernel else None
+    roof["traffic"] = counter_traffic(s.name, kernel)
     roof["kernel"] = kernel
     roof["mfma_dtype"] = fdt
     roof["duration_us"] = scan_ms[kernel] * 1e3
@@ -841,7 +858,7 @@ def main():
         if other == kernel:
             continue
         # the other scan of a mixed batch against its own binding roofline
-        if other == "k_traj_scan":
+        if other == traj_k:
             ob, of = cost["traj_bytes"], cost["traj_flops"]
             op = FP32_MFMA_PEAK_TFS if s.map_dtype == "f32" else BF16_MFMA_PEAK_TFS
         else:
@@ -854,7 +871,7 @@ def main():
             roof["other"] = {"kernel": other, "bound": "hbm", "achieved": ob / od / 1e9, "peak": HBM_PEAK_GBS,
                              "unit": "GB/s", "frac": ob / od / 1e9 / HBM_PEAK_GBS}
         roof["other"].update({"duration_us": scan_ms[other] * 1e3, "algorithmic_bytes": ob,
-                              "algorithmic_flops": of})
+                              "algorithmic_flops": of, "traffic": counter_traffic(s.name, other)})
     if cold_ms:
         # the same kernel's cold average and the fraction it reaches
         cold_s = cold_ms[kernel] * 1e-3
