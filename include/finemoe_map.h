@@ -56,21 +56,25 @@ typedef enum {
     FM_ERR_DEVICE = 5        /* fm_store_check found a sticky device-side range error */
 } fm_status;
 
-typedef enum { FM_F32 = 0, FM_BF16 = 1 } fm_dtype;
+/* The argument enums below end in a 32-bit sentinel so that any int a caller
+ * passes is a value of the type, which the library then checks and rejects
+ * if it is not one of the listed ones (FM_ERR_INVALID); the sentinels are not
+ * valid arguments. */
+typedef enum { FM_F32 = 0, FM_BF16 = 1, FM_DTYPE_ENUM_INT32_ = 0x7fffffff } fm_dtype;
 
 /* Threshold of Section 4.3: FIXED uses params.tau for every layer; DYNAMIC
  * uses delta = Clip(1 - score, 0, 1) with the best match's score (a NaN score
  * gives delta = 1). */
-typedef enum { FM_TAU_FIXED = 0, FM_TAU_DYNAMIC = 1 } fm_tau_mode;
+typedef enum { FM_TAU_FIXED = 0, FM_TAU_DYNAMIC = 1, FM_TAU_ENUM_INT32_ = 0x7fffffff } fm_tau_mode;
 
 /* Which probabilities guide a layer: NONE = the layer's row of the best match
  * (Sections 4.2.1 and 4.2.2 use the single highest-scoring map); SCORE = the
  * similarity-weighted mean of that row over the k kept matches, with weights
  * max(score, 0) (plain mean if every weight is 0). */
-typedef enum { FM_BLEND_NONE = 0, FM_BLEND_SCORE = 1 } fm_blend;
+typedef enum { FM_BLEND_NONE = 0, FM_BLEND_SCORE = 1, FM_BLEND_ENUM_INT32_ = 0x7fffffff } fm_blend;
 
 /* Which Section 4.5 priority fm_priority_order ranks by. */
-typedef enum { FM_PRI_PREFETCH = 0, FM_PRI_EVICT = 1 } fm_pri_kind;
+typedef enum { FM_PRI_PREFETCH = 0, FM_PRI_EVICT = 1, FM_PRI_ENUM_INT32_ = 0x7fffffff } fm_pri_kind;
 
 /* Sticky device-side flags reported by fm_store_check. */
 #define FM_FLAG_DEPTH_CLAMPED 0x1u   /* a trajectory depth was outside [1, max_depth] and was clamped */

@@ -1,8 +1,9 @@
 """ctypes declarations of the C ABI in include/finemoe_map.h.
 
-Loads ``libfinemoe_map.so`` from this package directory.  There is no
-fallback: if the library is missing the import fails with a message saying
-how to build it.
+Loads ``libfinemoe_map.so`` from this package directory (or, for the
+sanitizer tests, the library file FM_LIBRARY names).  There is no fallback:
+if the library is missing the import fails with a message saying how to
+build it.
 """
 from __future__ import annotations
 
@@ -10,7 +11,7 @@ import ctypes as C
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libfinemoe_map.so")
+LIB_PATH = os.environ.get("FM_LIBRARY") or os.path.join(HERE, "libfinemoe_map.so")
 
 FM_OK, FM_ERR_INVALID, FM_ERR_UNSUPPORTED, FM_ERR_FULL, FM_ERR_HIP, FM_ERR_DEVICE = range(6)
 FM_F32, FM_BF16 = 0, 1
