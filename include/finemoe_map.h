@@ -253,6 +253,28 @@ fm_status fm_select_prefetch(const fm_store* store, const int32_t* idx, const fl
                              const int32_t* layer_end, const fm_select_params* params,
                              uint64_t* mask_out, uint8_t* count_out, void* stream);
 
+/* A match call and the selection of its rows in one call: the semantic
+ * search of Section 4.2.1 (Eq. 4) or the trajectory search of Section 4.2.2
+ * (Eq. 5), then the prefetch sets of Section 4.3 (Eq. 6-8) of every row of
+ * the batch, with the merge of the search's per-workgroup lists and the
+ * selection in one launch.  Arguments, results and errors as for
+ * fm_match_semantic / fm_match_trajectory followed by fm_select_prefetch on
+ * the same B rows with the same k: idx_out/score_out receive the matches
+ * (device [B][k]), mask_out/count_out the sets (device [B][L]); layer_begin,
+ * layer_end and params as for fm_select_prefetch.  The results are those of
+ * the two separate calls. */
+fm_status fm_match_semantic_select(const fm_store* store, const void* q, int32_t B, int32_t k,
+                                   const int32_t* layer_begin, const int32_t* layer_end,
+                                   const fm_select_params* params, int32_t* idx_out, float* score_out,
+                                   uint64_t* mask_out, uint8_t* count_out, void* workspace,
+                                   size_t workspace_bytes, void* stream);
+fm_status fm_match_trajectory_select(const fm_store* store, const void* q, const int32_t* depth,
+                                     int32_t max_depth, int32_t B, int32_t k, const int32_t* layer_begin,
+                                     const int32_t* layer_end, const fm_select_params* params,
+                                     int32_t* idx_out, float* score_out, uint64_t* mask_out,
+                                     uint8_t* count_out, void* workspace, size_t workspace_bytes,
+                                     void* stream);
+
 /* Misses of prefetch sets (Section 3: R_{l,j} = 1 iff expert j of layer l is
  * activated and not cached).  q: device [B][L][E] of map_dtype, each query's
  * own gate probabilities (the experts its layers actually route to); the

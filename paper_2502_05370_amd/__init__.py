@@ -336,6 +336,66 @@ def select_prefetch(store: Store, idx: torch.Tensor, score: torch.Tensor, layer_
     return mask, count
 
 
+def _fused_outputs(store: Store, B: int, k: int, layer_begin, layer_end, out, dev):
+    _need(layer_begin, "layer_begin", torch.int32, (B,), dev)
+    _need(layer_end, "layer_end", torch.int32, (B,), dev)
+    if out is None:
+        out = (torch.empty((B, k), dtype=torch.int32, device=dev),
+               torch.empty((B, k), dtype=torch.float32, device=dev),
+               torch.empty((B, store.L), dtype=torch.int64, device=dev),
+               torch.empty((B, store.L), dtype=torch.uint8, device=dev))
+    idx, score, mask, count = out
+    _need(idx, "out[0] (idx)", torch.int32, (B, k), dev)
+    _need(score, "out[1] (score)", torch.float32, (B, k), dev)
+    _need(mask, "out[2] (mask)", torch.int64, (B, store.L), dev)
+    _need(count, "out[3] (count)", torch.uint8, (B, store.L), dev)
+    return out
+
+
+def match_trajectory_select(store: Store, q: torch.Tensor, depth: torch.Tensor, layer_begin: torch.Tensor,
+                            layer_end: torch.Tensor, k: int = 1, max_depth: Optional[int] = None, tau: float = 0.9,
+                            k_min: int = 1, k_max: Optional[int] = None, mode: int = FM_TAU_FIXED,
+                            blend: int = FM_BLEND_NONE, out=None, workspace: Optional[Workspace] = None,
+                            stream=None):
+    """match_trajectory, then select_prefetch of its rows, in one call -> (idx, score, mask, count)."""
+    dev = _dev(store)
+    _need(q, "q", _TORCH[store.dtype_code], (None, store.L, store.E), dev)
+    B = q.shape[0]
+    _need(depth, "depth", torch.int32, (B,), dev)
+    if max_depth is None:
+        max_depth = store.L
+    if k_max is None:
+        k_max = store.E
+    idx, score, mask, count = out = _fused_outputs(store, B, k, layer_begin, layer_end, out, dev)
+    ws = _ws(store, workspace)
+    p = SelectParams(mode, tau, k_min, k_max, blend)
+    _lib.check(_lib.load().fm_match_trajectory_select(store.handle, _ptr(q), _ptr(depth), max_depth, B, k,
+                                                      _ptr(layer_begin), _ptr(layer_end), C.byref(p), _ptr(idx),
+                                                      _ptr(score), _ptr(mask), _ptr(count), ws.ptr, ws.nbytes,
+                                                      _stream(stream)), "fm_match_trajectory_select")
+    return out
+
+
+def match_semantic_select(store: Store, q: torch.Tensor, layer_begin: torch.Tensor, layer_end: torch.Tensor,
+                          k: int = 1, tau: float = 0.9, k_min: int = 1, k_max: Optional[int] = None,
+                          mode: int = FM_TAU_FIXED, blend: int = FM_BLEND_NONE, out=None,
+                          workspace: Optional[Workspace] = None, stream=None):
+    """match_semantic, then select_prefetch of its rows, in one call -> (idx, score, mask, count)."""
+    dev = _dev(store)
+    _need(q, "q", torch.bfloat16, (None, store.d_emb), dev)
+    B = q.shape[0]
+    if k_max is None:
+        k_max = store.E
+    idx, score, mask, count = out = _fused_outputs(store, B, k, layer_begin, layer_end, out, dev)
+    ws = _ws(store, workspace)
+    p = SelectParams(mode, tau, k_min, k_max, blend)
+    _lib.check(_lib.load().fm_match_semantic_select(store.handle, _ptr(q), B, k, _ptr(layer_begin),
+                                                    _ptr(layer_end), C.byref(p), _ptr(idx), _ptr(score),
+                                                    _ptr(mask), _ptr(count), ws.ptr, ws.nbytes, _stream(stream)),
+               "fm_match_semantic_select")
+    return out
+
+
 def priority_order(store: Store, idx: torch.Tensor, score: torch.Tensor, masks: torch.Tensor,
                    l_now: Optional[torch.Tensor] = None, freq: Optional[torch.Tensor] = None,
                    kind: int = FM_PRI_PREFETCH, blend: int = FM_BLEND_NONE, cap: Optional[int] = None,

@@ -57,6 +57,10 @@ SIGNATURES = {
     "fm_match_trajectory": (C.c_int, [_vp, _vp, _vp, _i32, _i32, _i32, _vp, _vp, _vp, _sz, _vp]),
     "fm_match_trajectory_noalloc": (C.c_int, [_vp, _vp, _vp, _i32, _i32, _i32, _vp, _vp, _vp]),
     "fm_select_prefetch": (C.c_int, [_vp, _vp, _vp, _i32, _i32, _vp, _vp, C.POINTER(SelectParams), _vp, _vp, _vp]),
+    "fm_match_semantic_select": (C.c_int, [_vp, _vp, _i32, _i32, _vp, _vp, C.POINTER(SelectParams), _vp, _vp, _vp,
+                                           _vp, _vp, _sz, _vp]),
+    "fm_match_trajectory_select": (C.c_int, [_vp, _vp, _vp, _i32, _i32, _i32, _vp, _vp, C.POINTER(SelectParams),
+                                             _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "fm_miss_count": (C.c_int, [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
     "fm_priority_order": (C.c_int, [_vp, _vp, _vp, _i32, _i32, C.c_int, C.c_int, _vp, _vp, _vp, _i32, _vp, _vp, _vp,
                                     _vp]),

@@ -348,6 +348,19 @@ static fm_status check_match_common(const fm_store* s, int32_t B, int32_t k, con
   return check_workspace(s, ws, ws_bytes);
 }
 
+// The selection's own arguments (Section 4.3 parameters, layer ranges, outputs).
+static fm_status check_select(const fm_store* s, const int32_t* lb, const int32_t* le, const fm_select_params* p,
+                              const uint64_t* mask_out, const uint8_t* count_out) {
+  if (lb == nullptr || le == nullptr || p == nullptr || mask_out == nullptr || count_out == nullptr)
+    return fail(FM_ERR_INVALID, "layer_begin, layer_end, params, mask_out and count_out must be non-NULL");
+  if (p->mode != FM_TAU_FIXED && p->mode != FM_TAU_DYNAMIC) return fail(FM_ERR_INVALID, "tau mode %d", p->mode);
+  if (p->blend != FM_BLEND_NONE && p->blend != FM_BLEND_SCORE) return fail(FM_ERR_INVALID, "blend %d", p->blend);
+  if (p->k_min < 0 || p->k_min > p->k_max || p->k_max > s->v.E)
+    return fail(FM_ERR_INVALID, "need 0 <= k_min (%d) <= k_max (%d) <= E (%d)", p->k_min, p->k_max, s->v.E);
+  if (p->mode == FM_TAU_FIXED && p->tau != p->tau) return fail(FM_ERR_INVALID, "tau is NaN");
+  return FM_OK;
+}
+
 fm_status fm_match_semantic(const fm_store* s, const void* q, int32_t B, int32_t k, int32_t* idx_out,
                             float* score_out, void* ws, size_t ws_bytes, void* stream) {
   if (fm_status st = check_match_common(s, B, k, idx_out, score_out, ws, ws_bytes)) return st;
@@ -443,21 +456,52 @@ fm_status fm_select_prefetch(const fm_store* s, const int32_t* idx, const float*
                              const int32_t* lb, const int32_t* le, const fm_select_params* p,
                              uint64_t* mask_out, uint8_t* count_out, void* stream) {
   if (fm_status st = check_store(s)) return st;
-  if (idx == nullptr || score == nullptr || lb == nullptr || le == nullptr || p == nullptr || mask_out == nullptr ||
-      count_out == nullptr)
-    return fail(FM_ERR_INVALID, "idx, score, layer_begin, layer_end, params, mask_out and count_out must be non-NULL");
+  if (idx == nullptr || score == nullptr) return fail(FM_ERR_INVALID, "idx and score must be non-NULL");
   if (B < 1 || B > 65536) return fail(FM_ERR_INVALID, "B=%d outside [1, 65536]", B);
   if (k < 1 || k > fm::kMaxK) return fail(FM_ERR_INVALID, "k=%d outside [1, %d]", k, fm::kMaxK);
-  if (p->mode != FM_TAU_FIXED && p->mode != FM_TAU_DYNAMIC) return fail(FM_ERR_INVALID, "tau mode %d", p->mode);
-  if (p->blend != FM_BLEND_NONE && p->blend != FM_BLEND_SCORE) return fail(FM_ERR_INVALID, "blend %d", p->blend);
-  if (p->k_min < 0 || p->k_min > p->k_max || p->k_max > s->v.E)
-    return fail(FM_ERR_INVALID, "need 0 <= k_min (%d) <= k_max (%d) <= E (%d)", p->k_min, p->k_max, s->v.E);
-  if (p->mode == FM_TAU_FIXED && p->tau != p->tau) return fail(FM_ERR_INVALID, "tau is NaN");
+  if (fm_status st = check_select(s, lb, le, p, mask_out, count_out)) return st;
   DeviceGuard dg(s->device);
   if (!dg.ok) return fail(FM_ERR_HIP, "cannot select the store's device %d", s->device);
   hipError_t e = fm::launch_select(s->v, idx, score, B, k, lb, le, *p, mask_out, count_out,
                                    static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "select launch");
+  return ok();
+}
+
+fm_status fm_match_semantic_select(const fm_store* s, const void* q, int32_t B, int32_t k, const int32_t* lb,
+                                   const int32_t* le, const fm_select_params* p, int32_t* idx_out, float* score_out,
+                                   uint64_t* mask_out, uint8_t* count_out, void* ws, size_t ws_bytes,
+                                   void* stream) {
+  if (fm_status st = check_match_common(s, B, k, idx_out, score_out, ws, ws_bytes)) return st;
+  if (q == nullptr) return fail(FM_ERR_INVALID, "q is NULL");
+  if (reinterpret_cast<uintptr_t>(q) % 16 != 0) return fail(FM_ERR_INVALID, "q must be 16-byte aligned");
+  if (s->v.d_emb == 0) return fail(FM_ERR_INVALID, "store has no embeddings (d_emb = 0)");
+  if (fm_status st = check_select(s, lb, le, p, mask_out, count_out)) return st;
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(FM_ERR_HIP, "cannot select the store's device %d", s->device);
+  const fm::SelectFuse fuse{lb, le, *p, mask_out, count_out};
+  hipError_t e = fm::launch_match_semantic(s->v, q, B, k, idx_out, score_out, nullptr, carve(s, ws),
+                                           static_cast<hipStream_t>(stream), nullptr, 1.0, 0.0, &fuse);
+  if (e != hipSuccess) return hip_fail(e, "semantic match-and-select launch");
+  return ok();
+}
+
+fm_status fm_match_trajectory_select(const fm_store* s, const void* q, const int32_t* depth, int32_t max_depth,
+                                     int32_t B, int32_t k, const int32_t* lb, const int32_t* le,
+                                     const fm_select_params* p, int32_t* idx_out, float* score_out,
+                                     uint64_t* mask_out, uint8_t* count_out, void* ws, size_t ws_bytes,
+                                     void* stream) {
+  if (fm_status st = check_match_common(s, B, k, idx_out, score_out, ws, ws_bytes)) return st;
+  if (q == nullptr || depth == nullptr) return fail(FM_ERR_INVALID, "q and depth must be non-NULL");
+  if (max_depth < 1 || max_depth > s->v.L)
+    return fail(FM_ERR_INVALID, "max_depth=%d outside [1, L=%d]", max_depth, s->v.L);
+  if (fm_status st = check_select(s, lb, le, p, mask_out, count_out)) return st;
+  DeviceGuard dg(s->device);
+  if (!dg.ok) return fail(FM_ERR_HIP, "cannot select the store's device %d", s->device);
+  const fm::SelectFuse fuse{lb, le, *p, mask_out, count_out};
+  hipError_t e = fm::launch_match_trajectory(s->v, q, depth, max_depth, B, k, idx_out, score_out, nullptr,
+                                             carve(s, ws), static_cast<hipStream_t>(stream), &fuse);
+  if (e != hipSuccess) return hip_fail(e, "trajectory match-and-select launch");
   return ok();
 }
 

@@ -102,16 +102,41 @@ hipError_t launch_insert(const StoreView& s, const void* maps, const void* embs,
                          const int32_t* slot_of, int32_t* slots_out, hipStream_t st);
 hipError_t launch_insert_dedup(const StoreView& s, const void* maps, const void* embs, int32_t n, int32_t d,
                                int32_t* slots_out, const Workspace& ws, const DedupScratch& sc, hipStream_t st);
+// The selection a fused match-and-select call runs after the merge: the
+// rows' layer ranges, the parameters and the outputs, in the match call's
+// batch order (pointers to its first query).
+struct SelectFuse {
+  const int32_t* lb;
+  const int32_t* le;
+  fm_select_params p;
+  uint64_t* mask_out;   // [B][L]
+  uint8_t* count_out;   // [B][L]
+  SelectFuse at(int32_t b0, int32_t L) const {
+    SelectFuse f = *this;
+    f.lb = lb + b0;
+    f.le = le + b0;
+    f.mask_out = mask_out + static_cast<int64_t>(b0) * L;
+    f.count_out = count_out + static_cast<int64_t>(b0) * L;
+    return f;
+  }
+};
+// k_finalize and k_select in one launch (fm_select.hip): the merge of the
+// partial lists of positions 0 .. B-1 (query perm[pos], or pos), the
+// matches written to idx_out / score_out, then each row's selection.
+hipError_t launch_merge_select(const StoreView& s, const uint64_t* partial, const int32_t* perm, int32_t B, int32_t R,
+                               int32_t k, int KTOP, const int32_t* rgrp, int32_t qg, int32_t* idx_out,
+                               float* score_out, const SelectFuse& f, hipStream_t st);
+// With fuse set, the merge of each launch is the merge-and-select above.
 hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int32_t* depth,
                                    int32_t max_depth, int32_t B, int32_t k, int32_t* idx_out,
                                    float* score_out, float* dbg_scores, const Workspace& ws,
-                                   hipStream_t st);
+                                   hipStream_t st, const SelectFuse* fuse = nullptr);
 // With dbg_scores set, the dense scores are written there; with mix also set
 // (a dense [B][n] matrix), the dense output is w_self * score + w_mix * mix.
 hipError_t launch_match_semantic(const StoreView& s, const void* q, int32_t B, int32_t k,
                                  int32_t* idx_out, float* score_out, float* dbg_scores,
                                  const Workspace& ws, hipStream_t st, const float* mix = nullptr,
-                                 double w_self = 1.0, double w_mix = 0.0);
+                                 double w_self = 1.0, double w_mix = 0.0, const SelectFuse* fuse = nullptr);
 // Top-1 semantic scan (fm_sem_mm.hip): queries per group for a chunk of Bc
 // queries, and the scan itself on queries already staged by k_sem_prep
 // (b_pad = groups * queries per group); *R_out receives the partial lists per

@@ -55,20 +55,16 @@ __device__ __forceinline__ uint64_t ord_f64(double p) {
   return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
 }
 
-__global__ void __launch_bounds__(256) k_select(SelArgs a) {
-  __shared__ double sorted[4][kMaxE];
-  __shared__ uint64_t keys[4][kMaxE];
+// The selection of row (b, l) of the batch from the query's matches idx_b /
+// score_b (k of them, best first); one wavefront, lane j = expert j.
+__device__ __forceinline__ void select_row(const SelArgs& a, int b, int l, const int32_t* idx_b, const float* score_b,
+                                           double* sorted, uint64_t* keys) {
   const int lane = threadIdx.x % kWave;
-  const int wv = threadIdx.x / kWave;
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + wv;
-  if (row >= static_cast<int64_t>(a.B) * a.L) return;
-  const int b = static_cast<int>(row / a.L);
-  const int l = static_cast<int>(row - static_cast<int64_t>(b) * a.L);
-
+  const int64_t row = static_cast<int64_t>(b) * a.L + l;
   int lo = a.lb[b], hi = a.le[b];
   lo = lo < 0 ? 0 : (lo > a.L ? a.L : lo);
   hi = hi < 0 ? 0 : (hi > a.L ? a.L : hi);
-  const int y0 = a.idx[static_cast<int64_t>(b) * a.k];
+  const int y0 = idx_b[0];
   bool live = l >= lo && l < hi && y0 >= 0;
   if (live && y0 >= a.n) {
     if (lane == 0) atomicOr(a.flags, static_cast<uint32_t>(FM_FLAG_INDEX_RANGE));
@@ -85,14 +81,12 @@ __global__ void __launch_bounds__(256) k_select(SelArgs a) {
   // 1. guiding probability of expert `lane`
   const GuideView gv{a.planes, a.plane_elems, a.n, a.row, a.dtype};
   double p = 0.0;
-  if (lane < a.E)
-    p = guide_prob(gv, a.idx + static_cast<int64_t>(b) * a.k, a.score + static_cast<int64_t>(b) * a.k, a.k, a.blend, l,
-                   lane);
+  if (lane < a.E) p = guide_prob(gv, idx_b, score_b, a.k, a.blend, l, lane);
 
   // 2. threshold
   double tau;
   if (a.mode == FM_TAU_DYNAMIC) {
-    const double s = static_cast<double>(a.score[static_cast<int64_t>(b) * a.k]);
+    const double s = static_cast<double>(score_b[0]);
     if (s != s) tau = 1.0;
     else {
       double t = 1.0 - s;
@@ -106,16 +100,16 @@ __global__ void __launch_bounds__(256) k_select(SelArgs a) {
   // ordered integer keys read from LDS (broadcast reads, independent of
   // each other)
   const uint64_t key = ord_f64(p);
-  if (lane < a.E) keys[wv][lane] = key;
+  if (lane < a.E) keys[lane] = key;
   __builtin_amdgcn_s_waitcnt(0);
   __builtin_amdgcn_wave_barrier();
   int rank = 0;
 #pragma unroll 8
   for (int i = 0; i < a.E; ++i) {
-    const uint64_t ki = keys[wv][i];
+    const uint64_t ki = keys[i];
     rank += (ki > key || (ki == key && i < lane)) ? 1 : 0;
   }
-  if (lane < a.E) sorted[wv][rank] = p;
+  if (lane < a.E) sorted[rank] = p;
   __builtin_amdgcn_s_waitcnt(0);
   __builtin_amdgcn_wave_barrier();
 
@@ -128,7 +122,7 @@ __global__ void __launch_bounds__(256) k_select(SelArgs a) {
   for (int k0 = 0; k0 < a.E && !found; k0 += 8) {
     double v[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = k0 + u < a.E ? sorted[wv][k0 + u] : 0.0;
+    for (int u = 0; u < 8; ++u) v[u] = k0 + u < a.E ? sorted[k0 + u] : 0.0;
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       if (found || k0 + u >= a.E) break;
@@ -147,6 +141,76 @@ __global__ void __launch_bounds__(256) k_select(SelArgs a) {
     a.mask_out[row] = mask;
     a.count_out[row] = static_cast<uint8_t>(kk);
   }
+}
+
+__global__ void __launch_bounds__(256) k_select(SelArgs a) {
+  __shared__ double sorted[4][kMaxE];
+  __shared__ uint64_t keys[4][kMaxE];
+  const int wv = threadIdx.x / kWave;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + wv;
+  if (row >= static_cast<int64_t>(a.B) * a.L) return;
+  const int b = static_cast<int>(row / a.L);
+  const int l = static_cast<int>(row - static_cast<int64_t>(b) * a.L);
+  select_row(a, b, l, a.idx + static_cast<int64_t>(b) * a.k, a.score + static_cast<int64_t>(b) * a.k, sorted[wv],
+             keys[wv]);
+}
+
+// The cross-workgroup merge of a match call with the selection after it:
+// one wavefront per (sorted position, layer) row merges the position's
+// partial top-k lists (each of the row's L wavefronts on its own, so that no
+// wave waits for another), the layer-0 one writes the query's matches, and
+// every one selects its layer from the merged matches (staged in LDS).  The
+// same merge as k_finalize and the same selection as k_select.
+struct MergeArgs {
+  const uint64_t* partial;   // [positions][R][KTOP]
+  const int32_t* perm;       // query at each position (NULL: the position itself)
+  int32_t R;                 // lists per position
+  const int32_t* rgrp;       // lists per query group (NULL: R)
+  int32_t qg;                // positions per query group
+  int32_t* idx_out;          // [B][k]
+  float* score_out;          // [B][k]
+};
+
+template <int KTOP>
+__global__ void __launch_bounds__(256) k_merge_select(SelArgs a, MergeArgs m) {
+  __shared__ double sorted[4][kMaxE];
+  __shared__ uint64_t keys[4][kMaxE];
+  __shared__ int32_t midx[4][kMaxK];
+  __shared__ float mscore[4][kMaxK];
+  const int lane = threadIdx.x % kWave;
+  const int wv = threadIdx.x / kWave;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + wv;
+  if (row >= static_cast<int64_t>(a.B) * a.L) return;
+  const int pos = static_cast<int>(row / a.L);
+  const int l = static_cast<int>(row - static_cast<int64_t>(pos) * a.L);
+  const int nr = m.rgrp != nullptr ? m.rgrp[pos / m.qg] : m.R;
+  TopK<KTOP> t;
+  t.clear();
+  for (int r = lane; r < nr; r += kWave) t.merge(m.partial + (static_cast<int64_t>(pos) * m.R + r) * KTOP);
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    uint64_t o[KTOP];
+#pragma unroll
+    for (int jj = 0; jj < KTOP; ++jj) o[jj] = shfl_xor_u64(t.v[jj], off);
+    t.merge(o);
+  }
+  const int b = m.perm != nullptr ? m.perm[pos] : pos;
+  if (lane == 0) {
+#pragma unroll
+    for (int jj = 0; jj < kMaxK; ++jj) {
+      if (jj >= a.k) break;
+      const uint64_t key = jj < KTOP ? t.v[jj < KTOP ? jj : 0] : 0ull;
+      midx[wv][jj] = key_index(key);
+      mscore[wv][jj] = key_score(key);
+      if (l == 0) {
+        m.idx_out[static_cast<int64_t>(b) * a.k + jj] = key_index(key);
+        m.score_out[static_cast<int64_t>(b) * a.k + jj] = key_score(key);
+      }
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_wave_barrier();
+  select_row(a, b, l, midx[wv], mscore[wv], sorted[wv], keys[wv]);
 }
 
 // Misses of the prefetch sets (Section 3): one wavefront per (query, layer)
@@ -213,9 +277,11 @@ hipError_t launch_miss(const StoreView& s, const void* q, int32_t B, int32_t K, 
   return hipGetLastError();
 }
 
-hipError_t launch_select(const StoreView& s, const int32_t* idx, const float* score, int32_t B, int32_t k,
-                         const int32_t* lb, const int32_t* le, const fm_select_params& p, uint64_t* mask_out,
-                         uint8_t* count_out, hipStream_t st) {
+namespace {
+
+SelArgs select_args(const StoreView& s, const int32_t* idx, const float* score, int32_t B, int32_t k,
+                    const int32_t* lb, const int32_t* le, const fm_select_params& p, uint64_t* mask_out,
+                    uint8_t* count_out) {
   SelArgs a;
   a.planes = s.planes;
   a.plane_elems = s.plane_elems;
@@ -238,9 +304,38 @@ hipError_t launch_select(const StoreView& s, const int32_t* idx, const float* sc
   a.mask_out = mask_out;
   a.count_out = count_out;
   a.flags = s.flags;
+  return a;
+}
+
+}  // namespace
+
+hipError_t launch_select(const StoreView& s, const int32_t* idx, const float* score, int32_t B, int32_t k,
+                         const int32_t* lb, const int32_t* le, const fm_select_params& p, uint64_t* mask_out,
+                         uint8_t* count_out, hipStream_t st) {
+  const SelArgs a = select_args(s, idx, score, B, k, lb, le, p, mask_out, count_out);
   const int64_t rows = static_cast<int64_t>(B) * s.L;
   const int64_t blocks = (rows + 3) / 4;
   hipLaunchKernelGGL(k_select, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_merge_select(const StoreView& s, const uint64_t* partial, const int32_t* perm, int32_t B, int32_t R,
+                               int32_t k, int KTOP, const int32_t* rgrp, int32_t qg, int32_t* idx_out,
+                               float* score_out, const SelectFuse& f, hipStream_t st) {
+  const SelArgs a = select_args(s, nullptr, nullptr, B, k, f.lb, f.le, f.p, f.mask_out, f.count_out);
+  MergeArgs m;
+  m.partial = partial;
+  m.perm = perm;
+  m.R = R;
+  m.rgrp = rgrp;
+  m.qg = qg > 0 ? qg : 1;
+  m.idx_out = idx_out;
+  m.score_out = score_out;
+  const int64_t rows = static_cast<int64_t>(B) * s.L;
+  const dim3 grid(static_cast<unsigned>((rows + 3) / 4));
+  if (KTOP == 1) hipLaunchKernelGGL(k_merge_select<1>, grid, dim3(256), 0, st, a, m);
+  else if (KTOP == 4) hipLaunchKernelGGL(k_merge_select<4>, grid, dim3(256), 0, st, a, m);
+  else hipLaunchKernelGGL(k_merge_select<8>, grid, dim3(256), 0, st, a, m);
   return hipGetLastError();
 }
 

@@ -467,7 +467,7 @@ hipError_t sem_tq(int TQ, const SemArgs& a, hipStream_t st) {
 
 hipError_t launch_match_semantic(const StoreView& s, const void* q, int32_t B, int32_t k, int32_t* idx_out,
                                  float* score_out, float* dbg_scores, const Workspace& ws, hipStream_t st,
-                                 const float* mix, double w_self, double w_mix) {
+                                 const float* mix, double w_self, double w_mix, const SelectFuse* fuse) {
   const int KTOP = k == 1 ? 1 : (k <= 4 ? 4 : 8);
   // the dense-output form keeps top-1 lists (k = 1)
   const int tq_max = sem_tq_limit(dbg_scores != nullptr ? 1 : KTOP);
@@ -500,8 +500,12 @@ hipError_t launch_match_semantic(const StoreView& s, const void* q, int32_t B, i
                           &R, st);
       if (err != hipSuccess) return err;
       if (idx_out != nullptr) {
-        err = launch_finalize(ws.partial, nullptr, Bc, R, k, 1, idx_out + static_cast<int64_t>(b0) * k,
-                              score_out + static_cast<int64_t>(b0) * k, st);
+        err = fuse != nullptr
+                  ? launch_merge_select(s, ws.partial, nullptr, Bc, R, k, 1, nullptr, 0,
+                                        idx_out + static_cast<int64_t>(b0) * k,
+                                        score_out + static_cast<int64_t>(b0) * k, fuse->at(b0, s.L), st)
+                  : launch_finalize(ws.partial, nullptr, Bc, R, k, 1, idx_out + static_cast<int64_t>(b0) * k,
+                                    score_out + static_cast<int64_t>(b0) * k, st);
         if (err != hipSuccess) return err;
       }
       continue;
@@ -536,8 +540,12 @@ hipError_t launch_match_semantic(const StoreView& s, const void* q, int32_t B, i
     else err = sem_tq<8>(TQ, a, st);
     if (err != hipSuccess) return err;
     if (idx_out != nullptr) {
-      err = launch_finalize(ws.partial, nullptr, Bc, R, k, KTOP, idx_out + static_cast<int64_t>(b0) * k,
-                            score_out + static_cast<int64_t>(b0) * k, st);
+      err = fuse != nullptr
+                ? launch_merge_select(s, ws.partial, nullptr, Bc, R, k, KTOP, nullptr, 0,
+                                      idx_out + static_cast<int64_t>(b0) * k, score_out + static_cast<int64_t>(b0) * k,
+                                      fuse->at(b0, s.L), st)
+                : launch_finalize(ws.partial, nullptr, Bc, R, k, KTOP, idx_out + static_cast<int64_t>(b0) * k,
+                                  score_out + static_cast<int64_t>(b0) * k, st);
       if (err != hipSuccess) return err;
     }
   }

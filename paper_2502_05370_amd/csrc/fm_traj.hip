@@ -1035,7 +1035,7 @@ size_t traj_qrows_bytes(int L, int E, fm_dtype dt, int b_pad) {
 
 hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int32_t* depth, int32_t max_depth,
                                    int32_t B, int32_t k, int32_t* idx_out, float* score_out, float* dbg_scores,
-                                   const Workspace& ws, hipStream_t st) {
+                                   const Workspace& ws, hipStream_t st, const SelectFuse* fuse) {
   const bool bf = s.map_dtype == FM_BF16;
   const int esz = bf ? 2 : 4;
   const Geo geo = geometry(s.E);
@@ -1077,8 +1077,12 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
                            dbg_scores != nullptr ? dbg_scores + static_cast<int64_t>(b0) * s.n : nullptr, &R, st);
       if (err != hipSuccess) return err;
       if (idx_out != nullptr) {
-        err = launch_finalize(ws.partial, ws.perm, Bc, R, k, 1, idx_out + static_cast<int64_t>(b0) * k,
-                              score_out + static_cast<int64_t>(b0) * k, st);
+        err = fuse != nullptr
+                  ? launch_merge_select(s, ws.partial, ws.perm, Bc, R, k, 1, nullptr, 0,
+                                        idx_out + static_cast<int64_t>(b0) * k,
+                                        score_out + static_cast<int64_t>(b0) * k, fuse->at(b0, s.L), st)
+                  : launch_finalize(ws.partial, ws.perm, Bc, R, k, 1, idx_out + static_cast<int64_t>(b0) * k,
+                                    score_out + static_cast<int64_t>(b0) * k, st);
         if (err != hipSuccess) return err;
       }
       continue;
@@ -1160,8 +1164,12 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
     }
     if (err != hipSuccess) return err;
     if (idx_out != nullptr) {
-      err = launch_finalize(ws.partial, ws.perm, Bc, R, k, KTOP, idx_out + static_cast<int64_t>(b0) * k,
-                            score_out + static_cast<int64_t>(b0) * k, st, ws.rgrp, QG);
+      err = fuse != nullptr
+                ? launch_merge_select(s, ws.partial, ws.perm, Bc, R, k, KTOP, ws.rgrp, QG,
+                                      idx_out + static_cast<int64_t>(b0) * k, score_out + static_cast<int64_t>(b0) * k,
+                                      fuse->at(b0, s.L), st)
+                : launch_finalize(ws.partial, ws.perm, Bc, R, k, KTOP, idx_out + static_cast<int64_t>(b0) * k,
+                                  score_out + static_cast<int64_t>(b0) * k, st, ws.rgrp, QG);
       if (err != hipSuccess) return err;
     }
   }
