@@ -3,7 +3,9 @@
 One step = one pass of the whole hot path over one query batch that is
 already resident in HBM: the batched cosine search over the store (trajectory
 search, Eq. 5, and/or semantic search, Eq. 4, with ranking fused in), then the
-prefetch-set selection (Section 4.3, Eq. 6-8) for every (query, layer) row.
+prefetch-set selection (Section 4.3, Eq. 6-8) for every (query, layer) row,
+each half of the batch through its match-and-select call (the merge of the
+search's partial lists and the selection in one launch).
 
 Default workload: the largest one that fits one GPU, the mixed Qwen1.5-MoE
 batch (1,000,000 stored maps of 24 x 60 bfloat16, each with a 2048-dimension
@@ -16,8 +18,8 @@ Prints ONE JSON line.  ``roofline`` refers to the dominant kernel (the scan
 kernel of the match call; for the mixed workload the slower of the two
 scans, the other one's figures under ``roofline.other``), timed by HIP events
 that the library records right around its launch on the stream it runs on
-(fm_debug_scan_events); ``match_call_us`` is the whole match call (staging,
-scan, merge).  ``cpu_baseline`` is the CPU oracle timed on a bounded sample of
+(fm_debug_scan_events); ``calls_us`` is a step's match-and-select calls
+(staging, scan, merge and selection).  ``cpu_baseline`` is the CPU oracle timed on a bounded sample of
 the same batch.
 
 ``--path dedup`` measures the deduplicating insert instead (Section 4.4):
@@ -769,44 +771,44 @@ def main():
     if traj_k:
         timers[traj_k] = ScanTimer(hip, lib, args.steps)
 
-    def match(i=None, tm=timers):
+    sel = dict(tau=s.tau, k_min=s.k_min, k_max=s.k_max, mode=s.tau_mode, blend=s.blend)
+    h = s.B_sem
+
+    def step(i=None, tm=timers):
+        """One step: each half of the batch through its match-and-select call
+        (search, merge and selection of its rows)."""
         if s.B_sem:
             if i is not None:
                 tm[sem_k].arm(i)
-            fm.match_semantic(store, q_sem, s.k, out=(idx[:s.B_sem], score[:s.B_sem]), workspace=ws_sem,
-                              stream=stream)
+            fm.match_semantic_select(store, q_sem, lb[:h], le[:h], k=s.k, out=(idx[:h], score[:h], mask[:h],
+                                     count[:h]), workspace=ws_sem, stream=stream, **sel)
         if s.B_traj:
             if i is not None:
                 tm[traj_k].arm(i)
-            fm.match_trajectory(store, q_traj, depth, s.k, max_depth=max_depth,
-                                out=(idx[s.B_sem:], score[s.B_sem:]), workspace=ws_traj, stream=stream)
+            fm.match_trajectory_select(store, q_traj, depth, lb[h:], le[h:], k=s.k, max_depth=max_depth,
+                                       out=(idx[h:], score[h:], mask[h:], count[h:]), workspace=ws_traj,
+                                       stream=stream, **sel)
         if i is not None:
             lib.fm_debug_scan_events(None, None)
 
-    def select():
-        fm.select_prefetch(store, idx, score, lb, le, tau=s.tau, k_min=s.k_min, k_max=s.k_max,
-                           mode=s.tau_mode, blend=s.blend, out=(mask, count), stream=stream)
-
     for _ in range(args.warmup):
-        match()
-        select()
+        step()
     torch.cuda.synchronize()
 
-    # Timed region: K steps of (match, select) on one stream.  HIP events
-    # bracket the match call of every step, and the library records a second
-    # pair right around each scan kernel launch on the same stream.
+    # Timed region: K steps of the match-and-select calls on one stream.  HIP
+    # events bracket the calls of every step, and the library records a
+    # second pair right around each scan kernel launch on the same stream.
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
         ev[i][0].record(stream)
-        match(i)
+        step(i)
         ev[i][1].record(stream)
-        select()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     elapsed = t1 - t0
-    match_ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
+    calls_ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
     scan_ms = {k: t.mean_ms(args.steps) for k, t in timers.items() if t is not None}
 
     # Cold scans (outside the timed region): before each of these steps a
@@ -821,8 +823,7 @@ def main():
         torch.cuda.synchronize()
         for i in range(args.cold_reps):
             torch.amax(flush, dim=0, out=sink)
-            match(i, cold)
-            select()
+            step(i, cold)
         torch.cuda.synchronize()
         cold_ms = {k: t.mean_ms(args.cold_reps) for k, t in cold.items() if t is not None}
         del flush
@@ -854,7 +855,7 @@ def main():
     roof["algorithmic_bytes"] = byts
     roof["algorithmic_flops"] = flops
     roof["scan_us"] = {k: v * 1e3 for k, v in scan_ms.items()}
-    roof["match_call_us"] = match_ms * 1e3
+    roof["calls_us"] = calls_ms * 1e3
     for other in scan_ms:
         if other == kernel:
             continue
