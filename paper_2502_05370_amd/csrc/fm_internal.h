@@ -150,6 +150,7 @@ hipError_t launch_sem_mm(const StoreView& s, int32_t Bc, int32_t b_pad, const Wo
 // group); *R_out receives the partial lists per query for k_finalize.
 bool traj_mm_fits(bool bf, int KTOP, int32_t Bc, int32_t max_depth, int nlg, int ksg);
 int traj_mm_group();
+int traj_mm_workgroups();
 hipError_t launch_traj_mm(const StoreView& s, int spl, int lpg, int ksg, int nlg, int32_t max_depth, int32_t b_pad,
                           const Workspace& ws, float* dbg, int32_t* R_out, hipStream_t st);
 hipError_t launch_miss(const StoreView& s, const void* q, int32_t B, int32_t K, const uint64_t* masks,

@@ -268,12 +268,12 @@ __global__ void __launch_bounds__(256) k_traj_prep(PrepArgs a) {
       split2(v, h, l);
     }
     if (BF && a.tiled) {
-      // k_traj_mm layout: sorted tile T = pos / 16 is local tile T / n_qg of
-      // group T % n_qg; the 1 KB operand tile of (layer group, k-step, group,
+      // k_traj_mm layout: sorted tile T = pos / 16 is local tile T % 16 of
+      // band T / 16; the 1 KB operand tile of (layer group, k-step, band,
       // local tile) holds this unit at lane slot 16 g + c
       const int T = pos / 16;
-      const int tg = T % a.n_qg;
-      const int tl = T / a.n_qg;
+      const int tg = T / 16;
+      const int tl = T % 16;
       const int ks = unit / 4;
       const int gg = unit - 4 * ks;
       char* dst = static_cast<char*>(a.ws.qrows) +
@@ -1064,7 +1064,9 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
       pa.b_pad = b_pad;
       pa.qg = QG;
       pa.n_qg = n_qg;
-      pa.G = n_qg;
+      // the bands share the scan's workgroups by the layer groups they walk
+      // (a stage costs about the same however many of its tiles are active)
+      pa.G = traj_mm_workgroups();
       pa.epi16 = 0;
       pa.tiled = 1;
       pa.ws = ws;
@@ -1078,11 +1080,11 @@ hipError_t launch_match_trajectory(const StoreView& s, const void* q, const int3
       if (err != hipSuccess) return err;
       if (idx_out != nullptr) {
         err = fuse != nullptr
-                  ? launch_merge_select(s, ws.partial, ws.perm, Bc, R, k, 1, nullptr, 0,
+                  ? launch_merge_select(s, ws.partial, ws.perm, Bc, R, k, 1, ws.rgrp, QG,
                                         idx_out + static_cast<int64_t>(b0) * k,
                                         score_out + static_cast<int64_t>(b0) * k, fuse->at(b0, s.L), st)
                   : launch_finalize(ws.partial, ws.perm, Bc, R, k, 1, idx_out + static_cast<int64_t>(b0) * k,
-                                    score_out + static_cast<int64_t>(b0) * k, st);
+                                    score_out + static_cast<int64_t>(b0) * k, st, ws.rgrp, QG);
         if (err != hipSuccess) return err;
       }
       continue;

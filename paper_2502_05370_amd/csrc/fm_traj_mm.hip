@@ -8,24 +8,28 @@
 // stored index per query.  k_traj_prep (fm_traj.hip) sorts and stages the
 // queries before it runs; k_finalize merges its partial lists after.
 //
-// Query groups.  The sorted queries form tiles of 16 (deepest first); tile T
-// belongs to group T % n_qg as its local tile T / n_qg, so every group holds
-// the same mix of depths and needs the same work per map.  The workgroups of
-// one map range (one per group) are consecutive in the XCD-aware numbering,
-// run on one XCD at about the same pace, and read the same plane bytes: the
-// store streams from HBM about once, the other groups' reads hit that XCD's
-// L2.  Within a group a query tile takes part in the layer groups its
-// deepest query reaches; shallower queries of the tile contribute their
-// staged zeros.
+// Query bands.  The sorted queries form tiles of 16 (deepest first); tiles
+// 16 b .. 16 b + 15 form band b, which walks only the layer groups its
+// deepest query reaches, and within a band a query tile takes part in the
+// layer groups its own deepest query reaches (shallower queries of the tile
+// contribute their staged zeros).  The scan's 256 workgroups are shared
+// among the bands in proportion to the layer groups they walk (k_traj_prep
+// writes the shares), each band's workgroups covering even shares of the
+// store: with depths spread over the layers, the deep band's stages keep
+// most of their tiles active and the shallow band runs half as many stages
+// per map, whereas bands of mixed depths would each walk every layer with
+// half of their tiles idle.  Each band streams the planes of its own layers
+// (the shallow band's reads of the first layers are not shared with the
+// deep band's).
 //
 // Workgroup: 8 waves, two per SIMD, arranged 2 x 4 over (queries, maps).
-// Wave (wq, wm) holds 128 x 64 float32 accumulators: local query tiles
-// wq, wq + 2, ..., wq + 14 (so the two query rows of waves stay equally
-// deep) against the map blocks wm, wm + 4, wm + 8, wm + 12 of a slice (16
-// blocks of 16 maps).
+// Wave (wq, wm) holds 128 x 64 float32 accumulators: the band's local query
+// tiles wq, wq + 2, ..., wq + 14 (so the two query rows of waves stay
+// equally deep) against the map blocks wm, wm + 4, wm + 8, wm + 12 of a
+// slice (16 blocks of 16 maps).
 //
 // Pipeline: a stage is one k-step of one layer group of one slice.  Its map
-// tiles (1 KB of a plane tile: 8 expert quads of 16 maps) and the group's
+// tiles (1 KB of a plane tile: 8 expert quads of 16 maps) and the band's
 // query tiles (1 KB MFMA operand tiles staged by the prep) are copied
 // global -> LDS by buffer loads straight into ring slot j % 3; tiles of
 // queries that are all shallower than the layer group read as zeros without
@@ -56,16 +60,19 @@ struct TrajMmArgs {
   uint32_t tile_bytes;    // bytes of one 16-map tile of a plane (32 * row)
   const float* rnorm;     // [L][rn_stride] prefix inverse norms
   int32_t rn_stride;
-  const char* qst;        // staged queries: [lg][ks][group][local tile][1 KB]
+  const char* qst;        // staged queries: [lg][ks][band][local tile][1 KB]
   uint32_t qst_bytes;
   const float* rq;        // [b_pad] 1/|q[0:p]| at each sorted position
   const int32_t* sdep;    // [b_pad] depth at each sorted position (0: padding)
   const int32_t* perm;    // [b_pad] query index at each sorted position
-  uint64_t* partial;      // [b_pad][R] one packed key per (position, workgroup of its group)
+  uint64_t* partial;      // [b_pad][R] one packed key per (position, workgroup of its band)
+  const int32_t* pgrp;    // per band: its first workgroup (XCD-aware numbering)
+  const int32_t* rgrp;    // per band: its workgroups
+  const int32_t* ngrp;    // per band: the layer groups its deepest query reaches
   float* dbg;             // optional dense scores [B][n]
   int32_t n, L, row, spl, lpg, ksg, nlg, dmax;
-  int32_t n_qg;           // query groups (256 queries each)
-  int32_t R;              // workgroups per query group
+  int32_t n_qg;           // query bands (256 queries each)
+  int32_t R;              // stride of the partial lists per position (the grid's workgroups)
   int32_t n_blocks;       // 16-map blocks of the store
   int32_t grid;
 };
@@ -74,7 +81,7 @@ constexpr int kW = 8;          // waves per workgroup (two per SIMD)
 constexpr int kGM = 4;         // wave columns over the maps
 constexpr int kNT = 8;         // query tiles per wave
 constexpr int kNB = 4;         // map blocks per wave and slice
-constexpr int kQG = 256;       // queries per group
+constexpr int kQG = 256;       // queries per band
 constexpr int kSB = 16;        // map blocks per slice
 constexpr int kNS = 3;         // ring slots
 constexpr int kMPW = 2;        // map tile copies per wave and stage
@@ -122,21 +129,40 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int g = lane / 16;
   const int c = lane % 16;
 
+  // workgroup -> (query band, share of the store): band b owns the
+  // workgroups [pgrp[b], pgrp[b] + rgrp[b]) of the XCD-aware numbering u
+  // (shared in proportion to the layer groups the bands walk); values read
+  // back wave-uniform
   const int bid = blockIdx.x;
   const int u = (bid % 8) * (a.grid / 8) + bid / 8;
-  const bool active = u < a.n_qg * a.R;
-  const int grp = active ? u % a.n_qg : 0;
-  const int rr = active ? u / a.n_qg : 0;
-  const int b_begin = active ? static_cast<int>((static_cast<int64_t>(rr) * a.n_blocks) / a.R) : 0;
-  const int b_end = active ? static_cast<int>((static_cast<int64_t>(rr + 1) * a.n_blocks) / a.R) : 0;
+  int pg_l = 0x7fffffff, rg_l = 0, ng_l = 0;
+  if (lane < a.n_qg) {
+    pg_l = a.pgrp[lane];
+    rg_l = a.rgrp[lane];
+    ng_l = a.ngrp[lane];
+  }
+  const uint64_t gbal = __ballot(lane < a.n_qg && pg_l <= u);
+  const int qg_u = gbal != 0 ? __popcll(gbal) - 1 : 0;
+  const int Rg = __builtin_amdgcn_readfirstlane(__shfl(rg_l, qg_u, kWave));
+  const int Pg = __builtin_amdgcn_readfirstlane(__shfl(pg_l, qg_u, kWave));
+  const int Ng = __builtin_amdgcn_readfirstlane(__shfl(ng_l, qg_u, kWave));
+  const bool active = gbal != 0 && u - Pg < Rg;
+  const int grp = active ? qg_u : 0;
+  const int rr = active ? u - Pg : 0;
+  const int b_begin = active ? static_cast<int>((static_cast<int64_t>(rr) * a.n_blocks) / Rg) : 0;
+  const int b_end = active ? static_cast<int>((static_cast<int64_t>(rr + 1) * a.n_blocks) / Rg) : 0;
   const int n_slices = (b_end - b_begin + kSB - 1) / kSB;
   const int ksg = a.ksg;
-  const int nlg = a.nlg;
-  const int nst = nlg * ksg;   // stages per slice (at least 2)
+  // the band's layer groups, at least two stages per slice (the staged rows
+  // of layer groups past every query of the band are zeros)
+  int nlg = Ng < 1 ? 1 : Ng;
+  if (nlg * ksg < 2) nlg = 2;
+  if (nlg > a.nlg) nlg = a.nlg;
+  const int nst = nlg * ksg;
   const int nstages = n_slices * nst;
 
-  // sorted position of query c of this wave's tile t
-  auto pos_of = [&](int t) __attribute__((always_inline)) { return ((wq + 2 * t) * a.n_qg + grp) * 16 + c; };
+  // sorted position of query c of this wave's tile t (local tile wq + 2t of the band)
+  auto pos_of = [&](int t) __attribute__((always_inline)) { return (grp * 16 + wq + 2 * t) * 16 + c; };
   float rqv[kNT];
   uint32_t rows4[kNT / 4];   // the query's inverse-norm table row (depth - 1), a byte per tile
   int tmd[kNT];              // depth of the tile's deepest query (wave-uniform)
@@ -175,7 +201,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     // depths of the two local tiles this wave copies
     int qdep[kQPW];
 #pragma unroll
-    for (int i = 0; i < kQPW; ++i) qdep[i] = a.sdep[((w * kQPW + i) * a.n_qg + grp) * 16];
+    for (int i = 0; i < kQPW; ++i) qdep[i] = a.sdep[(grp * 16 + w * kQPW + i) * 16];
 #pragma unroll
     for (int i = 0; i < kQPW; ++i) qdep[i] = __builtin_amdgcn_readfirstlane(qdep[i]);
 
@@ -417,7 +443,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
       uint64_t m = 0;
 #pragma unroll
       for (int ww = 0; ww < kGM; ++ww) m = mbuf[ww * kQG + r] > m ? mbuf[ww * kQG + r] : m;
-      const int p = ((r / 16) * a.n_qg + grp) * 16 + r % 16;
+      const int p = grp * kQG + r;
       a.partial[static_cast<int64_t>(p) * a.R + rr] = m;
     }
   }
@@ -450,14 +476,13 @@ bool traj_mm_fits(bool bf, int KTOP, int32_t Bc, int32_t max_depth, int nlg, int
 
 int traj_mm_group() { return kQG; }
 
+int traj_mm_workgroups() { return 256; }
+
 hipError_t launch_traj_mm(const StoreView& s, int spl, int lpg, int ksg, int nlg, int32_t max_depth, int32_t b_pad,
                           const Workspace& ws, float* dbg, int32_t* R_out, hipStream_t st) {
   const int n_qg = b_pad / kQG;
   const int n_blocks = (s.n + 15) / 16;
-  int R = 256 / n_qg;
-  if (R < 1) R = 1;
-  if (R > n_blocks) R = n_blocks > 0 ? n_blocks : 1;
-  if (R > kMaxPartials) R = kMaxPartials;
+  const int R = traj_mm_workgroups();   // the prep shared them among the bands
   TrajMmArgs a;
   a.planes = static_cast<const char*>(s.planes);
   a.plane_bytes = static_cast<uint32_t>(s.plane_elems * 2);
@@ -470,6 +495,9 @@ hipError_t launch_traj_mm(const StoreView& s, int spl, int lpg, int ksg, int nlg
   a.sdep = ws.sdep;
   a.perm = ws.perm;
   a.partial = ws.partial;
+  a.pgrp = ws.pgrp;
+  a.rgrp = ws.rgrp;
+  a.ngrp = ws.ngrp;
   a.dbg = dbg;
   a.n = s.n;
   a.L = s.L;
@@ -482,7 +510,7 @@ hipError_t launch_traj_mm(const StoreView& s, int spl, int lpg, int ksg, int nlg
   a.n_qg = n_qg;
   a.R = R;
   a.n_blocks = n_blocks;
-  a.grid = (n_qg * R + 7) / 8 * 8;
+  a.grid = R;
   *R_out = R;
   return dbg != nullptr ? traj_mm_launch<true>(a, st) : traj_mm_launch<false>(a, st);
 }
