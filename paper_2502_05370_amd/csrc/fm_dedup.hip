@@ -14,10 +14,11 @@
 //                   keys (RDY descending, y ascending, NaN last);
 //   k_finalize      (shared with the scans) merges the chunks of a row into
 //                   its 8 best candidates;
-//   k_dedup_assign  one wavefront takes the new iterations in batch order:
-//                   each takes its first candidate not yet taken by an
-//                   earlier one (the highest remaining RDY); if all 8 are
-//                   taken it rescans its whole row, skipping taken entries;
+//   k_dedup_assign  one wavefront takes the new iterations in batch order
+//                   (64 at a time, one per lane): each takes its first
+//                   candidate not yet taken by an earlier one (the highest
+//                   remaining RDY); if all 8 are taken it rescans its whole
+//                   row, skipping taken entries;
 //   k_insert_*      (store kernels) write every new iteration to its slot.
 #include "fm_device.h"
 #include "fm_internal.h"
@@ -126,69 +127,94 @@ struct AssignArgs {
 // into the empty slot its own probe ended on (one LDS round trip per step;
 // LDS operations of one wave complete in issue order, so each step sees the
 // previous one's write).  The next row's candidates are read a step ahead.
+// Candidate j (wave-uniform) of lane t (wave-uniform).
+__device__ __forceinline__ int32_t cand_of(const int32_t (&cd)[kCand], int j, int t) {
+  switch (j) {
+    case 0: return __builtin_amdgcn_readlane(cd[0], t);
+    case 1: return __builtin_amdgcn_readlane(cd[1], t);
+    case 2: return __builtin_amdgcn_readlane(cd[2], t);
+    case 3: return __builtin_amdgcn_readlane(cd[3], t);
+    case 4: return __builtin_amdgcn_readlane(cd[4], t);
+    case 5: return __builtin_amdgcn_readlane(cd[5], t);
+    case 6: return __builtin_amdgcn_readlane(cd[6], t);
+    default: return __builtin_amdgcn_readlane(cd[7], t);
+  }
+}
+
+// Insert y into the taken set by one lane among several inserting distinct
+// values at once (compare-and-swap on the empty slot).
+__device__ __forceinline__ void taken_add_concurrent(int32_t* set, int32_t y) {
+  for (int h = hash_slot(y);; h = (h + 1) & (kHashSlots - 1))
+    if (atomicCAS(&set[h], -1, y) == -1) return;
+}
+
+// The new iterations in batch order, 64 at a time (lane = iteration): each
+// lane first drops its candidates taken by earlier chunks (the taken set in
+// LDS), then the chunk is resolved in batch order with wave-wide
+// operations: lane t's choice is its first candidate left, which every
+// later lane then drops; a lane with none left rescans its RDY row against
+// every pick so far.  The chunk's picks join the taken set at its end.
 __global__ void __launch_bounds__(kWave) k_dedup_assign(AssignArgs a) {
   __shared__ int32_t taken[kHashSlots];
-  __shared__ int32_t cand[kChunkB * kCand];
-  __shared__ int32_t picked[kChunkB];
   const int lane = threadIdx.x;
-  const bool reader = lane < kCand && a.size > 0;
   for (int i = lane; i < kHashSlots; i += kWave) taken[i] = -1;
-  if (a.size > 0)
-    for (int i = lane; i < a.m * kCand; i += kWave) cand[i] = a.cand[i];
   for (int i = lane; i < a.n_app; i += kWave) {
     a.slots[i] = a.size + i;
     if (a.slots_out != nullptr) a.slots_out[i] = a.size + i;
   }
   __syncthreads();
-  int32_t next = reader && a.m > 0 ? cand[lane] : -1;
-  for (int r = 0; r < a.m; ++r) {
-    const int32_t y = next;
-    if (reader && r + 1 < a.m) next = cand[(r + 1) * kCand + lane];
-    bool ok = false;
-    int h = 0;
-    if (y >= 0) {
-      for (h = hash_slot(y);; h = (h + 1) & (kHashSlots - 1)) {
-        const int32_t v = taken[h];
-        if (v == y) break;
-        if (v < 0) {
-          ok = true;
-          break;
-        }
-      }
-    }
-    const uint64_t bal = __ballot(ok);
-    if (bal != 0) {
-      if (lane == __builtin_ctzll(bal)) {
-        taken[h] = y;
-        picked[r] = y;
-      }
-    } else if (a.size > 0) {
-      // every candidate is taken: rescan the whole row
-      uint64_t best = 0;
-      const float* row = a.rdy + static_cast<int64_t>(r) * a.size;
-      for (int yy = lane; yy < a.size; yy += kWave) {
-        if (taken_has(taken, yy)) continue;
-        const uint64_t key = make_key(row[yy], yy);
-        best = key > best ? key : best;
-      }
+  for (int c0 = 0; c0 < a.m; c0 += kWave) {
+    const int r = c0 + lane;
+    const int nl = a.m - c0 < kWave ? a.m - c0 : kWave;
+    int32_t cd[kCand];
 #pragma unroll
-      for (int m = 1; m < kWave; m <<= 1) {
-        const uint64_t o = shfl_xor_u64(best, m);
-        best = o > best ? o : best;
+    for (int j = 0; j < kCand; ++j) cd[j] = (r < a.m && a.size > 0) ? a.cand[static_cast<int64_t>(r) * kCand + j] : -1;
+    uint32_t avail = 0;
+#pragma unroll
+    for (int j = 0; j < kCand; ++j)
+      if (cd[j] >= 0 && !taken_has(taken, cd[j])) avail |= 1u << j;
+    int32_t pick = -1;
+    int n_in = 0;   // lanes of this chunk whose picks are already in the taken set
+    for (int t = 0; t < nl; ++t) {
+      const uint32_t at = __builtin_amdgcn_readlane(avail, t);
+      int32_t choice = -1;
+      if (at != 0) {
+        choice = cand_of(cd, __builtin_ctz(at), t);
+      } else if (a.size > 0) {
+        // every candidate of iteration c0 + t is taken: the earlier picks
+        // of the chunk join the set, then the whole row is rescanned
+        if (lane >= n_in && lane < t && pick >= 0) taken_add_concurrent(taken, pick);
+        n_in = t;
+        __builtin_amdgcn_s_waitcnt(0);
+        __builtin_amdgcn_wave_barrier();
+        uint64_t best = 0;
+        const float* row = a.rdy + static_cast<int64_t>(c0 + t) * a.size;
+        for (int yy = lane; yy < a.size; yy += kWave) {
+          if (taken_has(taken, yy)) continue;
+          const uint64_t key = make_key(row[yy], yy);
+          best = key > best ? key : best;
+        }
+#pragma unroll
+        for (int m = 1; m < kWave; m <<= 1) {
+          const uint64_t o = shfl_xor_u64(best, m);
+          best = o > best ? o : best;
+        }
+        choice = key_index(best);
       }
-      const int32_t pick = key_index(best);
-      if (lane == 0) {
-        if (pick >= 0) taken_add(taken, pick);
-        picked[r] = pick;
+      if (lane == t) pick = choice;
+      if (choice >= 0) {
+#pragma unroll
+        for (int j = 0; j < kCand; ++j) avail &= cd[j] == choice ? ~(1u << j) : ~0u;
       }
-    } else if (lane == 0) {
-      picked[r] = -1;
     }
-  }
-  __syncthreads();
-  for (int i = lane; i < a.m; i += kWave) {
-    a.slots[a.n_app + i] = picked[i];
-    if (a.slots_out != nullptr) a.slots_out[a.n_app + i] = picked[i];
+    // the chunk's remaining picks join the taken set (distinct values)
+    if (lane >= n_in && lane < nl && pick >= 0) taken_add_concurrent(taken, pick);
+    if (r < a.m) {
+      a.slots[a.n_app + r] = pick;
+      if (a.slots_out != nullptr) a.slots_out[a.n_app + r] = pick;
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_wave_barrier();
   }
 }
 
