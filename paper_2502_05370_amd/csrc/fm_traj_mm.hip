@@ -95,26 +95,9 @@ constexpr int kLds = kNS * kSlot + 2 * kTab;
 static_assert(kSB == kW * kMPW && kQG / 16 == kW * kQPW, "copies per stage");
 static_assert(kLds <= 160 * 1024, "LDS");
 
-// Position of stage j: slice si, layer group lg, k-step ks and ring slot.
-struct TmPos {
-  int j, si, lg, ks, slot;
-};
-
-__device__ __forceinline__ TmPos tm_next(const TmPos& p, int ksg, int nlg) {
-  TmPos q;
-  q.j = p.j + 1;
-  const bool kwrap = p.ks + 1 == ksg;
-  const bool lwrap = kwrap && p.lg + 1 == nlg;
-  q.ks = kwrap ? 0 : p.ks + 1;
-  q.lg = lwrap ? 0 : (kwrap ? p.lg + 1 : p.lg);
-  q.si = lwrap ? p.si + 1 : p.si;
-  q.slot = p.slot + 1 == kNS ? 0 : p.slot + 1;
-  return q;
-}
-
 }  // namespace
 
-template <bool DBG>
+template <bool DBG, int KSG>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) k_traj_mm(TrajMmArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   unsigned char* ring = smem;                    // [kNS][kSlot]
@@ -152,18 +135,20 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int b_begin = active ? static_cast<int>((static_cast<int64_t>(rr) * a.n_blocks) / Rg) : 0;
   const int b_end = active ? static_cast<int>((static_cast<int64_t>(rr + 1) * a.n_blocks) / Rg) : 0;
   const int n_slices = (b_end - b_begin + kSB - 1) / kSB;
-  const int ksg = a.ksg;
   // the band's layer groups, at least two stages per slice (the staged rows
   // of layer groups past every query of the band are zeros)
   int nlg = Ng < 1 ? 1 : Ng;
-  if (nlg * ksg < 2) nlg = 2;
+  if (nlg * KSG < 2) nlg = 2;
   if (nlg > a.nlg) nlg = a.nlg;
-  const int nst = nlg * ksg;
+  // stages per slice, an even count: with one k-step per layer group an odd
+  // count gets one more group, past every query of the band (its tiles take
+  // no MFMAs; past the store's groups its copies read as zeros)
+  if (KSG == 1) nlg += nlg & 1;
+  const int nst = nlg * KSG;
   const int nstages = n_slices * nst;
 
   // sorted position of query c of this wave's tile t (local tile wq + 2t of the band)
   auto pos_of = [&](int t) __attribute__((always_inline)) { return (grp * 16 + wq + 2 * t) * 16 + c; };
-  float rqv[kNT];
   uint32_t rows4[kNT / 4];   // the query's inverse-norm table row (depth - 1), a byte per tile
   int tmd[kNT];              // depth of the tile's deepest query (wave-uniform)
 #pragma unroll
@@ -171,16 +156,20 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
   for (int t = 0; t < kNT; ++t) {
     const int p = pos_of(t);
-    rqv[t] = a.rq[p];
     const int d = a.sdep[p];
     rows4[t / 4] |= static_cast<uint32_t>(d > 0 ? d - 1 : 0) << (8 * (t % 4));
     tmd[t] = __builtin_amdgcn_readfirstlane(d);   // lane 0 holds row 0 of the tile, its deepest query
   }
+  // Best map per query tile, ranked by dot * 1/|x[0:p]|: the query's own
+  // factor 1/|q[0:p]| is positive (or 0 for a zero query, where every score
+  // is 0) and does not change the order, so it is applied once at the end.
+  // A NaN score ranks as the lowest finite float, below every other score.
+  constexpr float kNanFloor = -3.40282347e38f;
   float best_s[kNT];
   int best_i[kNT];
 #pragma unroll
   for (int t = 0; t < kNT; ++t) {
-    best_s[t] = kEmptyScore;
+    best_s[t] = -__builtin_inff();
     best_i[t] = -1;
   }
 
@@ -188,22 +177,16 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     // Lane L of a map tile copy takes 16 bytes of quad L / 8 (maps 2m, 2m+1,
     // m = L % 8) of k-step ks: slots 32 ks + 4 (L / 8) .. +3 lie in layer li
     // of the layer group at expert e0; quads past the row read as zeros.
-    uint32_t loff[2];
-    bool qv[2];
+    uint32_t loff[KSG];
+    bool qv[KSG];
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
+    for (int ks = 0; ks < KSG; ++ks) {
       const int s0 = 32 * ks + 4 * (lane / 8);
       const int li = s0 / a.spl;
       const int e0 = s0 - li * a.spl;
-      qv[ks] = ks < ksg && e0 < a.row;
+      qv[ks] = e0 < a.row;
       loff[ks] = static_cast<uint32_t>(li) * a.plane_bytes + static_cast<uint32_t>((e0 / 4) * 128 + (lane % 8) * 16);
     }
-    // depths of the two local tiles this wave copies
-    int qdep[kQPW];
-#pragma unroll
-    for (int i = 0; i < kQPW; ++i) qdep[i] = a.sdep[(grp * 16 + w * kQPW + i) * 16];
-#pragma unroll
-    for (int i = 0; i < kQPW; ++i) qdep[i] = __builtin_amdgcn_readfirstlane(qdep[i]);
 
     const __amdgpu_buffer_rsrc_t rs_q = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<char*>(a.qst), static_cast<short>(0), static_cast<int>(a.qst_bytes), kBufWord3);
@@ -211,61 +194,103 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
         const_cast<float*>(a.rnorm), static_cast<short>(0),
         static_cast<int>(static_cast<uint32_t>(a.L) * static_cast<uint32_t>(a.rn_stride) * 4u), kBufWord3);
 
-    // Copy `part` of the stage at position p into its ring slot: parts 0 and
-    // 1 a map tile each, 2 and 3 a query tile each, and part 4, at a slice's
-    // last k-step only, kNTAB table rows (whether or not p is past the last
-    // stage, so that the counts depend on the position only).  Positions past
-    // the last stage use offsets past every descriptor.
-    auto load_part = [&](const TmPos& p, int part) __attribute__((always_inline)) {
-      const bool real = p.j < nstages;
-      const int lg = real ? p.lg : 0;
-      const int ks = real ? p.ks : 0;
-      const int l0 = lg * a.lpg;
-      unsigned char* slot = ring + p.slot * kSlot;
-      const int blk0 = b_begin + p.si * kSB;
+    // The copies run kNS stages ahead of the MFMAs.  Their position (the
+    // "copy position") is kept as running scalars, stepped by one stage per
+    // stage: its layer group's first plane and byte count (the map
+    // descriptor), the byte offset of its staged query tiles, and its slice;
+    // the vector offsets of this wave's tiles depend on the slice only.
+    // (Scalar instructions are issued one per SIMD every fourth cycle and
+    // both waves of a SIMD need theirs: per-stage scalar work is kept small.)
+    const uint64_t lpgb = static_cast<uint64_t>(a.lpg) * a.plane_bytes;   // bytes of a layer group
+    const int last_lg = (a.L + a.lpg - 1) / a.lpg - 1;                     // the store's last group
+    const uint32_t full_rec = static_cast<uint32_t>(lpgb);
+    const uint32_t last_rec = static_cast<uint32_t>(a.L - last_lg * a.lpg) * a.plane_bytes;
+    const uint32_t qstep = static_cast<uint32_t>(a.n_qg) * 16384u;
+    auto rec_of = [&](int lg) __attribute__((always_inline)) {
+      return lg < last_lg ? full_rec : (lg == last_lg ? last_rec : 0u);
+    };
+    uint64_t c_base = reinterpret_cast<uint64_t>(a.planes);
+    uint32_t c_rec = rec_of(0);
+    int c_lg = 0;
+    uint32_t c_qoff = static_cast<uint32_t>(grp) * 16384u;
+    int c_blk0 = b_begin;
+    int c_tab = 0;          // which inverse-norm table the copy position's slice fills
+    int c_slot = 0;         // ring slot of the current stage = slot of the copy position
+    bool tab_prev = false;  // the copies issued last included table rows
+    // this wave's map tiles of the copy position's slice: byte offset in a
+    // plane and whether the block lies in the workgroup's range (copies of
+    // blocks past it, and of quads past the row, are outside every descriptor)
+    uint32_t c_moff[kMPW];
+    bool c_mok[kMPW];
+    auto set_slice = [&](int blk0) __attribute__((always_inline)) {
+#pragma unroll
+      for (int m = 0; m < kMPW; ++m) {
+        const int blk = blk0 + w * kMPW + m;
+        c_moff[m] = static_cast<uint32_t>(blk) * a.tile_bytes;
+        c_mok[m] = blk < b_end;
+      }
+    };
+    set_slice(b_begin);
+    const uint32_t vqo = static_cast<uint32_t>(w * kQPW * 1024 + lane * 16);
+
+    // Part `part` of the copies of the copy position (k-step KSC of its layer
+    // group) into the current stage's slot: parts 0 and 1 a map tile each, 2
+    // and 3 a query tile each, 4 the table rows when the position is its
+    // slice's last stage.
+    auto issue_part = [&](auto ksc_c, int part, bool with_tab) __attribute__((always_inline)) {
+      constexpr int KSC = decltype(ksc_c)::value;
+      unsigned char* slot = ring + c_slot * kSlot;
       if (part < kMPW) {
-        const int nl = a.L - l0 < a.lpg ? a.L - l0 : a.lpg;
         const __amdgpu_buffer_rsrc_t rs_map = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<char*>(a.planes + static_cast<uint64_t>(l0) * a.plane_bytes), static_cast<short>(0),
-            static_cast<int>(static_cast<uint32_t>(nl) * a.plane_bytes), kBufWord3);
-        const uint32_t lo = ks ? loff[1] : loff[0];
-        const bool lv = ks ? qv[1] : qv[0];
+            reinterpret_cast<char*>(c_base), static_cast<short>(0), static_cast<int>(c_rec), kBufWord3);
         const int tile = w * kMPW + part;
-        const int blk = blk0 + tile;
-        uint32_t off = lv ? lo + static_cast<uint32_t>(blk) * a.tile_bytes : kOutside;
-        off = (real && blk < b_end) ? off : kOutside;
-        // (opaque, so that the copy stays unconditional rather than becoming
-        // a branch on the lanes' quad validity)
-        asm volatile("" : "+v"(off));
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_map, (lds_vp)(slot + tile * 1024), 16, static_cast<int>(off), 0, 0,
-                                                 0);
+        const uint32_t off = (qv[KSC] && c_mok[part]) ? loff[KSC] + c_moff[part] : kOutside;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_map, (lds_vp)(slot + tile * 1024), 16, static_cast<int>(off), 0,
+                                                 0, 0);
       } else if (part < kNI) {
         const int i = part - kMPW;
-        const uint32_t qbase = static_cast<uint32_t>(((lg * ksg + ks) * a.n_qg + grp) * 16) * 1024u;
-        const int tl = w * kQPW + i;
-        const uint32_t off = (real && qdep[i] > l0) ? qbase + static_cast<uint32_t>(tl * 1024 + lane * 16) : kOutside;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_q, (lds_vp)(slot + (kSB + tl) * 1024), 16, static_cast<int>(off),
-                                                 0, 0, 0);
-      } else if (p.lg == nlg - 1 && p.ks == ksg - 1) {
-        const uint32_t ys = static_cast<uint32_t>(16 * blk0);
-        unsigned char* tb = tab + (p.si & 1) * kTab;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_q, (lds_vp)(slot + (kSB + w * kQPW + i) * 1024), 16,
+                                                 static_cast<int>(c_qoff + vqo + static_cast<uint32_t>(i * 1024)), 0,
+                                                 0, 0);
+      } else if (with_tab) {
+        unsigned char* tb = tab + c_tab * kTab;
 #pragma unroll
         for (int i = 0; i < kNTAB; ++i) {
           const int r = w * kNTAB + i;
-          const uint32_t off =
-              (real && r < a.dmax) ? (static_cast<uint32_t>(r) * static_cast<uint32_t>(a.rn_stride) + ys) * 4u +
-                                         static_cast<uint32_t>(lane * 16)
-                                   : kOutside;
+          const uint32_t off = r < a.dmax ? (static_cast<uint32_t>(r) * static_cast<uint32_t>(a.rn_stride) +
+                                             static_cast<uint32_t>(16 * c_blk0)) * 4u + static_cast<uint32_t>(lane * 16)
+                                          : kOutside;
           __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_rn, (lds_vp)(tb + r * 1024), 16, static_cast<int>(off), 0, 0, 0);
         }
       }
     };
-    auto load_stage = [&](const TmPos& p) __attribute__((always_inline)) {
-#pragma unroll
-      for (int part = 0; part <= kNI; ++part) load_part(p, part);
+    // Step the copy position past a stage: k-step KSC of its layer group,
+    // the group's last k-step when KSC == KSG - 1 (then the next group, or
+    // the next slice after the slice's last group).
+    auto step_copy = [&](auto ksc_c, bool with_tab) __attribute__((always_inline)) {
+      constexpr int KSC = decltype(ksc_c)::value;
+      c_slot = c_slot == kNS - 1 ? 0 : c_slot + 1;
+      c_qoff += qstep;
+      tab_prev = with_tab;
+      if constexpr (KSC == KSG - 1) {
+        if (with_tab) {
+          c_lg = 0;
+          c_base = reinterpret_cast<uint64_t>(a.planes);
+          c_rec = rec_of(0);
+          c_qoff = static_cast<uint32_t>(grp) * 16384u;
+          c_blk0 += kSB;
+          c_tab ^= 1;
+          set_slice(c_blk0);
+        } else {
+          ++c_lg;
+          c_base += lpgb;
+          c_rec = rec_of(c_lg);
+        }
+      }
     };
-    auto has_tab = [&](const TmPos& p) __attribute__((always_inline)) {
-      return p.lg == nlg - 1 && p.ks == ksg - 1;
+    auto copy_last = [&](auto ksc_c) __attribute__((always_inline)) {
+      constexpr int KSC = decltype(ksc_c)::value;
+      return KSC == KSG - 1 && c_lg == nlg - 1;
     };
 
     floatx4 acc[kNB][kNT];
@@ -316,16 +341,17 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int y = y0 + r;
-            const float s = acc[i][t][r] * rqv[t] * xr[t % 4][r];
             if constexpr (DBG) {
+              // the dense form writes every cosine and keeps no lists
               const int p = pos_of(t);
               const int b = a.perm[p];
-              if (b >= 0 && y < a.n) a.dbg[static_cast<int64_t>(b) * a.n + y] = s;
-            }
-            const float sv = __builtin_fmaxf(s, kNanScore);
-            if ((full || y < a.n) && sv > best_s[t]) {
-              best_s[t] = sv;
-              best_i[t] = y;
+              if (b >= 0 && y < a.n) a.dbg[static_cast<int64_t>(b) * a.n + y] = acc[i][t][r] * a.rq[p] * xr[t % 4][r];
+            } else {
+              const float sv = __builtin_fmaxf(acc[i][t][r] * xr[t % 4][r], kNanFloor);
+              if ((full || y < a.n) && sv > best_s[t]) {
+                best_s[t] = sv;
+                best_i[t] = y;
+              }
             }
           }
         }
@@ -343,14 +369,30 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
         }
     };
 
-    // prologue: the copies of stages 0 .. 2, then stage 0's fragments
-    TmPos pl{0, 0, 0, 0, 0};
-    bool tab_last = false;   // the latest copies issued include a table
+    // depth of each of this wave's tiles' deepest query, tile t at lane t:
+    // the tiles active in a layer group are those reaching its first layer
+    const int vtmd = lane < kNT ? a.sdep[(grp * 16 + wq + 2 * lane) * 16] : 0;
+
+    // prologue: the copies of stages 0 .. kNS-1, then stage 0's fragments
 #pragma unroll
     for (int s = 0; s < kNS; ++s) {
-      tab_last = has_tab(pl);
-      load_stage(pl);
-      pl = tm_next(pl, ksg, nlg);
+      if constexpr (KSG == 2) {
+        if (s % 2 == 0) {
+#pragma unroll
+          for (int part = 0; part <= kNI; ++part) issue_part(std::integral_constant<int, 0>{}, part, false);
+          step_copy(std::integral_constant<int, 0>{}, false);
+        } else {
+          const bool tl = copy_last(std::integral_constant<int, 1>{});
+#pragma unroll
+          for (int part = 0; part <= kNI; ++part) issue_part(std::integral_constant<int, 1>{}, part, tl);
+          step_copy(std::integral_constant<int, 1>{}, tl);
+        }
+      } else {
+        const bool tl = copy_last(std::integral_constant<int, 0>{});
+#pragma unroll
+        for (int part = 0; part <= kNI; ++part) issue_part(std::integral_constant<int, 0>{}, part, tl);
+        step_copy(std::integral_constant<int, 0>{}, tl);
+      }
     }
     u16x8 fa0[kNB], fa1[kNB], fb[kNT];
     wait_vmcnt<0>();
@@ -361,66 +403,91 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     for (int t = 0; t < kNT; ++t) fb[t] = read_qfrag(0, t);
     wait_lgkm0();
 
-    TmPos cur{0, 0, 0, 0, 0};
-    auto stage = [&](u16x8 (&fa)[kNB], u16x8 (&na)[kNB]) __attribute__((always_inline)) {
+    // One stage: its MFMAs (tiles whose deepest query reaches first layer
+    // l_first), the next stage's fragments, and the copy position's copies
+    // (k-step KSC of its group) into the current slot.  A slice's LAST stage
+    // reads no fragments: the next slice's are read after the epilogue, so
+    // that none of them is held through it.
+    auto stage = [&](auto ksc_c, auto last_c, int l_first, u16x8 (&fa)[kNB], u16x8 (&na)[kNB])
+                     __attribute__((always_inline)) {
+      constexpr bool LAST = decltype(last_c)::value;
       // stage j+1's copies have landed once only the latest ones (those of
       // stage j+2) are outstanding
-      if (tab_last) wait_vmcnt<kNI + kNTAB>();
+      if (tab_prev) wait_vmcnt<kNI + kNTAB>();
       else wait_vmcnt<kNI>();
       raw_barrier();
-      const TmPos pc = pl;   // the stage whose copies this one issues
-      tab_last = has_tab(pc);
-      pl = tm_next(pl, ksg, nlg);
-      const TmPos nxt = tm_next(cur, ksg, nlg);
-      const int sn = nxt.slot;
+      const bool tl = copy_last(ksc_c);
+      const int sn = c_slot == kNS - 1 ? 0 : c_slot + 1;
+      if constexpr (!LAST) {
 #pragma unroll
-      for (int i = 0; i < kNB; ++i) na[i] = read_mfrag(sn, i);
-      // active tiles: those whose deepest query reaches the layer group
-      const int l_first = cur.lg * a.lpg;
-      int nact = 0;   // (the depths fall with t)
-#pragma unroll
-      for (int t = 0; t < kNT; ++t) nact = tmd[t] > l_first ? t + 1 : nact;
+        for (int i = 0; i < kNB; ++i) na[i] = read_mfrag(sn, i);
+      }
+      const int nact = __builtin_popcountll(__ballot(vtmd > l_first));   // the depths fall with t
       __builtin_amdgcn_s_setprio(1);
       // per tile a uniform branch: its MFMAs, then its fragment of the next
-      // stage into the register they have just read; copy part t of stage
-      // j+3 after tile t (a copy can hold up this wave's issue while the
-      // vector memory unit is busy; the MFMAs already issued keep running)
+      // stage into the register they have just read; copy part t after tile t
 #pragma unroll
       for (int t = 0; t < kNT; ++t) {
         if (t < nact) {
 #pragma unroll
           for (int i = 0; i < kNB; ++i) acc[i][t] = mfma_bf16(fa[i], fb[t], acc[i][t]);
-          fb[t] = read_qfrag(sn, t);
+          if constexpr (!LAST) fb[t] = read_qfrag(sn, t);
         }
-        if (t <= kNI) load_part(pc, t);
+        if (t <= kNI) issue_part(ksc_c, t, tl);
       }
       __builtin_amdgcn_s_setprio(0);
-      // the next stage starts a slice: every tile's fragment
-      if (nxt.lg == 0 && nxt.ks == 0) {
-#pragma unroll
-        for (int t = 0; t < kNT; ++t) fb[t] = read_qfrag(sn, t);
-      }
-      wait_lgkm0();
-      cur = nxt;
+      step_copy(ksc_c, tl);
+      if constexpr (!LAST) wait_lgkm0();
     };
-    // per slice: its stages (pairs, then one more when nst is odd, after
-    // which the next slice's map fragments sit in fa1 and are moved to fa0),
-    // then the epilogue
+    using C0 = std::integral_constant<int, 0>;
+    using CA = std::integral_constant<int, KSG - 1>;
+    using F = std::false_type;
+    using T = std::true_type;
+    // Per slice its stages in pairs, the epilogue, then the next slice's
+    // first fragments (into fa0 and fb).  The copy position is kNS = 3
+    // stages ahead: with two k-steps per layer group the first stage of a
+    // pair (k-step 0) copies k-step 1 and the second k-step 0.
     for (int si = 0; si < n_slices; ++si) {
-      for (int s2 = 0; s2 + 1 < nst; s2 += 2) {
-        stage(fa0, fa1);
-        stage(fa1, fa0);
+      int l0 = 0;
+      for (int s2 = 0; s2 + 2 < nst; s2 += 2) {
+        stage(CA{}, F{}, l0, fa0, fa1);
+        if constexpr (KSG == 1) l0 += a.lpg;
+        stage(C0{}, F{}, l0, fa1, fa0);
+        l0 += a.lpg;
       }
-      if (nst & 1) {
-        stage(fa0, fa1);
-#pragma unroll
-        for (int i = 0; i < kNB; ++i) fa0[i] = fa1[i];
-      }
+      stage(CA{}, F{}, l0, fa0, fa1);
+      if constexpr (KSG == 1) l0 += a.lpg;
+      stage(C0{}, T{}, l0, fa1, fa0);
       epilogue(si);
+      // the next stage's slot (its copies have landed: waited for at the
+      // start of the last stage)
+#pragma unroll
+      for (int i = 0; i < kNB; ++i) fa0[i] = read_mfrag(c_slot, i);
+#pragma unroll
+      for (int t = 0; t < kNT; ++t) fb[t] = read_qfrag(c_slot, t);
+      wait_lgkm0();
     }
     wait_vmcnt<0>();   // the trailing copies
   }
   __syncthreads();
+
+  // the cosine of each tile's best: its score times 1/|q[0:p]|; a NaN score
+  // takes the in-scan NaN value, and a NaN query (every cosine NaN) the
+  // lowest index among this lane's maps
+  const int y_first = 16 * (b_begin + wm) + 4 * g;
+  const bool first_ok = b_begin + wm < b_end && y_first < a.n;
+#pragma unroll
+  for (int t = 0; t < kNT; ++t) {
+    const float rq = a.rq[pos_of(t)];
+    if (best_i[t] >= 0) {
+      if (rq != rq) {
+        best_s[t] = kNanScore;
+        best_i[t] = first_ok ? y_first : -1;
+      } else {
+        best_s[t] = best_s[t] == kNanFloor ? kNanScore : best_s[t] * rq;
+      }
+    }
+  }
 
   // merge: the four lane groups of a query, then the kGM waves of its tile row
   uint64_t key[kNT];
@@ -451,9 +518,9 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
 
 namespace {
 
-template <bool DBG>
+template <bool DBG, int KSG>
 hipError_t traj_mm_launch(const TrajMmArgs& a, hipStream_t st) {
-  auto kern = k_traj_mm<DBG>;
+  auto kern = k_traj_mm<DBG, KSG>;
   hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
                                        kLds);
   if (err != hipSuccess) return err;
@@ -471,7 +538,7 @@ hipError_t traj_mm_launch(const TrajMmArgs& a, hipStream_t st) {
 }  // namespace
 
 bool traj_mm_fits(bool bf, int KTOP, int32_t Bc, int32_t max_depth, int nlg, int ksg) {
-  return bf && KTOP == 1 && Bc > 128 && max_depth <= kRows && nlg * ksg >= 2;
+  return bf && KTOP == 1 && Bc > 128 && max_depth <= kRows && nlg * ksg >= 2 && (ksg == 1 || ksg == 2);
 }
 
 int traj_mm_group() { return kQG; }
@@ -512,7 +579,8 @@ hipError_t launch_traj_mm(const StoreView& s, int spl, int lpg, int ksg, int nlg
   a.n_blocks = n_blocks;
   a.grid = R;
   *R_out = R;
-  return dbg != nullptr ? traj_mm_launch<true>(a, st) : traj_mm_launch<false>(a, st);
+  if (ksg == 2) return dbg != nullptr ? traj_mm_launch<true, 2>(a, st) : traj_mm_launch<false, 2>(a, st);
+  return dbg != nullptr ? traj_mm_launch<true, 1>(a, st) : traj_mm_launch<false, 1>(a, st);
 }
 
 }  // namespace fm

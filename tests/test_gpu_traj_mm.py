@@ -111,3 +111,24 @@ def test_traj_mm_zero_and_nan_rows():
     oi, os_ = oracle_match(s, a)
     rep = compare_match(s, a, g.idx, g.score, oi, os_, np.arange(s.B))
     assert not rep.failures, rep.failures[:5]
+
+
+def test_traj_mm_signed_and_scaled_queries():
+    """Queries of either sign and of norms far from 1 (bf16 values scaled by
+    powers of two, exactly): a query whose cosines are all negative keeps its
+    least negative map, and the ranking does not depend on the query's norm."""
+    s = _bf16_spec(5, 60, 24, 3001, 300, 23)
+    a = synth.generate(s)
+    q = a["q_traj"].view(np.uint16).astype(np.uint32) << 16
+    qf = q.view(np.float32).reshape(a["q_traj"].shape).copy()
+    qf[0::3] *= -1.0          # every cosine of these queries is <= 0
+    qf[1::3] *= 64.0          # |q| >> 1
+    qf[2::6] *= 1.0 / 64.0    # |q| << 1
+    a["q_traj"] = synth.bf16_bits(qf.reshape(-1)).reshape(a["q_traj"].shape)
+    print(f"signed/scaled E=60 n={s.n} B_traj={s.B_traj}", flush=True)
+    g = run_gpu(s, a, max_depth=24)
+    assert g.flags == 0
+    oi, os_ = oracle_match(s, a)
+    rep = compare_match(s, a, g.idx, g.score, oi, os_, np.arange(s.B))
+    assert not rep.failures, rep.failures[:5]
+    assert np.all(g.score[0::3, 0] <= 0.0)
