@@ -422,16 +422,20 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
         for (int i = 0; i < kNB; ++i) na[i] = read_mfrag(sn, i);
       }
-      const int nact = __builtin_popcountll(__ballot(vtmd > l_first));   // the depths fall with t
+      // (tiles at lanes 0..7: the low half of the ballot)
+      const int nact = __builtin_popcount(static_cast<uint32_t>(__ballot(vtmd > l_first)));   // the depths fall with t
       __builtin_amdgcn_s_setprio(1);
       // per tile a uniform branch: its MFMAs, then its fragment of the next
       // stage into the register they have just read; copy part t after tile t
+      // (the fragment address is computed once, not in every tile's branch)
+      uint32_t qa = static_cast<uint32_t>(sn * kSlot + (kSB + wq) * 1024 + lane * 16);
+      asm volatile("" : "+v"(qa));
 #pragma unroll
       for (int t = 0; t < kNT; ++t) {
         if (t < nact) {
 #pragma unroll
           for (int i = 0; i < kNB; ++i) acc[i][t] = mfma_bf16(fa[i], fb[t], acc[i][t]);
-          if constexpr (!LAST) fb[t] = read_qfrag(sn, t);
+          if constexpr (!LAST) fb[t] = *reinterpret_cast<const u16x8*>(ring + qa + t * 2048);
         }
         if (t <= kNI) issue_part(ksc_c, t, tl);
       }
