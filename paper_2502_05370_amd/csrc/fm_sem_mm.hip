@@ -63,23 +63,6 @@ struct SemMmArgs {
   int32_t grid;
 };
 
-// Position of stage j: slice si, k-step ks and ring slot, stepped without
-// divisions.
-struct MmPos {
-  int j, si, ks, slot;
-};
-
-template <int NS>
-__device__ __forceinline__ MmPos mm_next(const MmPos& p, int ksteps) {
-  MmPos q;
-  q.j = p.j + 1;
-  const bool wrap = p.ks + 1 == ksteps;
-  q.ks = wrap ? 0 : p.ks + 1;
-  q.si = wrap ? p.si + 1 : p.si;
-  q.slot = p.slot + 1 == NS ? 0 : p.slot + 1;
-  return q;
-}
-
 template <int GQ>
 struct MmShape {
   static constexpr int W = 8;                   // waves per workgroup (two per SIMD)
@@ -132,27 +115,31 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   const bool active = u < a.n_qg * a.R;
   const int qgrp = active ? u % a.n_qg : 0;
   const int rr = active ? u / a.n_qg : 0;
-  const int b_begin = active ? static_cast<int>((static_cast<int64_t>(rr) * a.n_blocks) / a.R) : 0;
-  const int b_end = active ? static_cast<int>((static_cast<int64_t>(rr + 1) * a.n_blocks) / a.R) : 0;
+  // (wave-uniform: stated, so that what is derived from them stays scalar)
+  const int b_begin =
+      __builtin_amdgcn_readfirstlane(active ? static_cast<int>((static_cast<int64_t>(rr) * a.n_blocks) / a.R) : 0);
+  const int b_end =
+      __builtin_amdgcn_readfirstlane(active ? static_cast<int>((static_cast<int64_t>(rr + 1) * a.n_blocks) / a.R) : 0);
   const int n_slices = (b_end - b_begin + SB - 1) / SB;
   const int g0 = qgrp * QG;
   const int ksteps = a.ksteps;
   const int nstages = n_slices * ksteps;
   const uint32_t blk32 = static_cast<uint32_t>(ksteps) * 1024u;   // bytes of one 16-row block (d < 2^21)
 
-  float rqv[NT];
-#pragma unroll
-  for (int t = 0; t < NT; ++t) rqv[t] = a.rq[g0 + 16 * (NT * wq + t) + c];
+  // Best map per query tile, ranked by dot * 1/|x|: the query's factor 1/|q|
+  // is positive (or 0 for a zero query, where every score is 0) and does not
+  // change the order, so it is applied once at the end.  A NaN score ranks
+  // as the lowest finite float, below every other score.
+  constexpr float kNanFloor = -3.40282347e38f;
   float best_s[NT];
   int best_i[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
-    best_s[t] = kEmptyScore;
+    best_s[t] = -__builtin_inff();
     best_i[t] = -1;
   }
 
   if (nstages > 0) {
-    const char* xb = reinterpret_cast<const char*>(a.x);
     const char* qbase = reinterpret_cast<const char*>(a.qst) + static_cast<uint64_t>(g0 / 16) * blk32;
     const __amdgpu_buffer_rsrc_t rs_q = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<char*>(qbase), static_cast<short>(0), static_cast<int>(static_cast<uint32_t>(QG / 16) * blk32),
@@ -161,43 +148,71 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
         const_cast<float*>(a.xnorm), static_cast<short>(0), static_cast<int>(static_cast<uint32_t>(a.n) * 4u),
         kBufWord3);
 
-    // Copies of the stage at position p into its ring slot, branch-free so
-    // that they can be placed between the MFMAs: the map tiles through a
-    // descriptor based at the slice's first block whose range ends with the
-    // workgroup's blocks (blocks past it read as zeros), the query tiles
-    // through rs_q, positions past the last stage with offsets past every
-    // descriptor; every stage also issues the norm copy, into a scratch
-    // kilobyte of LDS except at a slice's first stage.
-    auto load_stage = [&](const MmPos& p) __attribute__((always_inline)) {
-      const bool real = p.j < nstages;
-      const int blk0 = b_begin + p.si * SB;
-      int nbk = b_end - blk0;
+    // The copies run NS stages ahead of the MFMAs.  Their position (the
+    // "copy position") is kept as running scalars stepped by one stage per
+    // stage: its slice's first block and map descriptor, its k-step's byte
+    // offset within a block (the loads' scalar offset), the stages left in
+    // its slice, and the norm buffer its slice fills; the vector offsets of
+    // this wave's tiles are fixed.  (Scalar instructions issue one per SIMD
+    // every fourth cycle, shared by both waves of a SIMD.)
+    int c_blk0 = b_begin;
+    uint32_t c_kofs = 0;
+    int c_left = ksteps;
+    int c_nb = 0;          // norm buffer of the copy position's slice
+    int c_slot = 0;        // ring slot of the current stage = slot of the copy position
+    uint64_t c_xbase = reinterpret_cast<uint64_t>(a.x) + static_cast<uint64_t>(static_cast<uint32_t>(b_begin)) * blk32;
+    uint32_t c_xrec;
+    {
+      int nbk = b_end - b_begin;
       nbk = nbk < 0 ? 0 : (nbk > SB ? SB : nbk);
-      nbk = __builtin_amdgcn_readfirstlane(real ? nbk : 0);   // wave-uniform: a scalar descriptor
+      c_xrec = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(nbk) * blk32);
+    }
+    // this wave's map tiles w * MPW + i and query tiles w * QPW + i: the
+    // tile's block offset plus the lane's 16 bytes
+    uint32_t vmo[MPW], vqo[QPW];
+#pragma unroll
+    for (int i = 0; i < MPW; ++i) vmo[i] = static_cast<uint32_t>(w * MPW + i) * blk32 + static_cast<uint32_t>(lane * 16);
+#pragma unroll
+    for (int i = 0; i < QPW; ++i) vqo[i] = static_cast<uint32_t>(w * QPW + i) * blk32 + static_cast<uint32_t>(lane * 16);
+    const uint32_t vno = static_cast<uint32_t>((w * 256 + lane * 4) * 4);
+
+    // Copies of the copy position into the current stage's slot: the map
+    // tiles (blocks past the workgroup's range lie past the slice's
+    // descriptor), the query tiles, and a norm copy, which at a slice's
+    // first k-step brings the slice's map norms and otherwise reads past
+    // every descriptor into a scratch kilobyte.
+    auto issue = [&]() __attribute__((always_inline)) {
+      unsigned char* slot = ring + c_slot * SLOT;
       const __amdgpu_buffer_rsrc_t rs_slice = __builtin_amdgcn_make_buffer_rsrc(
-          const_cast<char*>(xb + static_cast<uint64_t>(static_cast<uint32_t>(blk0)) * blk32), static_cast<short>(0),
-          static_cast<int>(static_cast<uint32_t>(nbk) * blk32), kBufWord3);
-      unsigned char* slot = ring + p.slot * SLOT;
-      const uint32_t kofs = static_cast<uint32_t>(p.ks * 1024 + lane * 16);
+          reinterpret_cast<char*>(c_xbase), static_cast<short>(0), static_cast<int>(c_xrec), kBufWord3);
 #pragma unroll
-      for (int i = 0; i < MPW; ++i) {
-        const int tile = w * MPW + i;
-        const uint32_t off = real ? static_cast<uint32_t>(tile) * blk32 + kofs : kOutside;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_slice, (lds_vp)(slot + tile * 1024), 16, static_cast<int>(off), 0, 0,
-                                                 0);
-      }
+      for (int i = 0; i < MPW; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_slice, (lds_vp)(slot + (w * MPW + i) * 1024), 16,
+                                                 static_cast<int>(vmo[i]), static_cast<int>(c_kofs), 0, 0);
 #pragma unroll
-      for (int i = 0; i < QPW; ++i) {
-        const int tile = w * QPW + i;
-        const uint32_t off = real ? static_cast<uint32_t>(tile) * blk32 + kofs : kOutside;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_q, (lds_vp)(slot + (SB + tile) * 1024), 16, static_cast<int>(off), 0,
-                                                 0, 0);
+      for (int i = 0; i < QPW; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_q, (lds_vp)(slot + (SB + w * QPW + i) * 1024), 16,
+                                                 static_cast<int>(vqo[i]), static_cast<int>(c_kofs), 0, 0);
+      const bool norm = c_kofs == 0 && w < NNORM;
+      const uint32_t noff = norm ? static_cast<uint32_t>(c_blk0) * 64u + vno : kOutside;
+      // (the destination as an offset from the LDS base: a select of two
+      // pointers would lose their address space)
+      const int ndst = norm ? NS * SLOT + (c_nb * NSTRIDE + w * 256) * 4 : NS * SLOT + 2 * NSTRIDE * 4;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_norm, (lds_vp)(smem + ndst), 16, static_cast<int>(noff), 0, 0, 0);
+    };
+    auto step_copy = [&]() __attribute__((always_inline)) {
+      c_slot = c_slot == NS - 1 ? 0 : c_slot + 1;
+      c_kofs += 1024u;
+      if (__builtin_expect(--c_left == 0, 0)) {
+        c_left = ksteps;
+        c_kofs = 0;
+        c_blk0 += SB;
+        c_nb ^= 1;
+        c_xbase += static_cast<uint64_t>(SB) * blk32;
+        int nbk = b_end - c_blk0;
+        nbk = nbk < 0 ? 0 : (nbk > SB ? SB : nbk);
+        c_xrec = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(nbk) * blk32);
       }
-      const bool norm = real && p.ks == 0 && w < NNORM;
-      const uint32_t noff =
-          norm ? static_cast<uint32_t>(((b_begin + p.si * SB) * 16 + w * 256 + lane * 4) * 4) : kOutside;
-      float* ndst = norm ? xnb + (p.si & 1) * NSTRIDE + w * 256 : junk;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_norm, (lds_vp)(ndst), 16, static_cast<int>(noff), 0, 0, 0);
     };
 
     floatx4 acc[NB][NT];
@@ -240,16 +255,16 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int y = y0 + r;
-            const float s = acc[i][t][r] * rqv[t] * rx[r];
             if constexpr (DBG) {
+              // the dense form writes every cosine and keeps no lists
               const int b = g0 + 16 * (NT * wq + t) + c;
-              if (b < a.B && y < a.n) a.dbg[static_cast<int64_t>(b) * a.n + y] = s;
-            }
-            // NaN -> -2 (maximum of a NaN and a number is the number)
-            const float sv = __builtin_fmaxf(s, kNanScore);
-            if ((full || y < a.n) && sv > best_s[t]) {
-              best_s[t] = sv;
-              best_i[t] = y;
+              if (b < a.B && y < a.n) a.dbg[static_cast<int64_t>(b) * a.n + y] = acc[i][t][r] * a.rq[b] * rx[r];
+            } else {
+              const float sv = __builtin_fmaxf(acc[i][t][r] * rx[r], kNanFloor);
+              if ((full || y < a.n) && sv > best_s[t]) {
+                best_s[t] = sv;
+                best_i[t] = y;
+              }
             }
           }
         }
@@ -263,11 +278,10 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     };
 
     // prologue: the copies of stages 0 .. NS-1, then stage 0's fragments
-    MmPos pl{0, 0, 0, 0};
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      load_stage(pl);
-      pl = mm_next<NS>(pl, ksteps);
+      issue();
+      step_copy();
     }
     u16x8 fa0[NB], fa1[NB], fb[NT];
     wait_vmcnt<(NS - 1) * NI>();
@@ -285,15 +299,13 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     // its MFMAs have just read. Blocks past the workgroup's range read as
     // zeros and their scores are never looked at, so a short last slice runs
     // the same code.
-    int slot_next = 1 % NS;
     auto stage = [&](u16x8 (&fa)[NB], u16x8 (&na)[NB]) __attribute__((always_inline)) {
       // stage j+1's copies have landed (this wave's, then everyone's)
       wait_vmcnt<(NS - 2) * NI>();
       raw_barrier();
-      load_stage(pl);
-      pl = mm_next<NS>(pl, ksteps);
-      const int sn = slot_next;
-      slot_next = slot_next + 1 == NS ? 0 : slot_next + 1;
+      const int sn = c_slot == NS - 1 ? 0 : c_slot + 1;
+      issue();
+      step_copy();
 #pragma unroll
       for (int i = 0; i < NB; ++i) na[i] = read_mfrag(sn, i);
       __builtin_amdgcn_s_setprio(1);
@@ -327,6 +339,26 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     wait_vmcnt<0>();   // the trailing copies
   }
   __syncthreads();
+
+  // the cosine of each tile's best: its score times 1/|q|; a NaN score takes
+  // the in-scan NaN value, and a NaN query (every cosine NaN) the lowest
+  // index among this lane's maps
+  if constexpr (!DBG) {
+    const int y_first = 16 * (b_begin + wm) + 4 * g;
+    const bool first_ok = b_begin + wm < b_end && y_first < a.n;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const float rq = a.rq[g0 + 16 * (NT * wq + t) + c];
+      if (best_i[t] >= 0) {
+        if (rq != rq) {
+          best_s[t] = kNanScore;
+          best_i[t] = first_ok ? y_first : -1;
+        } else {
+          best_s[t] = best_s[t] == kNanFloor ? kNanScore : best_s[t] * rq;
+        }
+      }
+    }
+  }
 
   // merge: the four lane groups of a query, then the GM waves of its tile row
   uint64_t key[NT];
