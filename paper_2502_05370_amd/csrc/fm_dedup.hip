@@ -121,26 +121,6 @@ struct AssignArgs {
   int32_t* slots_out;    // caller's copy, or null
 };
 
-// One wavefront: the candidate lists are staged in LDS, then the new
-// iterations are taken in batch order with the taken set in LDS.  Lane j < 8
-// probes candidate j; the lane of the first candidate not taken writes it
-// into the empty slot its own probe ended on (one LDS round trip per step;
-// LDS operations of one wave complete in issue order, so each step sees the
-// previous one's write).  The next row's candidates are read a step ahead.
-// Candidate j (wave-uniform) of lane t (wave-uniform).
-__device__ __forceinline__ int32_t cand_of(const int32_t (&cd)[kCand], int j, int t) {
-  switch (j) {
-    case 0: return __builtin_amdgcn_readlane(cd[0], t);
-    case 1: return __builtin_amdgcn_readlane(cd[1], t);
-    case 2: return __builtin_amdgcn_readlane(cd[2], t);
-    case 3: return __builtin_amdgcn_readlane(cd[3], t);
-    case 4: return __builtin_amdgcn_readlane(cd[4], t);
-    case 5: return __builtin_amdgcn_readlane(cd[5], t);
-    case 6: return __builtin_amdgcn_readlane(cd[6], t);
-    default: return __builtin_amdgcn_readlane(cd[7], t);
-  }
-}
-
 // Insert y into the taken set by one lane among several inserting distinct
 // values at once (compare-and-swap on the empty slot).
 __device__ __forceinline__ void taken_add_concurrent(int32_t* set, int32_t y) {
@@ -148,14 +128,23 @@ __device__ __forceinline__ void taken_add_concurrent(int32_t* set, int32_t y) {
     if (atomicCAS(&set[h], -1, y) == -1) return;
 }
 
-// The new iterations in batch order, 64 at a time (lane = iteration): each
-// lane first drops its candidates taken by earlier chunks (the taken set in
-// LDS), then the chunk is resolved in batch order with wave-wide
-// operations: lane t's choice is its first candidate left, which every
-// later lane then drops; a lane with none left rescans its RDY row against
-// every pick so far.  The chunk's picks join the taken set at its end.
+constexpr int kPropSlots = 2 * kWave;   // proposals of one round (at most kWave)
+
+// The new iterations in batch order, 64 at a time (lane = iteration), one
+// wavefront.  Each lane's choice is its first candidate not taken by an
+// earlier iteration; a choice can only be changed by an earlier iteration of
+// the same chunk taking that very candidate (its earlier candidates are
+// taken already).  So a chunk is resolved in rounds: every unresolved lane
+// proposes its first candidate left; the lanes before the first one whose
+// proposal an earlier lane also made keep their proposals (distinct, and
+// each still its first candidate left), their picks join the taken set, and
+// the next round starts at that lane.  A lane with no candidate left, once
+// every earlier lane is resolved, rescans its whole RDY row against the
+// taken set.  The result is the greedy assignment in batch order.
 __global__ void __launch_bounds__(kWave) k_dedup_assign(AssignArgs a) {
   __shared__ int32_t taken[kHashSlots];
+  __shared__ int32_t pkey[kPropSlots];   // a round's proposals (open addressing)
+  __shared__ int32_t pmin[kPropSlots];   // the lowest lane proposing each
   const int lane = threadIdx.x;
   for (int i = lane; i < kHashSlots; i += kWave) taken[i] = -1;
   for (int i = lane; i < a.n_app; i += kWave) {
@@ -169,26 +158,52 @@ __global__ void __launch_bounds__(kWave) k_dedup_assign(AssignArgs a) {
     int32_t cd[kCand];
 #pragma unroll
     for (int j = 0; j < kCand; ++j) cd[j] = (r < a.m && a.size > 0) ? a.cand[static_cast<int64_t>(r) * kCand + j] : -1;
+    // candidates not taken by earlier chunks
     uint32_t avail = 0;
 #pragma unroll
     for (int j = 0; j < kCand; ++j)
       if (cd[j] >= 0 && !taken_has(taken, cd[j])) avail |= 1u << j;
     int32_t pick = -1;
-    int n_in = 0;   // lanes of this chunk whose picks are already in the taken set
-    for (int t = 0; t < nl; ++t) {
-      const uint32_t at = __builtin_amdgcn_readlane(avail, t);
-      int32_t choice = -1;
-      if (at != 0) {
-        choice = cand_of(cd, __builtin_ctz(at), t);
-      } else if (a.size > 0) {
-        // every candidate of iteration c0 + t is taken: the earlier picks
-        // of the chunk join the set, then the whole row is rescanned
-        if (lane >= n_in && lane < t && pick >= 0) taken_add_concurrent(taken, pick);
-        n_in = t;
-        __builtin_amdgcn_s_waitcnt(0);
-        __builtin_amdgcn_wave_barrier();
+    int lo = 0;   // lanes below lo are resolved, their picks in the taken set
+    while (a.size > 0 && lo < nl) {
+      const bool live = lane >= lo && lane < nl;
+      int32_t prop = -1;   // first candidate left
+#pragma unroll
+      for (int j = kCand - 1; j >= 0; --j) prop = ((avail >> j) & 1u) ? cd[j] : prop;
+      const uint64_t none = __ballot(live && avail == 0);
+      const int tr = none != 0 ? static_cast<int>(__builtin_ctzll(none)) : nl;
+      // the lowest lane of [lo, tr) proposing each value
+      pkey[lane] = -1;
+      pkey[lane + kWave] = -1;
+      pmin[lane] = kWave;
+      pmin[lane + kWave] = kWave;
+      __builtin_amdgcn_s_waitcnt(0);
+      __builtin_amdgcn_wave_barrier();
+      const bool prop_here = lane >= lo && lane < tr;
+      int h = 0;
+      if (prop_here) {
+        h = static_cast<int>((static_cast<uint32_t>(prop) * 2654435761u) >> 25) & (kPropSlots - 1);
+        for (;;) {
+          const int32_t old = atomicCAS(&pkey[h], -1, prop);
+          if (old == -1 || old == prop) break;
+          h = (h + 1) & (kPropSlots - 1);
+        }
+        atomicMin(&pmin[h], lane);
+      }
+      __builtin_amdgcn_s_waitcnt(0);
+      __builtin_amdgcn_wave_barrier();
+      const uint64_t lose = __ballot(prop_here && pmin[h] != lane);
+      const int T = lose != 0 ? static_cast<int>(__builtin_ctzll(lose)) : tr;
+      if (lane >= lo && lane < T) {
+        pick = prop;
+        taken_add_concurrent(taken, prop);
+      }
+      __builtin_amdgcn_s_waitcnt(0);
+      __builtin_amdgcn_wave_barrier();
+      if (T == tr && tr < nl) {
+        // every candidate of iteration c0 + tr is taken: rescan its row
         uint64_t best = 0;
-        const float* row = a.rdy + static_cast<int64_t>(c0 + t) * a.size;
+        const float* row = a.rdy + static_cast<int64_t>(c0 + tr) * a.size;
         for (int yy = lane; yy < a.size; yy += kWave) {
           if (taken_has(taken, yy)) continue;
           const uint64_t key = make_key(row[yy], yy);
@@ -199,16 +214,24 @@ __global__ void __launch_bounds__(kWave) k_dedup_assign(AssignArgs a) {
           const uint64_t o = shfl_xor_u64(best, m);
           best = o > best ? o : best;
         }
-        choice = key_index(best);
+        const int32_t choice = key_index(best);
+        if (lane == tr) {
+          pick = choice;
+          if (choice >= 0) taken_add(taken, choice);
+        }
+        __builtin_amdgcn_s_waitcnt(0);
+        __builtin_amdgcn_wave_barrier();
+        lo = tr + 1;
+      } else {
+        lo = T;
       }
-      if (lane == t) pick = choice;
-      if (choice >= 0) {
+      // the lanes still to resolve drop their candidates taken meanwhile
+      if (lane >= lo && lane < nl) {
 #pragma unroll
-        for (int j = 0; j < kCand; ++j) avail &= cd[j] == choice ? ~(1u << j) : ~0u;
+        for (int j = 0; j < kCand; ++j)
+          if (((avail >> j) & 1u) && taken_has(taken, cd[j])) avail &= ~(1u << j);
       }
     }
-    // the chunk's remaining picks join the taken set (distinct values)
-    if (lane >= n_in && lane < nl && pick >= 0) taken_add_concurrent(taken, pick);
     if (r < a.m) {
       a.slots[a.n_app + r] = pick;
       if (a.slots_out != nullptr) a.slots_out[a.n_app + r] = pick;
