@@ -129,14 +129,18 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   // Best map per query tile, ranked by dot * 1/|x|: the query's factor 1/|q|
   // is positive (or 0 for a zero query, where every score is 0) and does not
   // change the order, so it is applied once at the end.  A NaN score ranks
-  // as the lowest finite float, below every other score.
+  // below every other score: the list starts at the lane's first map with
+  // the lowest finite float, which only a greater score replaces (a NaN
+  // compares false).
   constexpr float kNanFloor = -3.40282347e38f;
+  const int y_first = 16 * (b_begin + wm) + 4 * g;
+  const bool first_ok = b_begin + wm < b_end && y_first < a.n;
   float best_s[NT];
   int best_i[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
-    best_s[t] = -__builtin_inff();
-    best_i[t] = -1;
+    best_s[t] = kNanFloor;
+    best_i[t] = first_ok ? y_first : -1;
   }
 
   if (nstages > 0) {
@@ -249,7 +253,9 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
         for (int r = 0; r < 4; ++r) rx[r] = xn[r] > 0.0f ? __builtin_amdgcn_rcpf(xn[r]) : (xn[r] != xn[r] ? xn[r] : 0.0f);
         const int y0 = 16 * blk + 4 * g;
-        const bool full = 16 * blk + 16 <= a.n;
+        // rows past the store (the last block) score NaN: never kept
+#pragma unroll
+        for (int r = 0; r < 4; ++r) rx[r] = y0 + r < a.n ? rx[r] : __builtin_nanf("");
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
 #pragma unroll
@@ -260,8 +266,8 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
               const int b = g0 + 16 * (NT * wq + t) + c;
               if (b < a.B && y < a.n) a.dbg[static_cast<int64_t>(b) * a.n + y] = acc[i][t][r] * a.rq[b] * rx[r];
             } else {
-              const float sv = __builtin_fmaxf(acc[i][t][r] * rx[r], kNanFloor);
-              if ((full || y < a.n) && sv > best_s[t]) {
+              const float sv = acc[i][t][r] * rx[r];
+              if (sv > best_s[t]) {
                 best_s[t] = sv;
                 best_i[t] = y;
               }
@@ -344,8 +350,6 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   // the in-scan NaN value, and a NaN query (every cosine NaN) the lowest
   // index among this lane's maps
   if constexpr (!DBG) {
-    const int y_first = 16 * (b_begin + wm) + 4 * g;
-    const bool first_ok = b_begin + wm < b_end && y_first < a.n;
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
       const float rq = a.rq[g0 + 16 * (NT * wq + t) + c];

@@ -163,14 +163,18 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   // Best map per query tile, ranked by dot * 1/|x[0:p]|: the query's own
   // factor 1/|q[0:p]| is positive (or 0 for a zero query, where every score
   // is 0) and does not change the order, so it is applied once at the end.
-  // A NaN score ranks as the lowest finite float, below every other score.
+  // A NaN score ranks below every other score: the list starts at the
+  // lane's first map with the lowest finite float, which only a greater
+  // score replaces (a NaN compares false).
   constexpr float kNanFloor = -3.40282347e38f;
+  const int y_first = 16 * (b_begin + wm) + 4 * g;
+  const bool first_ok = b_begin + wm < b_end && y_first < a.n;
   float best_s[kNT];
   int best_i[kNT];
 #pragma unroll
   for (int t = 0; t < kNT; ++t) {
-    best_s[t] = -__builtin_inff();
-    best_i[t] = -1;
+    best_s[t] = kNanFloor;
+    best_i[t] = first_ok ? y_first : -1;
   }
 
   if (nstages > 0) {
@@ -324,37 +328,43 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
         // values depend on) so that the compiler does not wait for every copy
         // still in flight.
         const int y0 = 16 * blk + 4 * g;
-        const bool full = 16 * blk + 16 <= a.n;
-        floatx4 xr[4];   // the rows of four tiles at a time
+        // (the last block of the store checks its rows against n; the others
+        // take a copy of the loop without the check)
+        auto score_block = [&](auto full_c) __attribute__((always_inline)) {
+          constexpr bool FULL = decltype(full_c)::value;
+          floatx4 xr[4];   // the rows of four tiles at a time
 #pragma unroll
-        for (int t = 0; t < kNT; ++t) {
-          if (t % 4 == 0) {
+          for (int t = 0; t < kNT; ++t) {
+            if (t % 4 == 0) {
 #pragma unroll
-            for (int h = 0; h < 4; ++h) {
-              const int row = (rows4[t / 4] >> (8 * h)) & 0xFF;
-              const uint32_t addr =
-                  static_cast<uint32_t>(reinterpret_cast<uintptr_t>(tb + row * 1024 + (wm + kGM * i) * 64 + 16 * g));
-              asm volatile("ds_read_b128 %0, %1" : "=v"(xr[h]) : "v"(addr));
+              for (int h = 0; h < 4; ++h) {
+                const int row = (rows4[t / 4] >> (8 * h)) & 0xFF;
+                const uint32_t addr =
+                    static_cast<uint32_t>(reinterpret_cast<uintptr_t>(tb + row * 1024 + (wm + kGM * i) * 64 + 16 * g));
+                asm volatile("ds_read_b128 %0, %1" : "=v"(xr[h]) : "v"(addr));
+              }
+              asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(xr[0]), "+v"(xr[1]), "+v"(xr[2]), "+v"(xr[3]));
             }
-            asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(xr[0]), "+v"(xr[1]), "+v"(xr[2]), "+v"(xr[3]));
-          }
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int y = y0 + r;
-            if constexpr (DBG) {
-              // the dense form writes every cosine and keeps no lists
-              const int p = pos_of(t);
-              const int b = a.perm[p];
-              if (b >= 0 && y < a.n) a.dbg[static_cast<int64_t>(b) * a.n + y] = acc[i][t][r] * a.rq[p] * xr[t % 4][r];
-            } else {
-              const float sv = __builtin_fmaxf(acc[i][t][r] * xr[t % 4][r], kNanFloor);
-              if ((full || y < a.n) && sv > best_s[t]) {
-                best_s[t] = sv;
-                best_i[t] = y;
+            for (int r = 0; r < 4; ++r) {
+              const int y = y0 + r;
+              if constexpr (DBG) {
+                // the dense form writes every cosine and keeps no lists
+                const int p = pos_of(t);
+                const int b = a.perm[p];
+                if (b >= 0 && y < a.n) a.dbg[static_cast<int64_t>(b) * a.n + y] = acc[i][t][r] * a.rq[p] * xr[t % 4][r];
+              } else {
+                const float sv = acc[i][t][r] * xr[t % 4][r];
+                if ((FULL || y < a.n) && sv > best_s[t]) {
+                  best_s[t] = sv;
+                  best_i[t] = y;
+                }
               }
             }
           }
-        }
+        };
+        if (16 * blk + 16 <= a.n) score_block(std::true_type{});
+        else score_block(std::false_type{});
         __builtin_amdgcn_sched_barrier(0);
       }
       // (the zeros are hidden from the compiler: known-zero accumulators
@@ -478,8 +488,6 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   // the cosine of each tile's best: its score times 1/|q[0:p]|; a NaN score
   // takes the in-scan NaN value, and a NaN query (every cosine NaN) the
   // lowest index among this lane's maps
-  const int y_first = 16 * (b_begin + wm) + 4 * g;
-  const bool first_ok = b_begin + wm < b_end && y_first < a.n;
 #pragma unroll
   for (int t = 0; t < kNT; ++t) {
     const float rq = a.rq[pos_of(t)];
