@@ -29,8 +29,9 @@
 // its register as soon as the MFMAs of its tile have read it).  Every stage
 // issues the same copies per wave (copies past the last stage use offsets
 // past every descriptor: zeros, no memory traffic), so "stage j+1 has
-// landed" is a fixed vmcnt bound.  The map norms of a slice are copied with
-// its first stage into one of two buffers.
+// landed" is a fixed vmcnt bound.  The map norms of a slice are copied into
+// one of two buffers by one more copy of wave 0 at the slice's first stage
+// (issued before that stage's tile copies, so the bound still holds).
 
 // Epilogue of a slice: lane (g, c) holds, for block i and query tile t, the
 // dots of maps 4g .. 4g+3 of the block with query c of the tile; the cosine
@@ -75,11 +76,11 @@ struct MmShape {
   static constexpr int TILES = SB + QG / 16;    // 1 KB tiles per stage
   static constexpr int MPW = SB / W;            // map tile copies per wave and stage
   static constexpr int QPW = QG / 16 / W;       // query tile copies per wave and stage
-  static constexpr int NI = MPW + QPW + 1;      // copies per wave and stage (tiles, norms)
+  static constexpr int NI = MPW + QPW;          // tile copies per wave and stage
   static constexpr int SLOT = TILES * 1024;
   static constexpr int NNORM = (SB * 16 * 4 + 1023) / 1024;   // 1 KB copies of one slice's map norms
   static constexpr int NSTRIDE = NNORM * 256;   // floats per norm buffer
-  static constexpr int LDS = NS * SLOT + 2 * NNORM * 1024 + 1024;   // + a scratch kilobyte
+  static constexpr int LDS = NS * SLOT + 2 * NNORM * 1024;
 };
 
 }  // namespace
@@ -90,13 +91,12 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   constexpr int W = S::W, GM = S::GM, NT = S::NT, NB = S::NB, QG = S::QG, SB = S::SB, NS = S::NS, NI = S::NI;
   constexpr int MPW = S::MPW, QPW = S::QPW;
   constexpr int SLOT = S::SLOT, NNORM = S::NNORM, NSTRIDE = S::NSTRIDE;
-  static_assert(SB % W == 0 && (QG / 16) % W == 0 && (NS - 1) * NI < 64, "copies per stage");
+  static_assert(SB % W == 0 && (QG / 16) % W == 0 && (NS - 1) * NI < 64 && NNORM <= W, "copies per stage");
   static_assert(S::LDS <= 160 * 1024, "LDS");
 
   extern __shared__ __align__(16) unsigned char smem[];
   unsigned char* ring = smem;                                    // [NS][SLOT]
   float* xnb = reinterpret_cast<float*>(smem + NS * SLOT);       // [2][NSTRIDE] map norms
-  float* junk = xnb + 2 * NSTRIDE;                               // [256] target of unneeded norm copies
   uint64_t* mbuf = reinterpret_cast<uint64_t*>(smem);            // after the loop: [GM][QG]
 
   const int tid = threadIdx.x;
@@ -180,12 +180,14 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     for (int i = 0; i < QPW; ++i) vqo[i] = static_cast<uint32_t>(w * QPW + i) * blk32 + static_cast<uint32_t>(lane * 16);
     const uint32_t vno = static_cast<uint32_t>((w * 256 + lane * 4) * 4);
 
-    // Copies of the copy position into the current stage's slot: the map
-    // tiles (blocks past the workgroup's range lie past the slice's
-    // descriptor), the query tiles, and a norm copy, which at a slice's
-    // first k-step brings the slice's map norms and otherwise reads past
-    // every descriptor into a scratch kilobyte.
+    // Copies of the copy position into the current stage's slot: at a
+    // slice's first k-step the slice's map norms (waves below NNORM), then
+    // the map tiles (blocks past the workgroup's range lie past the slice's
+    // descriptor) and the query tiles.
     auto issue = [&]() __attribute__((always_inline)) {
+      if (c_kofs == 0 && w < NNORM)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_norm, (lds_vp)(xnb + c_nb * NSTRIDE + w * 256), 16,
+                                                 static_cast<int>(static_cast<uint32_t>(c_blk0) * 64u + vno), 0, 0, 0);
       unsigned char* slot = ring + c_slot * SLOT;
       const __amdgpu_buffer_rsrc_t rs_slice = __builtin_amdgcn_make_buffer_rsrc(
           reinterpret_cast<char*>(c_xbase), static_cast<short>(0), static_cast<int>(c_xrec), kBufWord3);
@@ -197,12 +199,6 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
       for (int i = 0; i < QPW; ++i)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_q, (lds_vp)(slot + (SB + w * QPW + i) * 1024), 16,
                                                  static_cast<int>(vqo[i]), static_cast<int>(c_kofs), 0, 0);
-      const bool norm = c_kofs == 0 && w < NNORM;
-      const uint32_t noff = norm ? static_cast<uint32_t>(c_blk0) * 64u + vno : kOutside;
-      // (the destination as an offset from the LDS base: a select of two
-      // pointers would lose their address space)
-      const int ndst = norm ? NS * SLOT + (c_nb * NSTRIDE + w * 256) * 4 : NS * SLOT + 2 * NSTRIDE * 4;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_norm, (lds_vp)(smem + ndst), 16, static_cast<int>(noff), 0, 0, 0);
     };
     auto step_copy = [&]() __attribute__((always_inline)) {
       c_slot = c_slot == NS - 1 ? 0 : c_slot + 1;
