@@ -14,13 +14,14 @@
 // layer groups its own deepest query reaches (shallower queries of the tile
 // contribute their staged zeros).  The scan's 256 workgroups are shared
 // among the bands in proportion to the layer groups they walk (k_traj_prep
-// writes the shares), each band's workgroups covering even shares of the
-// store: with depths spread over the layers, the deep band's stages keep
-// most of their tiles active and the shallow band runs half as many stages
-// per map, whereas bands of mixed depths would each walk every layer with
-// half of their tiles idle.  Each band streams the planes of its own layers
-// (the shallow band's reads of the first layers are not shared with the
-// deep band's).
+// writes the shares): with depths spread over the layers, the deep band's
+// stages keep most of their tiles active and the shallow band runs half as
+// many stages per map, whereas bands of mixed depths would each walk every
+// layer with half of their tiles idle.  A band's workgroups take the
+// store's 16-block slices round-robin, so every band sweeps the store from
+// front to back at about the same pace; each band streams the planes of its
+// own layers, and the shallow band's reads of the first layers come close
+// enough in time to the deep band's to find them in the memory-side cache.
 //
 // Workgroup: 8 waves, two per SIMD, arranged 2 x 4 over (queries, maps).
 // Wave (wq, wm) holds 128 x 64 float32 accumulators: the band's local query
@@ -132,9 +133,17 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   const bool active = gbal != 0 && u - Pg < Rg;
   const int grp = active ? qg_u : 0;
   const int rr = active ? u - Pg : 0;
-  const int b_begin = active ? static_cast<int>((static_cast<int64_t>(rr) * a.n_blocks) / Rg) : 0;
-  const int b_end = active ? static_cast<int>((static_cast<int64_t>(rr + 1) * a.n_blocks) / Rg) : 0;
-  const int n_slices = (b_end - b_begin + kSB - 1) / kSB;
+  // The band's workgroups take the store's slices (kSB blocks from block 0)
+  // round-robin: workgroup rr the slices rr, rr + Rg, rr + 2 Rg, ...  So
+  // every band sweeps the store from front to back at the pace of its
+  // layer share, and the bands read the planes they have in common at
+  // about the same time (the later read finds them in the memory-side
+  // cache).
+  const int n_sl_all = (a.n_blocks + kSB - 1) / kSB;
+  const int n_slices = active && rr < n_sl_all ? (n_sl_all - rr + Rg - 1) / Rg : 0;
+  const int b_begin = rr * kSB;              // first block of the first slice
+  const int b_end = a.n_blocks;
+  const int sstep = Rg * kSB;                // blocks from one of its slices to the next
   // the band's layer groups, at least two stages per slice (the staged rows
   // of layer groups past every query of the band are zeros)
   int nlg = Ng < 1 ? 1 : Ng;
@@ -168,7 +177,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
   // score replaces (a NaN compares false).
   constexpr float kNanFloor = -3.40282347e38f;
   const int y_first = 16 * (b_begin + wm) + 4 * g;
-  const bool first_ok = b_begin + wm < b_end && y_first < a.n;
+  const bool first_ok = n_slices > 0 && b_begin + wm < b_end && y_first < a.n;
   float best_s[kNT];
   int best_i[kNT];
 #pragma unroll
@@ -282,7 +291,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
           c_base = reinterpret_cast<uint64_t>(a.planes);
           c_rec = rec_of(0);
           c_qoff = static_cast<uint32_t>(grp) * 16384u;
-          c_blk0 += kSB;
+          c_blk0 += sstep;
           c_tab ^= 1;
           set_slice(c_blk0);
         } else {
@@ -317,7 +326,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
 
     // Slice epilogue: scores of this wave's blocks of slice si, best per query.
     auto epilogue = [&](int si) __attribute__((always_inline)) {
-      const int blk_s = b_begin + si * kSB;
+      const int blk_s = b_begin + si * sstep;
       const unsigned char* tb = tab + (si & 1) * kTab;
 #pragma unroll
       for (int i = 0; i < kNB; ++i) {
