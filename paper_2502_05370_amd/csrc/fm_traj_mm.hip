@@ -324,56 +324,73 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
       return *reinterpret_cast<const u16x8*>(ring + slot * kSlot + (kSB + wq + 2 * t) * 1024 + lane * 16);
     };
 
-    // Slice epilogue: scores of this wave's blocks of slice si, best per query.
+    // Slice epilogue: scores of this wave's blocks of slice si, best per
+    // query, in 8 groups (block i, tiles 4h .. 4h+3).  Each group needs the
+    // inverse norms of its 4 tiles' rows (one 16-byte LDS read per tile); the
+    // reads of the next group are issued before the current group is scored,
+    // so that their latency hides behind its arithmetic.  The table was copied
+    // with the slice's last stage and the stage waits have covered it; the
+    // reads are written out (with waits the values depend on) so that the
+    // compiler does not wait for every copy still in flight.
     auto epilogue = [&](int si) __attribute__((always_inline)) {
       const int blk_s = b_begin + si * sstep;
       const unsigned char* tb = tab + (si & 1) * kTab;
+      auto read_rows = [&](floatx4 (&xr)[4], int grp) __attribute__((always_inline)) {
+        const int i = grp / 2;
 #pragma unroll
-      for (int i = 0; i < kNB; ++i) {
-        const int blk = blk_s + wm + kGM * i;
-        if (blk >= b_end) break;
-        // The table was copied with the slice's last stage and the stage
-        // waits have covered it; the reads are written out (with one wait the
-        // values depend on) so that the compiler does not wait for every copy
-        // still in flight.
-        const int y0 = 16 * blk + 4 * g;
-        // (the last block of the store checks its rows against n; the others
-        // take a copy of the loop without the check)
-        auto score_block = [&](auto full_c) __attribute__((always_inline)) {
-          constexpr bool FULL = decltype(full_c)::value;
-          floatx4 xr[4];   // the rows of four tiles at a time
+        for (int h = 0; h < 4; ++h) {
+          const int row = (rows4[grp % 2] >> (8 * h)) & 0xFF;
+          const uint32_t addr =
+              static_cast<uint32_t>(reinterpret_cast<uintptr_t>(tb + row * 1024 + (wm + kGM * i) * 64 + 16 * g));
+          asm volatile("ds_read_b128 %0, %1" : "=v"(xr[h]) : "v"(addr));
+        }
+      };
+      // (the last block of the store checks its rows against n; the others
+      // take a copy of the loop without the check)
+      auto score_group = [&](const floatx4 (&xr)[4], int grp, auto full_c) __attribute__((always_inline)) {
+        constexpr bool FULL = decltype(full_c)::value;
+        const int i = grp / 2;
+        const int y0 = 16 * (blk_s + wm + kGM * i) + 4 * g;
 #pragma unroll
-          for (int t = 0; t < kNT; ++t) {
-            if (t % 4 == 0) {
+        for (int tt = 0; tt < 4; ++tt) {
+          const int t = 4 * (grp % 2) + tt;
 #pragma unroll
-              for (int h = 0; h < 4; ++h) {
-                const int row = (rows4[t / 4] >> (8 * h)) & 0xFF;
-                const uint32_t addr =
-                    static_cast<uint32_t>(reinterpret_cast<uintptr_t>(tb + row * 1024 + (wm + kGM * i) * 64 + 16 * g));
-                asm volatile("ds_read_b128 %0, %1" : "=v"(xr[h]) : "v"(addr));
-              }
-              asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(xr[0]), "+v"(xr[1]), "+v"(xr[2]), "+v"(xr[3]));
-            }
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int y = y0 + r;
-              if constexpr (DBG) {
-                // the dense form writes every cosine and keeps no lists
-                const int p = pos_of(t);
-                const int b = a.perm[p];
-                if (b >= 0 && y < a.n) a.dbg[static_cast<int64_t>(b) * a.n + y] = acc[i][t][r] * a.rq[p] * xr[t % 4][r];
-              } else {
-                const float sv = acc[i][t][r] * xr[t % 4][r];
-                if ((FULL || y < a.n) && sv > best_s[t]) {
-                  best_s[t] = sv;
-                  best_i[t] = y;
-                }
+          for (int r = 0; r < 4; ++r) {
+            const int y = y0 + r;
+            if constexpr (DBG) {
+              // the dense form writes every cosine and keeps no lists
+              const int p = pos_of(t);
+              const int b = a.perm[p];
+              if (b >= 0 && y < a.n) a.dbg[static_cast<int64_t>(b) * a.n + y] = acc[i][t][r] * a.rq[p] * xr[tt][r];
+            } else {
+              const float sv = acc[i][t][r] * xr[tt][r];
+              if ((FULL || y < a.n) && sv > best_s[t]) {
+                best_s[t] = sv;
+                best_i[t] = y;
               }
             }
           }
-        };
-        if (16 * blk + 16 <= a.n) score_block(std::true_type{});
-        else score_block(std::false_type{});
+        }
+      };
+      floatx4 xa[4], xb[4];
+      read_rows(xa, 0);
+#pragma unroll
+      for (int grp = 0; grp < 2 * kNB; ++grp) {
+        floatx4 (&cur)[4] = grp % 2 == 0 ? xa : xb;
+        floatx4 (&nxt)[4] = grp % 2 == 0 ? xb : xa;
+        // blocks past the store (the store's last slice) are read but not
+        // scored: the table row stays within its kilobyte
+        if (grp + 1 < 2 * kNB) {
+          read_rows(nxt, grp + 1);
+          asm volatile("s_waitcnt lgkmcnt(4)" : "+v"(cur[0]), "+v"(cur[1]), "+v"(cur[2]), "+v"(cur[3]));
+        } else {
+          asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(cur[0]), "+v"(cur[1]), "+v"(cur[2]), "+v"(cur[3]));
+        }
+        const int blk = blk_s + wm + kGM * (grp / 2);
+        if (blk < b_end) {
+          if (16 * blk + 16 <= a.n) score_group(cur, grp, std::true_type{});
+          else score_group(cur, grp, std::false_type{});
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
       // (the zeros are hidden from the compiler: known-zero accumulators
