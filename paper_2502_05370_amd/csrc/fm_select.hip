@@ -56,15 +56,23 @@ __device__ __forceinline__ uint64_t ord_f64(double p) {
 }
 
 // The selection of row (b, l) of the batch from the query's matches idx_b /
-// score_b (k of them, best first); one wavefront, lane j = expert j.
-__device__ __forceinline__ void select_row(const SelArgs& a, int b, int l, const int32_t* idx_b, const float* score_b,
-                                           double* sorted, uint64_t* keys) {
+// score_b (k of them, best first) and its layer bounds lb[b] / le[b] (as
+// given; clamped here); one wavefront, lane j = expert j.
+__device__ __forceinline__ void select_row(const SelArgs& a, int b, int l, int lo, int hi, const int32_t* idx_b,
+                                           const float* score_b, double* sorted, uint64_t* keys) {
   const int lane = threadIdx.x % kWave;
   const int64_t row = static_cast<int64_t>(b) * a.L + l;
-  int lo = a.lb[b], hi = a.le[b];
   lo = lo < 0 ? 0 : (lo > a.L ? a.L : lo);
   hi = hi < 0 ? 0 : (hi > a.L ? a.L : hi);
   const int y0 = idx_b[0];
+
+  // 1. guiding probability of expert `lane`: its loads need only the
+  // matches, so they are issued before the row's bounds are looked at (a
+  // row outside them discards the value)
+  const GuideView gv{a.planes, a.plane_elems, a.n, a.row, a.dtype};
+  double p = 0.0;
+  if (lane < a.E && y0 >= 0 && y0 < a.n) p = guide_prob(gv, idx_b, score_b, a.k, a.blend, l, lane);
+
   bool live = l >= lo && l < hi && y0 >= 0;
   if (live && y0 >= a.n) {
     if (lane == 0) atomicOr(a.flags, static_cast<uint32_t>(FM_FLAG_INDEX_RANGE));
@@ -77,11 +85,6 @@ __device__ __forceinline__ void select_row(const SelArgs& a, int b, int l, const
     }
     return;
   }
-
-  // 1. guiding probability of expert `lane`
-  const GuideView gv{a.planes, a.plane_elems, a.n, a.row, a.dtype};
-  double p = 0.0;
-  if (lane < a.E) p = guide_prob(gv, idx_b, score_b, a.k, a.blend, l, lane);
 
   // 2. threshold
   double tau;
@@ -151,8 +154,8 @@ __global__ void __launch_bounds__(256) k_select(SelArgs a) {
   if (row >= static_cast<int64_t>(a.B) * a.L) return;
   const int b = static_cast<int>(row / a.L);
   const int l = static_cast<int>(row - static_cast<int64_t>(b) * a.L);
-  select_row(a, b, l, a.idx + static_cast<int64_t>(b) * a.k, a.score + static_cast<int64_t>(b) * a.k, sorted[wv],
-             keys[wv]);
+  select_row(a, b, l, a.lb[b], a.le[b], a.idx + static_cast<int64_t>(b) * a.k, a.score + static_cast<int64_t>(b) * a.k,
+             sorted[wv], keys[wv]);
 }
 
 // The cross-workgroup merge of a match call with the selection after it:
@@ -183,10 +186,28 @@ __global__ void __launch_bounds__(256) k_merge_select(SelArgs a, MergeArgs m) {
   if (row >= static_cast<int64_t>(a.B) * a.L) return;
   const int pos = static_cast<int>(row / a.L);
   const int l = static_cast<int>(row - static_cast<int64_t>(pos) * a.L);
+  // The loads that do not depend on the merge go first, side by side: the
+  // group's list count, the query index (then its layer bounds) and, for
+  // top-1 lists, the first kMaxPartials lists of the stride (those past the
+  // group's count are read but not merged).
   const int nr = m.rgrp != nullptr ? m.rgrp[pos / m.qg] : m.R;
+  const int b = m.perm != nullptr ? m.perm[pos] : pos;
+  const uint64_t* plist = m.partial + static_cast<int64_t>(pos) * m.R * KTOP;
   TopK<KTOP> t;
   t.clear();
-  for (int r = lane; r < nr; r += kWave) t.merge(m.partial + (static_cast<int64_t>(pos) * m.R + r) * KTOP);
+  int r0 = lane;
+  if constexpr (KTOP == 1) {
+    constexpr int kPre = kMaxPartials / kWave;
+    uint64_t pk[kPre];
+#pragma unroll
+    for (int it = 0; it < kPre; ++it) pk[it] = lane + it * kWave < m.R ? plist[lane + it * kWave] : 0ull;
+#pragma unroll
+    for (int it = 0; it < kPre; ++it)
+      if (lane + it * kWave < nr) t.merge(&pk[it]);
+    r0 = lane + kMaxPartials;
+  }
+  const int lo = a.lb[b], hi = a.le[b];
+  for (int r = r0; r < nr; r += kWave) t.merge(plist + static_cast<int64_t>(r) * KTOP);
 #pragma unroll
   for (int off = 1; off < kWave; off <<= 1) {
     uint64_t o[KTOP];
@@ -194,7 +215,6 @@ __global__ void __launch_bounds__(256) k_merge_select(SelArgs a, MergeArgs m) {
     for (int jj = 0; jj < KTOP; ++jj) o[jj] = shfl_xor_u64(t.v[jj], off);
     t.merge(o);
   }
-  const int b = m.perm != nullptr ? m.perm[pos] : pos;
   if (lane == 0) {
 #pragma unroll
     for (int jj = 0; jj < kMaxK; ++jj) {
@@ -208,9 +228,10 @@ __global__ void __launch_bounds__(256) k_merge_select(SelArgs a, MergeArgs m) {
       }
     }
   }
-  __builtin_amdgcn_s_waitcnt(0);
+  // (LDS only: the bounds' loads stay in flight)
+  wait_lgkm0();
   __builtin_amdgcn_wave_barrier();
-  select_row(a, b, l, midx[wv], mscore[wv], sorted[wv], keys[wv]);
+  select_row(a, b, l, lo, hi, midx[wv], mscore[wv], sorted[wv], keys[wv]);
 }
 
 // Misses of the prefetch sets (Section 3): one wavefront per (query, layer)
