@@ -185,9 +185,13 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     // the map tiles (blocks past the workgroup's range lie past the slice's
     // descriptor) and the query tiles.
     auto issue = [&]() __attribute__((always_inline)) {
-      if (c_kofs == 0 && w < NNORM)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_norm, (lds_vp)(xnb + c_nb * NSTRIDE + w * 256), 16,
-                                                 static_cast<int>(static_cast<uint32_t>(c_blk0) * 64u + vno), 0, 0, 0);
+      // (two uniform branches: the common path is one compare and branch)
+      if (__builtin_expect(c_kofs == 0, 0)) {
+        if (w < NNORM)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_norm, (lds_vp)(xnb + c_nb * NSTRIDE + w * 256), 16,
+                                                   static_cast<int>(static_cast<uint32_t>(c_blk0) * 64u + vno), 0, 0,
+                                                   0);
+      }
       unsigned char* slot = ring + c_slot * SLOT;
       const __amdgpu_buffer_rsrc_t rs_slice = __builtin_amdgcn_make_buffer_rsrc(
           reinterpret_cast<char*>(c_xbase), static_cast<short>(0), static_cast<int>(c_xrec), kBufWord3);
@@ -200,8 +204,13 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_q, (lds_vp)(slot + (SB + w * QPW + i) * 1024), 16,
                                                  static_cast<int>(vqo[i]), static_cast<int>(c_kofs), 0, 0);
     };
+    // the next ring slot (a mask when NS is a power of two)
+    auto next_slot = [&](int sl) __attribute__((always_inline)) {
+      if constexpr ((NS & (NS - 1)) == 0) return (sl + 1) & (NS - 1);
+      else return sl == NS - 1 ? 0 : sl + 1;
+    };
     auto step_copy = [&]() __attribute__((always_inline)) {
-      c_slot = c_slot == NS - 1 ? 0 : c_slot + 1;
+      c_slot = next_slot(c_slot);
       c_kofs += 1024u;
       if (__builtin_expect(--c_left == 0, 0)) {
         c_left = ksteps;
@@ -305,7 +314,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
       // stage j+1's copies have landed (this wave's, then everyone's)
       wait_vmcnt<(NS - 2) * NI>();
       raw_barrier();
-      const int sn = c_slot == NS - 1 ? 0 : c_slot + 1;
+      const int sn = next_slot(c_slot);
       issue();
       step_copy();
 #pragma unroll
