@@ -66,9 +66,9 @@ COUNTERS_KIB = {
     # workload: {kernel: (FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch}
     "mixtral_traj_n1k": {"k_traj_scan": (610.1, 10.9)},
     "qwen_traj_n50k_b64": {"k_traj_scan": (138797.4, 128.0)},
-    "semantic_d4096_n100k_b256": {"k_sem_mm": (417176.4, 512.0)},
+    "semantic_d4096_n100k_b256": {"k_sem_mm": (417145.2, 512.0)},
     "phi_traj_top4_n200k_b512": {"k_traj_scan": (333131.3, 1012.0)},
-    "qwen_mixed_bf16_n1m_b1024": {"k_sem_mm": (2308499.5, 512.0), "k_traj_mm": (2276146.0, 563.3)},
+    "qwen_mixed_bf16_n1m_b1024": {"k_sem_mm": (2657013.4, 512.0), "k_traj_mm": (2276903.6, 557.0)},
 }
 
 
