@@ -140,10 +140,11 @@ hipError_t launch_match_semantic(const StoreView& s, const void* q, int32_t B, i
 // Top-1 semantic scan (fm_sem_mm.hip): queries per group for a chunk of Bc
 // queries, and the scan itself on queries already staged by k_sem_prep
 // (b_pad = groups * queries per group); *R_out receives the partial lists per
-// query for k_finalize.
+// query for k_finalize.  The dense form (dbg set) writes every cosine, or
+// w_self * cosine + w_mix * mix[b][y] when mix is set.
 int sem_mm_group(int32_t Bc);
 hipError_t launch_sem_mm(const StoreView& s, int32_t Bc, int32_t b_pad, const Workspace& ws, float* dbg, int32_t* R_out,
-                         hipStream_t st);
+                         hipStream_t st, const float* mix = nullptr, double w_self = 1.0, double w_mix = 0.0);
 // Top-1 trajectory scan of bf16 stores (fm_traj_mm.hip): whether a chunk of
 // Bc queries takes it, its queries per group, and the scan itself on queries
 // staged by k_traj_prep in its tiled layout (b_pad = groups * queries per

@@ -472,8 +472,10 @@ hipError_t launch_match_semantic(const StoreView& s, const void* q, int32_t B, i
   // the dense-output form keeps top-1 lists (k = 1)
   const int tq_max = sem_tq_limit(dbg_scores != nullptr ? 1 : KTOP);
   const int n_blocks = (s.n + 15) / 16;
-  // top-1 searches run on the 128 x 128 wave-tile scan (fm_sem_mm.hip)
-  const bool mm = mix == nullptr && (dbg_scores != nullptr || KTOP == 1);
+  // top-1 searches and the dense form (which keeps no lists there) run on
+  // the 128 x 128 wave-tile scan (fm_sem_mm.hip); lists of 4 or 8, and a
+  // dense form that also returns matches, on the general scan
+  const bool mm = dbg_scores != nullptr ? idx_out == nullptr : KTOP == 1 && mix == nullptr;
   for (int b0 = 0; b0 < B; b0 += kChunkB) {
     const int Bc = (B - b0) < kChunkB ? (B - b0) : kChunkB;
     int TQ = 1;
@@ -497,7 +499,7 @@ hipError_t launch_match_semantic(const StoreView& s, const void* q, int32_t B, i
     if (mm) {
       int R = 1;
       err = launch_sem_mm(s, Bc, b_pad, ws, dbg_scores != nullptr ? dbg_scores + static_cast<int64_t>(b0) * s.n : nullptr,
-                          &R, st);
+                          &R, st, mix != nullptr ? mix + static_cast<int64_t>(b0) * s.n : nullptr, w_self, w_mix);
       if (err != hipSuccess) return err;
       if (idx_out != nullptr) {
         err = fuse != nullptr

@@ -57,6 +57,11 @@ struct SemMmArgs {
   const float* rq;       // [b_pad] 1/|q|
   uint64_t* partial;     // [b_pad][R]: one packed key per (query, workgroup of its group)
   float* dbg;            // optional dense scores [B][n]
+  // dense form only: the score written is w_self * cosine + w_mix * mix[b][y]
+  // (float64, rounded once) when mix is set
+  const float* mix;
+  double w_self, w_mix;
+  int32_t vec16;         // dense rows written (and mix read) 16 bytes at a time: n % 4 == 0, aligned buffers
   int32_t n, ksteps, B;
   int32_t n_qg;          // query groups
   int32_t R;             // workgroups per query group
@@ -263,19 +268,48 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
         for (int r = 0; r < 4; ++r) rx[r] = y0 + r < a.n ? rx[r] : __builtin_nanf("");
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
+          if constexpr (DBG) {
+            // The dense form writes every cosine (or its weighted sum with
+            // mix) and keeps no lists: the lane's 4 consecutive maps of its
+            // query as one 16-byte store where the row allows it.
+            const int b = g0 + 16 * (NT * wq + t) + c;
+            if (b < a.B) {
+              const int64_t o = static_cast<int64_t>(b) * a.n + y0;
+              const bool whole = a.vec16 != 0 && y0 + 3 < a.n;
+              const float rqb = a.rq[b];
+              floatx4 v;
+#pragma unroll
+              for (int r = 0; r < 4; ++r) v[r] = acc[i][t][r] * rqb * rx[r];
+              if (a.mix != nullptr) {
+                floatx4 mv = floatx4{0.f, 0.f, 0.f, 0.f};
+                if (whole) {
+                  mv = *reinterpret_cast<const floatx4*>(a.mix + o);
+                } else {
+#pragma unroll
+                  for (int r = 0; r < 4; ++r)
+                    if (y0 + r < a.n) mv[r] = a.mix[o + r];
+                }
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                  v[r] = static_cast<float>(__dadd_rn(__dmul_rn(a.w_self, static_cast<double>(v[r])),
+                                                      __dmul_rn(a.w_mix, static_cast<double>(mv[r]))));
+              }
+              if (whole) {
+                *reinterpret_cast<floatx4*>(a.dbg + o) = v;
+              } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                  if (y0 + r < a.n) a.dbg[o + r] = v[r];
+              }
+            }
+            continue;
+          }
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const int y = y0 + r;
-            if constexpr (DBG) {
-              // the dense form writes every cosine and keeps no lists
-              const int b = g0 + 16 * (NT * wq + t) + c;
-              if (b < a.B && y < a.n) a.dbg[static_cast<int64_t>(b) * a.n + y] = acc[i][t][r] * a.rq[b] * rx[r];
-            } else {
-              const float sv = acc[i][t][r] * rx[r];
-              if (sv > best_s[t]) {
-                best_s[t] = sv;
-                best_i[t] = y;
-              }
+            const float sv = acc[i][t][r] * rx[r];
+            if (sv > best_s[t]) {
+              best_s[t] = sv;
+              best_i[t] = y0 + r;
             }
           }
         }
@@ -349,12 +383,14 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     }
     wait_vmcnt<0>();   // the trailing copies
   }
+  // the dense form keeps no lists (it serves calls that return no matches)
+  if constexpr (DBG) return;
   __syncthreads();
 
   // the cosine of each tile's best: its score times 1/|q|; a NaN score takes
   // the in-scan NaN value, and a NaN query (every cosine NaN) the lowest
   // index among this lane's maps
-  if constexpr (!DBG) {
+  {
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
       const float rq = a.rq[g0 + 16 * (NT * wq + t) + c];
@@ -420,7 +456,7 @@ hipError_t sem_mm_launch(const SemMmArgs& a, hipStream_t st) {
 int sem_mm_group(int32_t Bc) { return Bc > 128 ? 256 : 128; }
 
 hipError_t launch_sem_mm(const StoreView& s, int32_t Bc, int32_t b_pad, const Workspace& ws, float* dbg, int32_t* R_out,
-                         hipStream_t st) {
+                         hipStream_t st, const float* mix, double w_self, double w_mix) {
   const int QG = sem_mm_group(Bc);
   const int n_qg = b_pad / QG;
   const int n_blocks = (s.n + 15) / 16;
@@ -437,6 +473,11 @@ hipError_t launch_sem_mm(const StoreView& s, int32_t Bc, int32_t b_pad, const Wo
   a.rq = ws.rq;
   a.partial = ws.partial;
   a.dbg = dbg;
+  a.mix = mix;
+  a.w_self = w_self;
+  a.w_mix = w_mix;
+  a.vec16 = s.n % 4 == 0 && reinterpret_cast<uintptr_t>(dbg) % 16 == 0 &&
+            reinterpret_cast<uintptr_t>(mix) % 16 == 0;
   a.n = s.n;
   a.ksteps = s.d_emb / 32;
   a.B = Bc;
