@@ -60,6 +60,7 @@ CASES = [
     (4, 3001, 3001, 33, 0),      # Phi-3.5 shape
     (3, 700, 700, 24, 32),       # d = L: semantic only
     (1, 517, 517, 100, 0),       # many replacements on a small store
+    (3, 1203, 1203, 40, 5),      # folded semantic + trajectory rows of a length not a multiple of 4
 ]
 
 
