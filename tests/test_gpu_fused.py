@@ -91,11 +91,23 @@ def test_fused_threshold_modes_and_blend(mode, blend):
 
 
 def test_fused_batch_beyond_one_launch():
+    """1030 semantic and 1100 trajectory queries: a launch of 1024 on the
+    top-1 scans, then the rest (6 semantic queries on the 128-query shape, 76
+    trajectory queries on the general scan); fused equals separate, and both
+    halves match the oracle on every row."""
     s = synth.spec(5).scaled(n=1500, B_traj=1100, B_sem=1030)
     print(f"config 5 n={s.n} B_traj={s.B_traj} B_sem={s.B_sem}", flush=True)
     a = synth.generate(s)
-    sep, fus, _ = _run_both(s, a)
+    sep, fus, flags = _run_both(s, a)
     _assert_identical(sep, fus)
+    assert flags == 0
+    idx, score, mask, count = fus
+    oi, os_ = oracle_match(s, a)
+    rep = compare_match(s, a, idx.astype(np.int64), score.astype(np.float64), oi, os_, np.arange(s.B))
+    assert not rep.failures, rep.failures[:5]
+    g = GpuResult(idx.astype(np.int64), score.astype(np.float64), mask.view(np.uint64), count, flags)
+    bad, _, _ = compare_select(s, a, g)
+    assert bad.size == 0, bad[:10]
 
 
 def test_fused_against_oracle():
