@@ -42,7 +42,9 @@ def _oracle_check(maps, dtype, q, depth, gi, gs):
     assert not rep.failures, rep.failures[:5]
 
 
-@pytest.mark.parametrize("cfg,n,B1,B2,k", [(2, 3001, 150, 37, 1), (5, 2500, 300, 20, 4), (4, 1800, 64, 9, 4)])
+# (the bf16 top-1 case of more than 128 queries runs the depth-band scan on the first call)
+@pytest.mark.parametrize("cfg,n,B1,B2,k", [(2, 3001, 150, 37, 1), (5, 2500, 300, 20, 4), (4, 1800, 64, 9, 4),
+                                           (5, 2500, 300, 20, 1)])
 def test_noalloc_matches_workspace_call(cfg, n, B1, B2, k):
     import paper_2502_05370_amd as fm
     print(f"noalloc cfg={cfg} n={n} B={B1},{B2} k={k}", flush=True)
