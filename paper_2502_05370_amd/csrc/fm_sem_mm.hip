@@ -4,10 +4,12 @@
 // (B x d) with the stored embeddings (n x d), both bf16, on
 // v_mfma_f32_16x16x32_bf16 (exact bf16 products, float32 accumulation),
 // followed by the cosine scaling and the best stored index per query.  This
-// kernel serves searches that keep one match per query; k_sem_scan
-// (fm_sem.hip) serves top-4/8 lists and the dense forms of the deduplicating
-// insert.  k_sem_prep stages the queries in the embedding tile layout and
-// writes 1/|q| before it runs; k_finalize merges its partial lists after.
+// kernel serves searches that keep one match per query and the dense form
+// (every cosine, or its weighted sum with a second dense matrix: the
+// deduplicating insert's RDY); k_sem_scan (fm_sem.hip) serves top-2..8
+// lists.  k_sem_prep stages the queries in the embedding tile layout and
+// writes 1/|q| before it runs; k_finalize (or k_merge_select, with the
+// selection) merges its partial lists after.
 //
 // Workgroup: 8 waves, two per SIMD (two waves on a SIMD let one issue its
 // LDS reads and copies while the other's MFMAs run), arranged GQ x GM over
@@ -34,13 +36,16 @@
 // (issued before that stage's tile copies, so the bound still holds).
 
 // Epilogue of a slice: lane (g, c) holds, for block i and query tile t, the
-// dots of maps 4g .. 4g+3 of the block with query c of the tile; the cosine
-// is (dot * 1/|q|) * 1/|x| and the lane keeps the best (score, index) per
-// query tile.  Maps are visited in increasing index order and only a
-// strictly better score replaces the kept one, so equal scores keep the
-// lower index; a NaN score is taken as -2 (below every cosine, above "no
-// match").  The lists are merged over lane groups and waves and stored as
-// the workgroup's partial list (one packed key per query).
+// dots of maps 4g .. 4g+3 of the block with query c of the tile.  The top-1
+// form ranks them by dot * 1/|x| (the query's factor 1/|q| is positive, or
+// 0 for a zero query, and is applied once after the scan) and keeps the best
+// (score, index) per query tile: maps are visited in increasing index order
+// and only a strictly greater score replaces the kept one, so equal scores
+// keep the lower index, and a NaN score ranks below every other.  The lists
+// are merged over lane groups and waves and stored as the workgroup's
+// partial list (one packed key per query).  The dense form writes the
+// cosines (dot * 1/|q| * 1/|x|) instead, a lane's 4 maps of a row as one
+// 16-byte store where the row allows it, and keeps no lists.
 #include <type_traits>
 
 #include "fm_device.h"

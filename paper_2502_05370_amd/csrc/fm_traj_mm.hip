@@ -43,10 +43,13 @@
 //
 // Epilogue of a slice: lane (g, c) holds, for block i and query tile t, the
 // dots of maps 4g .. 4g+3 of the block with query c of the tile; the cosine
-// is (dot * 1/|q[0:p]|) * 1/|x[y][0:p]| at the query's depth p, and the lane
-// keeps the best (score, index) per query tile (strictly better replaces,
-// maps in increasing order: equal scores keep the lower index; a NaN score
-// is taken as -2).  The lists are merged over lane groups and waves and
+// at the query's depth p is (dot * 1/|q[0:p]|) * 1/|x[y][0:p]|.  The lane
+// ranks by dot * 1/|x[y][0:p]| (1/|q[0:p]| is positive, or 0, and is applied
+// once after the scan) and keeps the best (score, index) per query tile: a
+// lane visits its maps in increasing index order (its slices in order, the
+// blocks of a slice in order) and only a strictly greater score replaces the
+// kept one, so equal scores keep the lower index, and a NaN score ranks
+// below every other.  The lists are merged over lane groups and waves and
 // stored as the workgroup's partial list.
 #include "fm_device.h"
 #include "fm_internal.h"
